@@ -1,0 +1,273 @@
+/*
+ * specblock.h - C ABI of the SpecBlock block-expansion hot path on MI355X.
+ *
+ * SpecBlock (Block-Iterative Speculative Decoding with Dynamic Tree
+ * Drafting) alternates drafting and verification.  One verifier iteration
+ * (Alg. 2 of the paper) is:
+ *
+ *   for m = 1..M:  sb_draft_block_expand   one batched drafter forward over
+ *                                          every start x K block positions,
+ *                                          then psi, rank head, branching and
+ *                                          sibling attachment (Sec. 3.1-3.2)
+ *   sb_tree_verify                         one target forward over the tree
+ *   sb_accept                              greedy acceptance walk
+ *   sb_commit                              keep the accepted K/V, advance
+ *
+ * Conventions
+ * - Every pointer inside the structs below is a DEVICE pointer unless its
+ *   comment says "host".  The caller allocates and owns all memory: the
+ *   library never allocates or frees device memory.  Its scratch lives in one
+ *   caller-provided workspace of sb_workspace_bytes() bytes.
+ * - Floating-point storage type "elem" is float32 when cfg.dtype == SB_F32
+ *   and bfloat16 (uint16_t bits, round-to-nearest-even) when SB_BF16.
+ *   Accumulation, norms, softmax, residual stream, logits, h^(L) and all
+ *   outputs typed float are float32.
+ * - Matrices are row-major [out_features][in_features] (y = W x).
+ * - Calls are asynchronous: they enqueue work on `stream` (a hipStream_t;
+ *   NULL = the default stream) and return.  Outputs are valid once the
+ *   stream has reached that point.  No call synchronises with the host.
+ * - Every call returns SB_OK (0) or an error code; arguments are validated on
+ *   the host before anything is enqueued, so an error leaves device state
+ *   untouched.  sb_last_error() describes the last failure of a context.
+ * - One context may be used by one host thread / stream at a time.
+ */
+#ifndef SPECBLOCK_H
+#define SPECBLOCK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum sb_status {
+  SB_OK = 0,
+  SB_EINVAL = 1,   /* NULL or misaligned pointer, bad argument value        */
+  SB_ESHAPE = 2,   /* dimensions inconsistent with the configuration       */
+  SB_EBUDGET = 3,  /* tree, row, page or workspace capacity exceeded        */
+  SB_EDTYPE = 4,   /* unknown storage type                                  */
+  SB_EHIP = 5,     /* a HIP runtime call failed (message in sb_last_error)  */
+  SB_ESTATE = 6    /* call out of order (e.g. before sb_bind)               */
+};
+
+enum sb_dtype { SB_F32 = 0, SB_BF16 = 1 };
+
+#define SB_TOPK 10     /* top-k kept per drafter row (psi uses the top 10) */
+#define SB_PSI_DIM 15  /* distribution summary psi (App. B)                */
+#define SB_N_BUCKETS 4 /* rank-head buckets b0..b3 (Sec. 3.2)              */
+
+/* Llama-style decoder dimensions (the drafter layers match the target's
+ * per-layer architecture, Sec. 3.1). */
+typedef struct sb_model_dims {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ff, vocab;
+  float rope_theta, norm_eps;
+} sb_model_dims;
+
+typedef struct sb_config {
+  sb_model_dims target;     /* drafter width/heads/vocab equal the target's  */
+  int32_t drafter_layers;   /* L of the drafter                               */
+  int32_t tap_layers[3];    /* target layers giving h_low, h_mid, h_top (Eq.1)*/
+  int32_t K;                /* block depth: positions per drafter forward     */
+  int32_t M;                /* block expansions per verifier iteration        */
+  int32_t B_max;            /* next-block starts per sequence                 */
+  int32_t budget;           /* tree nodes per sequence, root included (<=512) */
+  int32_t branch_map[4];    /* bucket -> branching b(.) (App. A.4), 0..10     */
+  int32_t dtype;            /* enum sb_dtype                                  */
+  int32_t max_seqs;         /* sequences per call                             */
+  int32_t page_size;        /* K/V page size in tokens; must be 16            */
+  int32_t max_pages;        /* page-table row length (pages per sequence)     */
+  int32_t prefill_chunk;    /* rows per prefill step (multiple of 16)         */
+} sb_config;
+
+/* One decoder layer.  elem matrices; float gains. */
+typedef struct sb_layer_weights {
+  const void* attn_norm;  /* float [d]                                        */
+  const void* w_qkv;      /* elem [(H + 2 Hkv) hd][d]: Q heads, K heads, V heads */
+  const void* w_o;        /* elem [d][H hd]                                   */
+  const void* mlp_norm;   /* float [d]                                        */
+  const void* w_gate_up;  /* elem [2F][d]: gate rows 0..F-1, then up rows     */
+  const void* w_down;     /* elem [d][F]                                      */
+  const void* w_shift;    /* drafter: elem [d][2d] layer-wise shift (Eq. 3),
+                             applied to [h_k, h_{k-1}]; target: NULL          */
+} sb_layer_weights;
+
+typedef struct sb_target_weights {
+  const void* embed;                /* elem [V][d] (shared with the drafter)  */
+  const sb_layer_weights* layers;   /* host array [n_layers]                  */
+  const void* final_norm;           /* float [d]                              */
+  const void* lm_head;              /* elem [V][d]                            */
+} sb_target_weights;
+
+typedef struct sb_drafter_weights {
+  const void* w_cond;      /* elem [d][3d]: c = W_cond [h_low,h_mid,h_top] (Eq.1)*/
+  const void* norm_c;      /* float [d] RMSNorm gain of c       (Eq. 2)       */
+  const void* norm_e;      /* float [d] RMSNorm gain of embed(x)              */
+  const void* norm_q;      /* float [d] RMSNorm gain of q_k                   */
+  const void* pos_query;   /* elem [K][d] learnable position queries q_1..q_K */
+  const void* w_fuse;      /* elem [d][3d]: W_fuse [norm c, norm e, norm q]   */
+  const sb_layer_weights* layers;   /* host array [drafter_layers]            */
+  const void* final_norm;  /* float [d]                                       */
+  const void* lm_head;     /* elem [V][d]                                     */
+  const void* rank_w;      /* float [4][d + 15]: rank head over [h^(L), psi]  */
+  const void* rank_b;      /* float [4]                                       */
+} sb_drafter_weights;
+
+/* Paged K/V cache of one model.  Entry i of sequence s lives in page
+ * page_table[s][i / 16] at slot i % 16.  Per layer and page:
+ *   k: [n_kv_heads][16][head_dim]   elem
+ *   v: [n_kv_heads][head_dim][16]   elem (transposed within the page)
+ * i.e. k is [n_layers][n_pages][n_kv_heads][16][head_dim].
+ * The target cache holds positions 0..T-1 (entry i = position i); the
+ * drafter cache holds positions 1..T (entry i = position i + 1). */
+typedef struct sb_kv {
+  void* k;
+  void* v;
+  const int32_t* page_table;   /* [max_seqs][max_pages]                      */
+  int32_t n_layers;            /* host value                                 */
+  int32_t n_pages;             /* host value: pages in the pool              */
+} sb_kv;
+
+/* Per-sequence decoding state. */
+typedef struct sb_seqs {
+  int32_t n_seqs;      /* host value, <= cfg.max_seqs                        */
+  int32_t* root;       /* [S] root token x_T (last verified, not yet run)    */
+  int32_t* T;          /* [S] root position = committed entries per cache    */
+  float* cond_taps;    /* [S][3][d] target taps at position T-1 (Eq. 1 input)*/
+} sb_seqs;
+
+/* Draft tree of the current iteration plus the drafter rows that built it.
+ * Node 0 is the root.  Nodes are topologically ordered (parent < child).
+ * Row r of sequence s is the r-th drafter row produced in this iteration;
+ * the rows of one start are consecutive, k = 1..K. */
+typedef struct sb_tree {
+  int32_t* n_nodes;     /* [S]                                               */
+  int32_t* token;       /* [S][budget]                                       */
+  int32_t* parent;      /* [S][budget] (-1 for the root)                     */
+  int32_t* depth;       /* [S][budget]                                       */
+  int32_t* row;         /* [S][budget] row that proposed the node (-1 root)  */
+  int32_t* rank;        /* [S][budget] 1-based rank in that row (0 root)     */
+  float* logp;          /* [S][budget] log p of the token in its row         */
+  float* cum_logp;      /* [S][budget] sum of logp along the root path       */
+  uint32_t* anc;        /* [S][budget][ceil(budget/32)] ancestor-or-self bits*/
+  int32_t* n_rows;      /* [S]                                               */
+  int32_t* row_block;   /* [S][row_cap] expansion index m (1-based)          */
+  int32_t* row_start;   /* [S][row_cap] start node of the row's block        */
+  int32_t* row_k;       /* [S][row_cap] block position k (1-based)           */
+  int32_t* row_pos;     /* [S][row_cap] RoPE position                        */
+  uint32_t* row_vis;    /* [S][row_cap][ceil(row_cap/32)] visible rows       */
+  float* h_last;        /* [S][row_cap][d] cached h^(L) (pre final norm)     */
+  int32_t* n_starts;    /* [S] starts of the next block                      */
+  int32_t* starts;      /* [S][B_max] their node ids                         */
+} sb_tree;
+/* row_cap = K + (M - 1) * B_max * K, see sb_row_capacity(). */
+
+/* Per-row results of one block expansion, indexed [S][row_cap]. */
+typedef struct sb_draft_out {
+  int32_t* topk_id;     /* [S][row_cap][10] ids, larger logit first, ties to
+                           the smaller id                                    */
+  float* topk_logit;    /* [S][row_cap][10]                                  */
+  float* lse;           /* [S][row_cap] log-sum-exp of the row's logits      */
+  float* psi;           /* [S][row_cap][15] App. B summary                   */
+  int32_t* bucket;      /* [S][row_cap] rank-head bucket 0..3 (Eq. 4)        */
+  int32_t* branch;      /* [S][row_cap] b(bucket)                            */
+  float* logits;        /* optional (NULL = not written): [call_cap][V] in
+                           call-row order                                    */
+  int32_t* call_seq;    /* [call_cap] sequence of call row i                 */
+  int32_t* call_row;    /* [call_cap] its row id within the sequence         */
+  int32_t* n_call;      /* [1] rows in this call                             */
+} sb_draft_out;
+/* call_cap = max_seqs * B_max * K (block 1: max_seqs * K). */
+
+typedef struct sb_verify_out {
+  int32_t* argmax;      /* [S][budget] target greedy token per node          */
+  float* taps;          /* [S][budget][3][d] target taps per node            */
+  float* logits;        /* optional: [max_seqs * budget][V] in call-row order
+                           (sequence-major, node order)                      */
+} sb_verify_out;
+
+typedef struct sb_accept_out {
+  int32_t* path;        /* [S][M K] accepted node ids, root excluded         */
+  int32_t* n_accepted;  /* [S] a: accepted draft tokens                      */
+  int32_t* bonus;       /* [S] target token after the last accepted node     */
+} sb_accept_out;
+
+typedef struct sb_ctx sb_ctx;
+
+/* Capacities derived from a configuration. */
+int32_t sb_row_capacity(const sb_config* cfg);
+/* Workspace bytes sb_bind needs for this configuration (0 if invalid). */
+size_t sb_workspace_bytes(const sb_config* cfg);
+
+/* Validate cfg (SB_EINVAL / SB_ESHAPE / SB_EDTYPE) and create a context. */
+int sb_create(const sb_config* cfg, sb_ctx** out);
+void sb_destroy(sb_ctx* ctx);
+/* Thread-unsafe description of the last error of ctx (or of the last failed
+ * sb_create when ctx is NULL). */
+const char* sb_last_error(const sb_ctx* ctx);
+
+/* Attach weights and workspace.  Tables are copied (host arrays may be
+ * freed); the device memory they point to must outlive the context. */
+int sb_bind(sb_ctx* ctx, const sb_target_weights* target,
+            const sb_drafter_weights* drafter, void* workspace,
+            size_t workspace_bytes);
+
+/* Prefill (setup, not the hot path): causal target forward over each prompt
+ * x_0..x_{n_s-1}, writing target K/V entries 0..n_s-1, the root x_{n_s}
+ * (greedy), T = n_s and cond_taps; then drafter catch-up rows for positions
+ * 1..n_s (a K = 1 block started at position p-1 conditioned on the target
+ * taps of position p-2, zero for p = 1), written to the drafter cache.
+ * prompt: device [n_seqs][ld_prompt]; lens: HOST [n_seqs], 1..max_pages*16-1.
+ * The caller fills both page tables. */
+int sb_prefill(sb_ctx* ctx, const sb_seqs* seqs, const int32_t* prompt,
+               int32_t ld_prompt, const int32_t* lens, sb_kv* target_kv,
+               sb_kv* draft_kv, void* stream);
+
+/* One block expansion (Sec. 3.1-3.2; Alg. 2 inner loop).
+ * block_index 1 starts a new iteration: it resets `tree` to the root
+ * (seqs->root at seqs->T) and conditions the single start on
+ * c = W_cond [cond_taps] (Eq. 1).  block_index m > 1 expands the starts the
+ * previous call left in tree->starts, each conditioned on the cached h^(L)
+ * of the row that proposed it (bypassing W_cond).  Each start runs K rows:
+ * h0_k = W_fuse [norm c, norm embed(token), norm q_k] (Eq. 2), then per
+ * drafter layer the shift W_shift [h_k, h_{k-1}] (Eq. 3, h_0 := h_1) and the
+ * decoder layer, attending to the drafter prefix (entries 1..T), the rows of
+ * earlier blocks on the start's path and its own rows <= k.  Then the final
+ * norm, LM head, top-10 / log-sum-exp / entropy, psi, the rank head
+ * (argmax, ties to the lower bucket), b = branch_map[bucket], sibling
+ * attachment in (k, start, rank) order within the budget, and the next
+ * starts (chain ends first, then rank>=2 siblings of b1/b2 rows by cum_logp,
+ * at most B_max, none when the tree is full).
+ * K must equal cfg.K; block_index 1..cfg.M. */
+int sb_draft_block_expand(sb_ctx* ctx, int32_t block_index, int32_t K,
+                          const sb_seqs* seqs, const sb_kv* draft_kv,
+                          sb_tree* tree, sb_draft_out* out, void* stream);
+
+/* Tree verification (Alg. 2): one target forward over every tree node, node
+ * n at position T + depth(n), attending to target entries 0..T-1 and its
+ * ancestors-or-self.  Writes the node K/V to the library's tree scratch
+ * (kept for sb_commit), argmax (ties to the smaller id) and taps. */
+int sb_tree_verify(sb_ctx* ctx, const sb_seqs* seqs, const sb_tree* tree,
+                   const sb_kv* target_kv, sb_verify_out* out, void* stream);
+
+/* Greedy acceptance: from the root follow the child whose token equals the
+ * target's argmax at the current node (lowest node id on duplicates); the
+ * argmax at the last accepted node is the bonus.  tau = n_accepted + 1. */
+int sb_accept(sb_ctx* ctx, int32_t n_seqs, const sb_tree* tree,
+              const int32_t* argmax, sb_accept_out* out, void* stream);
+
+/* Commit: target K/V of the root and accepted nodes (from the last
+ * sb_tree_verify) become entries T..T+a; drafter entries for positions
+ * T+1..T+a reuse the K/V of the rows that proposed the accepted nodes, and
+ * position T+a+1 reuses the row continuing the last accepted node, or, when
+ * the tree has none, a catch-up row (K = 1 block started at the last
+ * accepted node, conditioned on the taps of its parent).  Then root = bonus,
+ * T += a + 1, cond_taps = taps of the last accepted node. */
+int sb_commit(sb_ctx* ctx, sb_seqs* seqs, const sb_tree* tree,
+              const sb_verify_out* verify, const sb_accept_out* acc,
+              sb_kv* target_kv, sb_kv* draft_kv, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPECBLOCK_H */

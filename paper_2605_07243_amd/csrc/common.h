@@ -1,0 +1,127 @@
+// Device-side helpers shared by the gfx950 kernels: bf16 storage,
+// MFMA fragments, wavefront reductions.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define SB_WAVE 64
+#define SB_TOPK_K 10   // top-k kept per drafter row
+#define SB_PSI 15      // distribution summary size
+#define SB_MAX_ANC_WORDS 16  // ancestor bit words (budget <= 512)
+
+typedef uint16_t bf16_t;
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t b) {
+  return __uint_as_float(((uint32_t)b) << 16);
+}
+
+// float -> bfloat16, round to nearest, ties to even (finite inputs).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+// Storage-type traits: elem is float (SB_F32) or bf16_t (SB_BF16).
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  __device__ __forceinline__ static float load(const float* p) { return *p; }
+  __device__ __forceinline__ static float to_f32(float v) { return v; }
+  __device__ __forceinline__ static float from_f32(float v) { return v; }
+};
+template <> struct Elem<bf16_t> {
+  __device__ __forceinline__ static float load(const bf16_t* p) {
+    return bf16_to_f32(*p);
+  }
+  __device__ __forceinline__ static float to_f32(bf16_t v) {
+    return bf16_to_f32(v);
+  }
+  __device__ __forceinline__ static bf16_t from_f32(float v) {
+    return f32_to_bf16(v);
+  }
+};
+
+// An MFMA operand fragment: 8 consecutive elements along the contraction
+// dimension held by one lane (16 B for bf16, 32 B for float).
+template <typename T> struct Frag8;
+template <> struct Frag8<bf16_t> {
+  uint4 v;
+  __device__ __forceinline__ void load(const bf16_t* p) {
+    v = *reinterpret_cast<const uint4*>(p);
+  }
+  __device__ __forceinline__ void zero() { v = make_uint4(0, 0, 0, 0); }
+};
+template <> struct Frag8<float> {
+  float4 a, b;
+  __device__ __forceinline__ void load(const float* p) {
+    a = reinterpret_cast<const float4*>(p)[0];
+    b = reinterpret_cast<const float4*>(p)[1];
+  }
+  __device__ __forceinline__ void zero() {
+    a = make_float4(0.f, 0.f, 0.f, 0.f);
+    b = a;
+  }
+};
+
+// acc[16x16] += A[16 x 32] * B[32 x 16] where lane l holds row (l % 16) of A
+// and column (l % 16) of B, each with the 8 contraction indices of lane
+// group l / 16.  Output: lane l holds acc[4 * (l / 16) + r][l % 16].
+// bf16: one v_mfma_f32_16x16x32_bf16; float: eight v_mfma_f32_16x16x4_f32
+// (element j of the fragment is contraction step j).
+__device__ __forceinline__ f32x4_t mma_16x16x32(const Frag8<bf16_t>& a,
+                                                const Frag8<bf16_t>& b,
+                                                f32x4_t acc) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+      __builtin_bit_cast(bf16x8_t, a.v), __builtin_bit_cast(bf16x8_t, b.v),
+      acc, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4_t mma_16x16x32(const Frag8<float>& a,
+                                                const Frag8<float>& b,
+                                                f32x4_t acc) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.a.x, b.a.x, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.a.y, b.a.y, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.a.z, b.a.z, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.a.w, b.a.w, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.b.x, b.b.x, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.b.y, b.b.y, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.b.z, b.b.z, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.b.w, b.b.w, acc, 0, 0, 0);
+  return acc;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, SB_WAVE);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, SB_WAVE));
+  return v;
+}
+__device__ __forceinline__ int wave_sum_i(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, SB_WAVE);
+  return v;
+}
+
+// Sum over a block of `nthreads` threads (multiple of 64); `red` holds
+// nthreads/64 floats of LDS.  Every thread gets the total.
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int nw = blockDim.x >> 6;
+  v = wave_sum(v);
+  __syncthreads();
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  float t = 0.f;
+  for (int i = 0; i < nw; ++i) t += red[i];
+  return t;
+}
+
+// Larger (value, smaller id) first.
+__device__ __forceinline__ bool better(float v, int id, float bv, int bid) {
+  return v > bv || (v == bv && id < bid);
+}

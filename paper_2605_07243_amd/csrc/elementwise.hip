@@ -1,0 +1,295 @@
+// Row-wise kernels around the projections: embedding gather, RMSNorm,
+// residual add of split-K partials, RoPE + K/V segment write, SwiGLU, the
+// layer-wise shift operand and the drafter input fusion operand.
+// One workgroup per call row; the active row count is read on the device.
+#include "common.h"
+#include "kernels.h"
+
+namespace sb {
+
+template <typename T>
+__global__ __launch_bounds__(256) void embed_kernel(const int* __restrict__ n,
+                                                    const int* __restrict__ tok,
+                                                    const T* __restrict__ E,
+                                                    int d, float* __restrict__ x) {
+  const int i = blockIdx.x;
+  if (i >= *n) return;
+  const T* e = E + (size_t)tok[i] * d;
+  float* xr = x + (size_t)i * d;
+  for (int j = threadIdx.x; j < d; j += blockDim.x) xr[j] = Elem<T>::to_f32(e[j]);
+}
+
+template <typename T>
+void launch_embed(const CallPlan& p, const T* embed, int d, float* x,
+                  hipStream_t st) {
+  embed_kernel<T><<<p.cap, 256, 0, st>>>(p.n, p.token, embed, d, x);
+}
+
+// Writes rmsnorm(src) * g as T into out (d elements).
+template <typename T>
+__device__ __forceinline__ void norm_row(const float* __restrict__ src, int d,
+                                         const float* __restrict__ g, float eps,
+                                         T* __restrict__ out, float* red) {
+  float ss = 0.f;
+  for (int j = threadIdx.x; j < d; j += blockDim.x) {
+    const float v = src[j];
+    ss += v * v;
+  }
+  ss = block_sum(ss, red);
+  const float r = 1.0f / sqrtf(ss / (float)d + eps);
+  for (int j = threadIdx.x; j < d; j += blockDim.x)
+    out[j] = Elem<T>::from_f32(src[j] * r * g[j]);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(
+    const float* __restrict__ x, const int* __restrict__ n, int d,
+    const float* __restrict__ g, float eps, T* __restrict__ out, int ldo) {
+  __shared__ float red[4];
+  const int i = blockIdx.x;
+  if (i >= *n) return;
+  norm_row<T>(x + (size_t)i * d, d, g, eps, out + (size_t)i * ldo, red);
+}
+
+template <typename T>
+void launch_rmsnorm(const float* x, const int* n, int cap, int d,
+                    const float* g, float eps, T* out, int ldo,
+                    hipStream_t st) {
+  rmsnorm_kernel<T><<<cap, 256, 0, st>>>(x, n, d, g, eps, out, ldo);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void residual_kernel(
+    float* __restrict__ x, const float* __restrict__ P, int ks,
+    size_t part_stride, const int* __restrict__ n, int d, int accumulate,
+    const float* __restrict__ g, float eps, T* __restrict__ out, int ldo,
+    float* __restrict__ taps, int tap_mask, const int* __restrict__ out_row) {
+  __shared__ float red[4];
+  const int i = blockIdx.x;
+  if (i >= *n) return;
+  float* xr = x + (size_t)i * d;
+  float* tr = nullptr;
+  if (taps != nullptr && tap_mask != 0 && out_row[i] >= 0)
+    tr = taps + (size_t)out_row[i] * 3 * d;
+  for (int j = threadIdx.x; j < d; j += blockDim.x) {
+    float v = accumulate ? xr[j] : 0.f;
+    for (int s = 0; s < ks; ++s) v += P[s * part_stride + (size_t)i * d + j];
+    xr[j] = v;
+    if (tr) {
+      if (tap_mask & 1) tr[j] = v;
+      if (tap_mask & 2) tr[d + j] = v;
+      if (tap_mask & 4) tr[2 * d + j] = v;
+    }
+  }
+  if (g != nullptr) {
+    __syncthreads();
+    norm_row<T>(xr, d, g, eps, out + (size_t)i * ldo, red);
+  }
+}
+
+template <typename T>
+void launch_residual(float* x, const float* P, int ks, size_t part_stride,
+                     const int* n, int cap, int d, bool accumulate,
+                     const float* g, float eps, T* out, int ldo, float* taps,
+                     int tap_mask, const int* out_row, hipStream_t st) {
+  residual_kernel<T><<<cap, 256, 0, st>>>(x, P, ks, part_stride, n, d,
+                                          accumulate ? 1 : 0, g, eps, out, ldo,
+                                          taps, tap_mask, out_row);
+}
+
+// RoPE (rotate-half pairs (j, j + hd/2), angle pos * theta^(-2j/hd)) on the
+// Q and K heads of the summed QKV projection; Q -> q [cap][H][hd], K and V ->
+// the row's slot of its sequence's segment pages.
+template <typename T>
+__global__ __launch_bounds__(256) void qkv_post_kernel(
+    const float* __restrict__ P, int ks, size_t part_stride, CallPlan p, int H,
+    int Hkv, int hd, float theta, T* __restrict__ q, T* __restrict__ seg_k,
+    T* __restrict__ seg_v, int seg_pages) {
+  __shared__ float cs[128], sn[128];
+  const int i = blockIdx.x;
+  if (i >= *p.n) return;
+  const int half = hd >> 1;
+  const int ncol = (H + 2 * Hkv) * hd;
+  const double pos = (double)p.pos[i];
+  for (int j = threadIdx.x; j < half; j += blockDim.x) {
+    const double inv = exp(-((double)(2 * j) / (double)hd) * log((double)theta));
+    double s, c;
+    sincos(pos * inv, &s, &c);
+    cs[j] = (float)c;
+    sn[j] = (float)s;
+  }
+  __syncthreads();
+  const float* Pr = P + (size_t)i * ncol;
+  auto col = [&](int c) {
+    float v = 0.f;
+    for (int s = 0; s < ks; ++s) v += Pr[s * part_stride + c];
+    return v;
+  };
+  const int seq = p.seq[i], slot = p.slot[i];
+  const int page = slot >> 4, sl = slot & 15;
+  const size_t page_base = (size_t)seq * seg_pages + page;
+  // rotated pairs of the H query heads and Hkv key heads
+  for (int idx = threadIdx.x; idx < (H + Hkv) * half; idx += blockDim.x) {
+    const int head = idx / half, j = idx % half;
+    const float a = col(head * hd + j), b = col(head * hd + j + half);
+    const float ra = a * cs[j] - b * sn[j];
+    const float rb = b * cs[j] + a * sn[j];
+    if (head < H) {
+      T* qr = q + ((size_t)i * H + head) * hd;
+      qr[j] = Elem<T>::from_f32(ra);
+      qr[j + half] = Elem<T>::from_f32(rb);
+    } else {
+      const int kh = head - H;
+      T* kr = seg_k + ((page_base * Hkv + kh) * 16 + sl) * hd;
+      kr[j] = Elem<T>::from_f32(ra);
+      kr[j + half] = Elem<T>::from_f32(rb);
+    }
+  }
+  for (int idx = threadIdx.x; idx < Hkv * hd; idx += blockDim.x) {
+    const int kh = idx / hd, j = idx % hd;
+    const float v = col((H + Hkv) * hd + idx);
+    seg_v[((page_base * Hkv + kh) * hd + j) * 16 + sl] = Elem<T>::from_f32(v);
+  }
+}
+
+template <typename T>
+void launch_qkv_post(const float* P, int ks, size_t part_stride,
+                     const CallPlan& p, int H, int Hkv, int hd, float theta,
+                     T* q, void* seg_k, void* seg_v, int seg_pages,
+                     hipStream_t st) {
+  qkv_post_kernel<T><<<p.cap, 256, 0, st>>>(P, ks, part_stride, p, H, Hkv, hd,
+                                            theta, q, (T*)seg_k, (T*)seg_v,
+                                            seg_pages);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void swiglu_kernel(
+    const float* __restrict__ P, int ks, size_t part_stride,
+    const int* __restrict__ n, int F, T* __restrict__ out) {
+  const int i = blockIdx.x;
+  if (i >= *n) return;
+  const float* Pr = P + (size_t)i * 2 * F;
+  for (int j = threadIdx.x; j < F; j += blockDim.x) {
+    float gt = 0.f, up = 0.f;
+    for (int s = 0; s < ks; ++s) {
+      gt += Pr[s * part_stride + j];
+      up += Pr[s * part_stride + F + j];
+    }
+    const float si = gt / (1.0f + expf(-gt));
+    out[(size_t)i * F + j] = Elem<T>::from_f32(si * up);
+  }
+}
+
+template <typename T>
+void launch_swiglu(const float* P, int ks, size_t part_stride, const int* n,
+                   int cap, int F, T* out, hipStream_t st) {
+  swiglu_kernel<T><<<cap, 256, 0, st>>>(P, ks, part_stride, n, F, out);
+}
+
+// Layer-wise shift operand (Eq. 3): [h_k, h_{k-1}] with h_0 := h_1.
+template <typename T>
+__global__ __launch_bounds__(256) void shift_prep_kernel(
+    const float* __restrict__ h, const int* __restrict__ n,
+    const int* __restrict__ pred, int d, T* __restrict__ out) {
+  const int i = blockIdx.x;
+  if (i >= *n) return;
+  const float* a = h + (size_t)i * d;
+  const float* b = h + (size_t)pred[i] * d;
+  T* o = out + (size_t)i * 2 * d;
+  for (int j = threadIdx.x; j < d; j += blockDim.x) {
+    o[j] = Elem<T>::from_f32(a[j]);
+    o[d + j] = Elem<T>::from_f32(b[j]);
+  }
+}
+
+template <typename T>
+void launch_shift_prep(const float* h, const CallPlan& p, int d, T* out,
+                       hipStream_t st) {
+  shift_prep_kernel<T><<<p.cap, 256, 0, st>>>(h, p.n, p.pred, d, out);
+}
+
+// Drafter input fusion operand (Eq. 2): [norm_c(c), norm_e(embed(x)),
+// norm_q(q_k)], each an RMSNorm with its own gain.
+template <typename T>
+__global__ __launch_bounds__(256) void fuse_prep_kernel(
+    const float* __restrict__ cond, CallPlan p, const T* __restrict__ E,
+    const T* __restrict__ Q, const float* __restrict__ gc,
+    const float* __restrict__ ge, const float* __restrict__ gq, float eps,
+    int d, T* __restrict__ out) {
+  __shared__ float red[4];
+  __shared__ float buf[8192];
+  const int i = blockIdx.x;
+  if (i >= *p.n) return;
+  T* o = out + (size_t)i * 3 * d;
+  const int c = p.cond[i];
+  if (c >= 0) {
+    norm_row<T>(cond + (size_t)c * d, d, gc, eps, o, red);
+  } else {
+    for (int j = threadIdx.x; j < d; j += blockDim.x)
+      o[j] = Elem<T>::from_f32(0.f);
+  }
+  __syncthreads();
+  const T* e = E + (size_t)p.token[i] * d;
+  for (int j = threadIdx.x; j < d; j += blockDim.x) buf[j] = Elem<T>::to_f32(e[j]);
+  __syncthreads();
+  norm_row<T>(buf, d, ge, eps, o + d, red);
+  __syncthreads();
+  const T* qk = Q + (size_t)(p.k[i] - 1) * d;
+  for (int j = threadIdx.x; j < d; j += blockDim.x) buf[j] = Elem<T>::to_f32(qk[j]);
+  __syncthreads();
+  norm_row<T>(buf, d, gq, eps, o + 2 * d, red);
+}
+
+template <typename T>
+void launch_fuse_prep(const float* cond, const CallPlan& p, const T* embed,
+                      const T* pos_query, const float* gc, const float* ge,
+                      const float* gq, float eps, int d, T* out,
+                      hipStream_t st) {
+  fuse_prep_kernel<T><<<p.cap, 256, 0, st>>>(cond, p, embed, pos_query, gc, ge,
+                                             gq, eps, d, out);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void rows_to_elem_kernel(
+    const float* __restrict__ src, const int* __restrict__ idx,
+    const int* __restrict__ n, int w, T* __restrict__ out) {
+  const int i = blockIdx.x;
+  if (i >= *n) return;
+  const float* s = src + (size_t)(idx ? idx[i] : i) * w;
+  for (int j = threadIdx.x; j < w; j += blockDim.x)
+    out[(size_t)i * w + j] = Elem<T>::from_f32(s[j]);
+}
+
+template <typename T>
+void launch_rows_to_elem(const float* src, const int* idx, const int* n,
+                         int cap, int w, T* out, hipStream_t st) {
+  rows_to_elem_kernel<T><<<cap, 256, 0, st>>>(src, idx, n, w, out);
+}
+
+#define SB_INST(T)                                                             \
+  template void launch_embed<T>(const CallPlan&, const T*, int, float*,        \
+                                hipStream_t);                                  \
+  template void launch_rmsnorm<T>(const float*, const int*, int, int,          \
+                                  const float*, float, T*, int, hipStream_t);  \
+  template void launch_residual<T>(float*, const float*, int, size_t,          \
+                                   const int*, int, int, bool, const float*,   \
+                                   float, T*, int, float*, int, const int*,    \
+                                   hipStream_t);                               \
+  template void launch_qkv_post<T>(const float*, int, size_t, const CallPlan&, \
+                                   int, int, int, float, T*, void*, void*,     \
+                                   int, hipStream_t);                          \
+  template void launch_swiglu<T>(const float*, int, size_t, const int*, int,   \
+                                 int, T*, hipStream_t);                        \
+  template void launch_shift_prep<T>(const float*, const CallPlan&, int, T*,   \
+                                     hipStream_t);                             \
+  template void launch_fuse_prep<T>(const float*, const CallPlan&, const T*,   \
+                                    const T*, const float*, const float*,      \
+                                    const float*, float, int, T*,              \
+                                    hipStream_t);                              \
+  template void launch_rows_to_elem<T>(const float*, const int*, const int*,   \
+                                       int, int, T*, hipStream_t);
+SB_INST(float)
+SB_INST(bf16_t)
+#undef SB_INST
+
+}  // namespace sb

@@ -1,0 +1,793 @@
+// C-ABI entry points: argument validation, workspace layout and the launch
+// sequence of each call.  All device work is enqueued on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "specblock.h"
+
+using namespace sb;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int kVocabRec10 = 2 * SB_TOPK + 3;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* b) : base(static_cast<char*>(b)) {}
+  template <typename P>
+  P* take(size_t bytes) {
+    P* p = base ? reinterpret_cast<P*>(base + off) : nullptr;
+    off = align_up(off + bytes);
+    return p;
+  }
+};
+
+struct Dims {
+  int S, d, H, Hkv, hd, F, V, L, LD, qkv_n, es;
+  int K, M, B_max, budget, row_cap, rw, bw, vis_words, R_cap, chunk;
+  int tpages, dpages, n_chunks, ksplit_cap, n_split;
+  size_t part_elems;
+};
+
+Dims derive(const sb_config& c) {
+  Dims D{};
+  D.S = c.max_seqs;
+  D.d = c.target.d_model;
+  D.H = c.target.n_heads;
+  D.Hkv = c.target.n_kv_heads;
+  D.hd = c.target.head_dim;
+  D.F = c.target.d_ff;
+  D.V = c.target.vocab;
+  D.L = c.target.n_layers;
+  D.LD = c.drafter_layers;
+  D.qkv_n = (D.H + 2 * D.Hkv) * D.hd;
+  D.es = c.dtype == SB_BF16 ? 2 : 4;
+  D.K = c.K;
+  D.M = c.M;
+  D.B_max = c.B_max;
+  D.budget = c.budget;
+  D.row_cap = c.K + (c.M - 1) * c.B_max * c.K;
+  D.rw = ceil_div(D.row_cap, 32);
+  D.bw = ceil_div(D.budget, 32);
+  D.chunk = c.prefill_chunk;
+  D.vis_words = ceil_div(std::max(std::max(D.budget, D.row_cap), D.chunk), 32);
+  D.R_cap = std::max(std::max(D.S * D.budget, D.S * D.B_max * D.K),
+                     std::max(D.chunk, D.S));
+  D.tpages = ceil_div(std::max(D.budget, D.chunk), 16);
+  D.dpages = ceil_div(std::max(D.row_cap, D.chunk), 16);
+  D.n_chunks = std::max(1, std::min(64, D.V / 2048));
+  D.ksplit_cap = 8;
+  D.n_split = 16;
+  // partial-sum buffer: the largest ks * N over the projections
+  size_t mx = 0;
+  auto upd = [&](int N, int Kd) {
+    mx = std::max(mx, (size_t)gemm_ksplit(N, Kd, D.ksplit_cap) * N);
+  };
+  upd(D.qkv_n, D.d);
+  upd(D.d, D.H * D.hd);
+  upd(2 * D.F, D.d);
+  upd(D.d, D.F);
+  upd(D.d, 3 * D.d);
+  upd(D.d, 2 * D.d);
+  D.part_elems = mx * D.R_cap;
+  return D;
+}
+
+}  // namespace
+
+struct sb_ctx {
+  sb_config cfg{};
+  Dims D{};
+  std::string err;
+  bool bound = false;
+  sb_target_weights tw{};
+  std::vector<sb_layer_weights> tl;
+  sb_drafter_weights dw{};
+  std::vector<sb_layer_weights> dl;
+  // workspace
+  float* x = nullptr;
+  void* A = nullptr;
+  float* P = nullptr;
+  void* q = nullptr;
+  float* o_part = nullptr;
+  float* ml = nullptr;
+  float* logits = nullptr;
+  float* vpart = nullptr;
+  float* cond_buf = nullptr;
+  float* taps_pf = nullptr;
+  int* taps_idx = nullptr;
+  int* n_aux = nullptr;
+  int* one = nullptr;
+  int* root_arg = nullptr;
+  int* blk_row0 = nullptr;
+  int* blk_nst = nullptr;
+  CommitInfo ci{};
+  CallPlan plan{};
+  CallPlan fb{};
+  void* tseg_k = nullptr;
+  void* tseg_v = nullptr;
+  void* dseg_k = nullptr;
+  void* dseg_v = nullptr;
+  int* zero = nullptr;
+};
+
+static thread_local std::string g_create_err;
+
+static int fail(sb_ctx* c, int code, const std::string& msg) {
+  if (c)
+    c->err = msg;
+  else
+    g_create_err = msg;
+  return code;
+}
+
+static size_t layout(const Dims& D, void* base, sb_ctx* c) {
+  Carver cv(base);
+  const size_t R = D.R_cap;
+  const int es = D.es;
+  const int widest = std::max(std::max(3 * D.d, D.F), std::max(D.H * D.hd, 2 * D.d));
+  float* x = cv.take<float>(R * D.d * 4);
+  void* A = cv.take<char>(R * widest * es);
+  float* P = cv.take<float>(D.part_elems * 4);
+  void* q = cv.take<char>(R * D.H * D.hd * es);
+  float* o_part = cv.take<float>((size_t)D.n_split * R * D.H * D.hd * 4);
+  float* ml = cv.take<float>((size_t)D.n_split * R * D.H * 2 * 4);
+  float* logits = cv.take<float>(R * D.V * 4);
+  float* vpart = cv.take<float>(R * D.n_chunks * kVocabRec10 * 4);
+  float* cond_buf = cv.take<float>(R * D.d * 4);
+  float* taps_pf = cv.take<float>((size_t)(D.chunk + 1) * 3 * D.d * 4);
+  int* taps_idx = cv.take<int>(R * 4);
+  int* n_aux = cv.take<int>(4);
+  int* one = cv.take<int>(4);
+  int* root_arg = cv.take<int>(4);
+  int* zero = cv.take<int>(4);
+  int* blk_row0 = cv.take<int>(D.S * 4);
+  int* blk_nst = cv.take<int>(D.S * 4);
+  CommitInfo ci{cv.take<int>(D.S * 4), cv.take<int>(D.S * 4),
+                cv.take<int>(D.S * 4), cv.take<int>(D.S * 4)};
+  auto make_plan = [&](int cap) {
+    CallPlan p{};
+    p.n = cv.take<int>(4);
+    p.seq = cv.take<int>(cap * 4);
+    p.slot = cv.take<int>(cap * 4);
+    p.pos = cv.take<int>(cap * 4);
+    p.token = cv.take<int>(cap * 4);
+    p.vis = cv.take<uint32_t>((size_t)cap * D.vis_words * 4);
+    p.k = cv.take<int>(cap * 4);
+    p.pred = cv.take<int>(cap * 4);
+    p.cond = cv.take<int>(cap * 4);
+    p.seq_off = cv.take<int>((D.S + 1) * 4);
+    p.prefix_len = cv.take<int>(D.S * 4);
+    p.seg_len = cv.take<int>(D.S * 4);
+    p.out_row = cv.take<int>(cap * 4);
+    p.kv_dst = cv.take<int>(cap * 4);
+    p.cap = cap;
+    p.vis_words = D.vis_words;
+    p.n_seqs = D.S;
+    return p;
+  };
+  CallPlan plan = make_plan(D.R_cap);
+  CallPlan fb = make_plan(D.S);
+  const size_t page = (size_t)D.Hkv * 16 * D.hd * es;
+  void* tseg_k = cv.take<char>((size_t)D.L * D.S * D.tpages * page);
+  void* tseg_v = cv.take<char>((size_t)D.L * D.S * D.tpages * page);
+  void* dseg_k = cv.take<char>((size_t)D.LD * D.S * D.dpages * page);
+  void* dseg_v = cv.take<char>((size_t)D.LD * D.S * D.dpages * page);
+  if (c) {
+    c->x = x;
+    c->A = A;
+    c->P = P;
+    c->q = q;
+    c->o_part = o_part;
+    c->ml = ml;
+    c->logits = logits;
+    c->vpart = vpart;
+    c->cond_buf = cond_buf;
+    c->taps_pf = taps_pf;
+    c->taps_idx = taps_idx;
+    c->n_aux = n_aux;
+    c->one = one;
+    c->root_arg = root_arg;
+    c->zero = zero;
+    c->blk_row0 = blk_row0;
+    c->blk_nst = blk_nst;
+    c->ci = ci;
+    c->plan = plan;
+    c->fb = fb;
+    c->tseg_k = tseg_k;
+    c->tseg_v = tseg_v;
+    c->dseg_k = dseg_k;
+    c->dseg_v = dseg_v;
+  }
+  return cv.off;
+}
+
+static int validate_cfg(const sb_config* c, std::string& msg) {
+  if (!c) {
+    msg = "cfg is NULL";
+    return SB_EINVAL;
+  }
+  if (c->dtype != SB_F32 && c->dtype != SB_BF16) {
+    msg = "dtype must be SB_F32 or SB_BF16";
+    return SB_EDTYPE;
+  }
+  const sb_model_dims& t = c->target;
+  if (t.n_layers < 1 || t.d_model < 32 || t.n_heads < 1 || t.n_kv_heads < 1 ||
+      t.head_dim < 1 || t.d_ff < 32 || t.vocab < SB_TOPK) {
+    msg = "model dimensions out of range";
+    return SB_ESHAPE;
+  }
+  if (t.head_dim != 64 && t.head_dim != 128) {
+    msg = "head_dim must be 64 or 128";
+    return SB_ESHAPE;
+  }
+  if (t.n_heads % t.n_kv_heads || t.n_heads > 64) {
+    msg = "n_heads must be a multiple of n_kv_heads and <= 64";
+    return SB_ESHAPE;
+  }
+  if (t.d_model % 32 || t.d_ff % 32 || t.d_model > 8192 ||
+      (t.n_heads * t.head_dim) % 32) {
+    msg = "d_model and d_ff must be multiples of 32 (d_model <= 8192)";
+    return SB_ESHAPE;
+  }
+  if (t.vocab % 16 || ((t.n_heads + 2 * t.n_kv_heads) * t.head_dim) % 16) {
+    msg = "vocab and the QKV width must be multiples of 16";
+    return SB_ESHAPE;
+  }
+  if (!(t.rope_theta > 0.f) || !(t.norm_eps > 0.f)) {
+    msg = "rope_theta and norm_eps must be positive";
+    return SB_EINVAL;
+  }
+  if (c->drafter_layers < 1) {
+    msg = "drafter_layers must be >= 1";
+    return SB_ESHAPE;
+  }
+  for (int i = 0; i < 3; ++i)
+    if (c->tap_layers[i] < 0 || c->tap_layers[i] >= t.n_layers) {
+      msg = "tap layer out of range";
+      return SB_ESHAPE;
+    }
+  if (c->K < 1 || c->M < 1 || c->B_max < 1 || c->B_max > 64) {
+    msg = "need K >= 1, M >= 1, 1 <= B_max <= 64";
+    return SB_EINVAL;
+  }
+  if (c->budget < 1 || c->budget > 512) {
+    msg = "budget must be in 1..512";
+    return SB_EBUDGET;
+  }
+  const int row_cap = c->K + (c->M - 1) * c->B_max * c->K;
+  if (row_cap > 512 || c->M * c->K > 512) {
+    msg = "K + (M-1) B_max K must be <= 512";
+    return SB_EBUDGET;
+  }
+  for (int i = 0; i < 4; ++i)
+    if (c->branch_map[i] < 0 || c->branch_map[i] > SB_TOPK) {
+      msg = "branch_map entries must be in 0..10";
+      return SB_EINVAL;
+    }
+  if (c->max_seqs < 1 || c->max_seqs > SB_MAX_SEQS) {
+    msg = "max_seqs must be in 1..64";
+    return SB_EINVAL;
+  }
+  if (c->page_size != 16) {
+    msg = "page_size must be 16";
+    return SB_ESHAPE;
+  }
+  if (c->max_pages < 1) {
+    msg = "max_pages must be >= 1";
+    return SB_EINVAL;
+  }
+  if (c->prefill_chunk < 16 || c->prefill_chunk % 16 || c->prefill_chunk > 512) {
+    msg = "prefill_chunk must be a multiple of 16 in 16..512";
+    return SB_EINVAL;
+  }
+  return SB_OK;
+}
+
+extern "C" {
+
+int32_t sb_row_capacity(const sb_config* cfg) {
+  std::string m;
+  if (validate_cfg(cfg, m) != SB_OK) return 0;
+  return cfg->K + (cfg->M - 1) * cfg->B_max * cfg->K;
+}
+
+size_t sb_workspace_bytes(const sb_config* cfg) {
+  std::string m;
+  if (validate_cfg(cfg, m) != SB_OK) return 0;
+  return layout(derive(*cfg), nullptr, nullptr);
+}
+
+int sb_create(const sb_config* cfg, sb_ctx** out) {
+  if (!out) return fail(nullptr, SB_EINVAL, "out is NULL");
+  *out = nullptr;
+  std::string m;
+  const int rc = validate_cfg(cfg, m);
+  if (rc != SB_OK) return fail(nullptr, rc, m);
+  sb_ctx* c = new sb_ctx();
+  c->cfg = *cfg;
+  c->D = derive(*cfg);
+  *out = c;
+  return SB_OK;
+}
+
+void sb_destroy(sb_ctx* ctx) { delete ctx; }
+
+const char* sb_last_error(const sb_ctx* ctx) {
+  return ctx ? ctx->err.c_str() : g_create_err.c_str();
+}
+
+static bool bad_ptr(const void* p, size_t align) {
+  return p == nullptr || (reinterpret_cast<uintptr_t>(p) % align) != 0;
+}
+
+static int check_layer(sb_ctx* c, const sb_layer_weights& l, bool drafter) {
+  if (bad_ptr(l.attn_norm, 4) || bad_ptr(l.mlp_norm, 4) || bad_ptr(l.w_qkv, 16) ||
+      bad_ptr(l.w_o, 16) || bad_ptr(l.w_gate_up, 16) || bad_ptr(l.w_down, 16))
+    return fail(c, SB_EINVAL, "layer weight pointer NULL or misaligned");
+  if (drafter && bad_ptr(l.w_shift, 16))
+    return fail(c, SB_EINVAL, "drafter layer needs w_shift");
+  return SB_OK;
+}
+
+int sb_bind(sb_ctx* c, const sb_target_weights* tw,
+            const sb_drafter_weights* dw, void* ws, size_t ws_bytes) {
+  if (!c) return SB_EINVAL;
+  if (!tw || !dw || !tw->layers || !dw->layers)
+    return fail(c, SB_EINVAL, "weight tables must not be NULL");
+  if (bad_ptr(tw->embed, 16) || bad_ptr(tw->final_norm, 4) ||
+      bad_ptr(tw->lm_head, 16))
+    return fail(c, SB_EINVAL, "target weight pointer NULL or misaligned");
+  if (bad_ptr(dw->w_cond, 16) || bad_ptr(dw->norm_c, 4) ||
+      bad_ptr(dw->norm_e, 4) || bad_ptr(dw->norm_q, 4) ||
+      bad_ptr(dw->pos_query, 16) || bad_ptr(dw->w_fuse, 16) ||
+      bad_ptr(dw->final_norm, 4) || bad_ptr(dw->lm_head, 16) ||
+      bad_ptr(dw->rank_w, 4) || bad_ptr(dw->rank_b, 4))
+    return fail(c, SB_EINVAL, "drafter weight pointer NULL or misaligned");
+  for (int i = 0; i < c->D.L; ++i) {
+    const int rc = check_layer(c, tw->layers[i], false);
+    if (rc) return rc;
+  }
+  for (int i = 0; i < c->D.LD; ++i) {
+    const int rc = check_layer(c, dw->layers[i], true);
+    if (rc) return rc;
+  }
+  const size_t need = layout(c->D, nullptr, nullptr);
+  if (bad_ptr(ws, kAlign)) return fail(c, SB_EINVAL, "workspace NULL or not 256-byte aligned");
+  if (ws_bytes < need)
+    return fail(c, SB_EBUDGET, "workspace too small: need " + std::to_string(need));
+  c->tw = *tw;
+  c->tl.assign(tw->layers, tw->layers + c->D.L);
+  c->tw.layers = c->tl.data();
+  c->dw = *dw;
+  c->dl.assign(dw->layers, dw->layers + c->D.LD);
+  c->dw.layers = c->dl.data();
+  layout(c->D, ws, c);
+  c->bound = true;
+  return SB_OK;
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// forward passes
+
+namespace {
+
+hipStream_t S_(void* s) { return static_cast<hipStream_t>(s); }
+
+int hip_check(sb_ctx* c, const char* where) {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess)
+    return fail(c, SB_EHIP, std::string(where) + ": " + hipGetErrorString(e));
+  return SB_OK;
+}
+
+template <typename T>
+int gemm(sb_ctx* c, const void* X, int ldx, const void* W, int N, int K,
+         const int* n, int m_cap, hipStream_t st) {
+  const int ks = gemm_ksplit(N, K, c->D.ksplit_cap);
+  return launch_gemm_xwt<T>(static_cast<const T*>(X), ldx,
+                            static_cast<const T*>(W), N, K, c->P,
+                            (size_t)c->D.R_cap * N, n, m_cap, ks, st);
+}
+
+struct Prefix {
+  const sb_kv* kv;
+  void* seg_k;   // all layers
+  void* seg_v;
+  int seg_pages;
+};
+
+// Decoder layer body after the attention-norm operand is in A: QKV + RoPE,
+// tree attention, O + residual, MLP + residual.  next_g: gain of the norm
+// that follows (written into A), or nullptr.
+template <typename T>
+void layer_body(sb_ctx* c, const sb_layer_weights& lw, int layer,
+                const CallPlan& p, const Prefix& pf, int rows_per_seq,
+                const float* next_g, float* taps, int tap_mask,
+                hipStream_t st) {
+  const Dims& D = c->D;
+  const float eps = c->cfg.target.norm_eps;
+  const int R = p.cap;
+  const size_t page = (size_t)D.Hkv * 16 * D.hd;
+  T* A = static_cast<T*>(c->A);
+  int ks = gemm<T>(c, A, D.d, lw.w_qkv, D.qkv_n, D.d, p.n, R, st);
+  T* segk = static_cast<T*>(pf.seg_k) + (size_t)layer * D.S * pf.seg_pages * page;
+  T* segv = static_cast<T*>(pf.seg_v) + (size_t)layer * D.S * pf.seg_pages * page;
+  launch_qkv_post<T>(c->P, ks, (size_t)D.R_cap * D.qkv_n, p, D.H, D.Hkv, D.hd,
+                     c->cfg.target.rope_theta, static_cast<T*>(c->q), segk,
+                     segv, pf.seg_pages, st);
+  KVView kv{};
+  kv.k = static_cast<const T*>(pf.kv->k) + (size_t)layer * pf.kv->n_pages * page;
+  kv.v = static_cast<const T*>(pf.kv->v) + (size_t)layer * pf.kv->n_pages * page;
+  kv.page_table = pf.kv->page_table;
+  kv.max_pages = c->cfg.max_pages;
+  kv.n_pages = pf.kv->n_pages;
+  kv.seg_k = segk;
+  kv.seg_v = segv;
+  kv.seg_pages = pf.seg_pages;
+  const int max_prefix = c->cfg.max_pages * 16;
+  const int n_split = std::max(1, std::min(D.n_split, ceil_div(max_prefix, 256)));
+  launch_tree_attn<T>(static_cast<const T*>(c->q), p, kv, rows_per_seq, D.H,
+                      D.Hkv, D.hd, n_split, max_prefix, c->o_part, c->ml, A,
+                      st);
+  ks = gemm<T>(c, A, D.H * D.hd, lw.w_o, D.d, D.H * D.hd, p.n, R, st);
+  launch_residual<T>(c->x, c->P, ks, (size_t)D.R_cap * D.d, p.n, R, D.d, true,
+                     lw.mlp_norm ? static_cast<const float*>(lw.mlp_norm) : nullptr,
+                     eps, A, D.d, nullptr, 0, nullptr, st);
+  ks = gemm<T>(c, A, D.d, lw.w_gate_up, 2 * D.F, D.d, p.n, R, st);
+  launch_swiglu<T>(c->P, ks, (size_t)D.R_cap * 2 * D.F, p.n, R, D.F, A, st);
+  ks = gemm<T>(c, A, D.F, lw.w_down, D.d, D.F, p.n, R, st);
+  launch_residual<T>(c->x, c->P, ks, (size_t)D.R_cap * D.d, p.n, R, D.d, true,
+                     next_g, eps, A, D.d, taps, tap_mask, p.out_row, st);
+}
+
+// Target forward over the plan's rows.  Ends with rmsnorm(final) in A when
+// lm_rows is true (the LM head is run by the caller).
+template <typename T>
+void target_forward(sb_ctx* c, const CallPlan& p, const Prefix& pf,
+                    int rows_per_seq, float* taps, hipStream_t st) {
+  const Dims& D = c->D;
+  const float eps = c->cfg.target.norm_eps;
+  launch_embed<T>(p, static_cast<const T*>(c->tw.embed), D.d, c->x, st);
+  launch_rmsnorm<T>(c->x, p.n, p.cap, D.d,
+                    static_cast<const float*>(c->tw.layers[0].attn_norm), eps,
+                    static_cast<T*>(c->A), D.d, st);
+  for (int l = 0; l < D.L; ++l) {
+    const float* next_g = l + 1 < D.L
+                              ? static_cast<const float*>(c->tw.layers[l + 1].attn_norm)
+                              : static_cast<const float*>(c->tw.final_norm);
+    int mask = 0;
+    for (int j = 0; j < 3; ++j)
+      if (c->cfg.tap_layers[j] == l) mask |= 1 << j;
+    layer_body<T>(c, c->tw.layers[l], l, p, pf, rows_per_seq, next_g,
+                  taps, mask, st);
+  }
+}
+
+// Drafter forward over the plan's rows (Eq. 2, Eq. 3, decoder layers).
+// cond_base: rows of conditions indexed by p.cond.  Leaves the final
+// residual h^(L) in x and, when lm is true, rmsnorm(final) in A.
+template <typename T>
+void drafter_forward(sb_ctx* c, const CallPlan& p, const float* cond_base,
+                     const Prefix& pf, int rows_per_seq, bool lm,
+                     hipStream_t st) {
+  const Dims& D = c->D;
+  const float eps = c->cfg.target.norm_eps;
+  const int R = p.cap;
+  T* A = static_cast<T*>(c->A);
+  launch_fuse_prep<T>(cond_base, p, static_cast<const T*>(c->tw.embed),
+                      static_cast<const T*>(c->dw.pos_query),
+                      static_cast<const float*>(c->dw.norm_c),
+                      static_cast<const float*>(c->dw.norm_e),
+                      static_cast<const float*>(c->dw.norm_q), eps, D.d, A, st);
+  int ks = gemm<T>(c, A, 3 * D.d, c->dw.w_fuse, D.d, 3 * D.d, p.n, R, st);
+  launch_residual<T>(c->x, c->P, ks, (size_t)D.R_cap * D.d, p.n, R, D.d, false,
+                     nullptr, eps, A, D.d, nullptr, 0, nullptr, st);
+  for (int l = 0; l < D.LD; ++l) {
+    const sb_layer_weights& lw = c->dw.layers[l];
+    launch_shift_prep<T>(c->x, p, D.d, A, st);
+    ks = gemm<T>(c, A, 2 * D.d, lw.w_shift, D.d, 2 * D.d, p.n, R, st);
+    launch_residual<T>(c->x, c->P, ks, (size_t)D.R_cap * D.d, p.n, R, D.d,
+                       false, static_cast<const float*>(lw.attn_norm), eps, A,
+                       D.d, nullptr, 0, nullptr, st);
+    const float* next_g = (l + 1 == D.LD && lm)
+                              ? static_cast<const float*>(c->dw.final_norm)
+                              : nullptr;
+    layer_body<T>(c, lw, l, p, pf, rows_per_seq, next_g, nullptr, 0, st);
+  }
+}
+
+// W_cond rows: cond_buf[i] = W_cond [taps of row idx[i]] for i < *n.
+template <typename T>
+void cond_rows(sb_ctx* c, const float* taps, const int* idx, const int* n,
+               int cap, hipStream_t st) {
+  const Dims& D = c->D;
+  T* A = static_cast<T*>(c->A);
+  launch_rows_to_elem<T>(taps, idx, n, cap, 3 * D.d, A, st);
+  const int ks = gemm<T>(c, A, 3 * D.d, c->dw.w_cond, D.d, 3 * D.d, n, cap, st);
+  launch_residual<T>(c->cond_buf, c->P, ks, (size_t)D.R_cap * D.d, n, cap, D.d,
+                     false, nullptr, c->cfg.target.norm_eps, A, D.d, nullptr, 0,
+                     nullptr, st);
+}
+
+
+// LM head: logits[i] = W_lm A[i] for the plan's rows (one K-chunk, written
+// straight into the logits buffer).
+template <typename T>
+void lm_head(sb_ctx* c, const void* A, const void* W, float* logits,
+             const int* n, int cap, hipStream_t st) {
+  const Dims& D = c->D;
+  launch_gemm_xwt<T>(static_cast<const T*>(A), D.d, static_cast<const T*>(W),
+                     D.V, D.d, logits, (size_t)cap * D.V, n, cap, 1, st);
+}
+
+TreeDims tree_dims(const sb_ctx* c, int n_seqs) {
+  const Dims& D = c->D;
+  return TreeDims{n_seqs, D.K, D.M, D.B_max, D.budget, D.bw, D.row_cap, D.rw, D.d};
+}
+
+template <typename T>
+int draft_expand_impl(sb_ctx* c, int m, const sb_seqs* sq, const sb_kv* dkv,
+                      sb_tree* t, sb_draft_out* o, hipStream_t st) {
+  const Dims& D = c->D;
+  const TreeDims td = tree_dims(c, sq->n_seqs);
+  CallPlan p = c->plan;
+  p.n_seqs = sq->n_seqs;
+  const float* cond_base = t->h_last;
+  if (m == 1) {
+    launch_block1_reset(td, *t, sq->root, c->n_aux, st);
+    cond_rows<T>(c, sq->cond_taps, nullptr, c->n_aux, D.S, st);
+    cond_base = c->cond_buf;
+  }
+  launch_plan_block(td, m, *t, sq->T, p, c->blk_row0, c->blk_nst, st);
+  launch_export_rows(p, D.S * D.B_max * D.K, o->call_seq, o->call_row,
+                     o->n_call, st);
+  const Prefix pf{dkv, c->dseg_k, c->dseg_v, D.dpages};
+  drafter_forward<T>(c, p, cond_base, pf, D.B_max * D.K, true, st);
+  float* logits = o->logits ? o->logits : c->logits;
+  lm_head<T>(c, c->A, c->dw.lm_head, logits, p.n, p.cap, st);
+  launch_vocab_partial(logits, p.n, p.cap, D.V, D.n_chunks, SB_TOPK, c->vpart,
+                       st);
+  const DraftRowOut ro{o->topk_id, o->topk_logit, o->lse, o->psi, o->bucket,
+                       o->branch, t->h_last, D.row_cap};
+  const int4 bmap = make_int4(c->cfg.branch_map[0], c->cfg.branch_map[1],
+                              c->cfg.branch_map[2], c->cfg.branch_map[3]);
+  launch_draft_finalize(c->vpart, D.n_chunks, p, c->x,
+                        static_cast<const float*>(c->dw.rank_w),
+                        static_cast<const float*>(c->dw.rank_b), D.d, bmap, ro,
+                        st);
+  launch_attach(td, *t, *o, c->blk_row0, c->blk_nst, st);
+  return hip_check(c, "sb_draft_block_expand");
+}
+
+template <typename T>
+int verify_impl(sb_ctx* c, const sb_seqs* sq, const sb_tree* t,
+                const sb_kv* tkv, sb_verify_out* out, hipStream_t st) {
+  const Dims& D = c->D;
+  const TreeDims td = tree_dims(c, sq->n_seqs);
+  CallPlan p = c->plan;
+  p.n_seqs = sq->n_seqs;
+  launch_plan_verify(td, *t, sq->T, p, st);
+  const Prefix pf{tkv, c->tseg_k, c->tseg_v, D.tpages};
+  target_forward<T>(c, p, pf, D.budget, out->taps, st);
+  float* logits = out->logits ? out->logits : c->logits;
+  lm_head<T>(c, c->A, c->tw.lm_head, logits, p.n, p.cap, st);
+  launch_vocab_partial(logits, p.n, p.cap, D.V, D.n_chunks, 1, c->vpart, st);
+  launch_verify_finalize(c->vpart, D.n_chunks, p.n, p.cap, p.out_row,
+                         out->argmax, st);
+  return hip_check(c, "sb_tree_verify");
+}
+
+template <typename T>
+int commit_impl(sb_ctx* c, sb_seqs* sq, const sb_tree* t,
+                const sb_verify_out* v, const sb_accept_out* acc,
+                sb_kv* tkv, sb_kv* dkv, hipStream_t st) {
+  const Dims& D = c->D;
+  const TreeDims td = tree_dims(c, sq->n_seqs);
+  launch_commit_plan(td, *t, *acc, sq->T, c->ci, c->fb, c->taps_idx, c->n_aux,
+                     st);
+  const KVPools tp{tkv->k, tkv->v, tkv->page_table, c->cfg.max_pages,
+                   tkv->n_pages, c->tseg_k, c->tseg_v, D.tpages};
+  const KVPools dp{dkv->k, dkv->v, dkv->page_table, c->cfg.max_pages,
+                   dkv->n_pages, c->dseg_k, c->dseg_v, D.dpages};
+  launch_commit_copy<T>(td, *t, *acc, c->ci, false, tp, D.S, D.L, D.Hkv, D.hd,
+                        st);
+  launch_commit_copy<T>(td, *t, *acc, c->ci, true, dp, D.S, D.LD, D.Hkv, D.hd,
+                        st);
+  // catch-up rows where the tree has no row continuing the accepted path
+  cond_rows<T>(c, v->taps, c->taps_idx, c->n_aux, D.S, st);
+  const Prefix pf{dkv, c->dseg_k, c->dseg_v, D.dpages};
+  CallPlan fb = c->fb;
+  fb.n_seqs = sq->n_seqs;
+  drafter_forward<T>(c, fb, c->cond_buf, pf, 1, false, st);
+  launch_seg_to_cache<T>(fb, dp, D.S, D.LD, D.Hkv, D.hd, st);
+  launch_commit_state(td, *sq, *acc, c->ci, v->taps, st);
+  return hip_check(c, "sb_commit");
+}
+
+template <typename T>
+int prefill_impl(sb_ctx* c, const sb_seqs* sq, const int32_t* prompt, int ld,
+                 const int32_t* lens, sb_kv* tkv, sb_kv* dkv, hipStream_t st) {
+  const Dims& D = c->D;
+  const CallPlan& p = c->plan;
+  const int S = D.S;
+  launch_set_int(c->one, 1, st);
+  launch_set_int(c->zero, 0, st);
+  const KVPools tp{tkv->k, tkv->v, tkv->page_table, c->cfg.max_pages,
+                   tkv->n_pages, c->tseg_k, c->tseg_v, D.tpages};
+  const KVPools dp{dkv->k, dkv->v, dkv->page_table, c->cfg.max_pages,
+                   dkv->n_pages, c->dseg_k, c->dseg_v, D.dpages};
+  const Prefix tpf{tkv, c->tseg_k, c->tseg_v, D.tpages};
+  const Prefix dpf{dkv, c->dseg_k, c->dseg_v, D.dpages};
+  const size_t tap_row = (size_t)3 * D.d;
+  for (int s = 0; s < sq->n_seqs; ++s) {
+    const int len = lens[s];
+    for (int a = 0; a < len; a += D.chunk) {
+      const int n = std::min(D.chunk, len - a);
+      launch_plan_prefill_target(S, s, a, n, prompt, ld, p, st);
+      target_forward<T>(c, p, tpf, D.chunk, c->taps_pf, st);
+      launch_seg_to_cache<T>(p, tp, S, D.L, D.Hkv, D.hd, st);
+      if (a + n == len) {
+        const T* last = static_cast<const T*>(c->A) + (size_t)(n - 1) * D.d;
+        lm_head<T>(c, last, c->tw.lm_head, c->logits, c->one, 1, st);
+        launch_vocab_partial(c->logits, c->one, 1, D.V, D.n_chunks, 1,
+                             c->vpart, st);
+        launch_verify_finalize(c->vpart, D.n_chunks, c->one, 1, c->zero,
+                               c->root_arg, st);
+      }
+      launch_plan_prefill_draft(S, s, a, n, prompt, ld, p, c->n_aux, st);
+      cond_rows<T>(c, c->taps_pf, nullptr, c->n_aux, D.chunk, st);
+      drafter_forward<T>(c, p, c->cond_buf, dpf, D.chunk, false, st);
+      launch_seg_to_cache<T>(p, dp, S, D.LD, D.Hkv, D.hd, st);
+      launch_copy_f32(c->taps_pf, c->taps_pf + (size_t)n * tap_row,
+                      (int)tap_row, st);
+    }
+    launch_prefill_finish(*sq, s, len, D.d, c->taps_pf, 0, c->root_arg, st);
+  }
+  return hip_check(c, "sb_prefill");
+}
+
+int check_common(sb_ctx* c) {
+  if (!c) return SB_EINVAL;
+  if (!c->bound) return fail(c, SB_ESTATE, "context not bound (call sb_bind)");
+  return SB_OK;
+}
+
+int check_seqs(sb_ctx* c, const sb_seqs* sq) {
+  if (!sq) return fail(c, SB_EINVAL, "seqs is NULL");
+  if (sq->n_seqs < 1 || sq->n_seqs > c->cfg.max_seqs)
+    return fail(c, SB_ESHAPE, "n_seqs must be in 1..max_seqs");
+  if (bad_ptr(sq->root, 4) || bad_ptr(sq->T, 4) || bad_ptr(sq->cond_taps, 4))
+    return fail(c, SB_EINVAL, "seqs pointer NULL or misaligned");
+  return SB_OK;
+}
+
+int check_kv(sb_ctx* c, const sb_kv* kv, int n_layers, const char* what) {
+  if (!kv) return fail(c, SB_EINVAL, std::string(what) + " is NULL");
+  if (bad_ptr(kv->k, 16) || bad_ptr(kv->v, 16) || bad_ptr(kv->page_table, 4))
+    return fail(c, SB_EINVAL, std::string(what) + " pointer NULL or misaligned");
+  if (kv->n_layers != n_layers)
+    return fail(c, SB_ESHAPE, std::string(what) + " has the wrong layer count");
+  if (kv->n_pages < 1) return fail(c, SB_EINVAL, std::string(what) + " has no pages");
+  return SB_OK;
+}
+
+int check_tree(sb_ctx* c, const sb_tree* t) {
+  if (!t) return fail(c, SB_EINVAL, "tree is NULL");
+  const void* ps[] = {t->n_nodes, t->token, t->parent, t->depth, t->row,
+                      t->rank, t->logp, t->cum_logp, t->anc, t->n_rows,
+                      t->row_block, t->row_start, t->row_k, t->row_pos,
+                      t->row_vis, t->h_last, t->n_starts, t->starts};
+  for (const void* q : ps)
+    if (bad_ptr(q, 4)) return fail(c, SB_EINVAL, "tree pointer NULL or misaligned");
+  return SB_OK;
+}
+
+bool is_bf16(const sb_ctx* c) { return c->cfg.dtype == SB_BF16; }
+
+}  // namespace
+
+extern "C" {
+
+int sb_draft_block_expand(sb_ctx* c, int32_t block_index, int32_t K,
+                          const sb_seqs* seqs, const sb_kv* draft_kv,
+                          sb_tree* tree, sb_draft_out* out, void* stream) {
+  int rc = check_common(c);
+  if (rc) return rc;
+  if (K != c->cfg.K) return fail(c, SB_ESHAPE, "K differs from cfg.K");
+  if (block_index < 1 || block_index > c->cfg.M)
+    return fail(c, SB_EINVAL, "block_index must be in 1..M");
+  if ((rc = check_seqs(c, seqs)) || (rc = check_kv(c, draft_kv, c->D.LD, "draft_kv")) ||
+      (rc = check_tree(c, tree)))
+    return rc;
+  if (!out) return fail(c, SB_EINVAL, "out is NULL");
+  const void* ps[] = {out->topk_id, out->topk_logit, out->lse, out->psi,
+                      out->bucket, out->branch, out->call_seq, out->call_row,
+                      out->n_call};
+  for (const void* q : ps)
+    if (bad_ptr(q, 4)) return fail(c, SB_EINVAL, "out pointer NULL or misaligned");
+  if (out->logits && bad_ptr(out->logits, 16))
+    return fail(c, SB_EINVAL, "out->logits misaligned");
+  return is_bf16(c) ? draft_expand_impl<bf16_t>(c, block_index, seqs, draft_kv, tree, out, S_(stream))
+                    : draft_expand_impl<float>(c, block_index, seqs, draft_kv, tree, out, S_(stream));
+}
+
+int sb_tree_verify(sb_ctx* c, const sb_seqs* seqs, const sb_tree* tree,
+                   const sb_kv* target_kv, sb_verify_out* out, void* stream) {
+  int rc = check_common(c);
+  if (rc) return rc;
+  if ((rc = check_seqs(c, seqs)) || (rc = check_kv(c, target_kv, c->D.L, "target_kv")) ||
+      (rc = check_tree(c, tree)))
+    return rc;
+  if (!out || bad_ptr(out->argmax, 4) || bad_ptr(out->taps, 4))
+    return fail(c, SB_EINVAL, "verify out pointer NULL or misaligned");
+  if (out->logits && bad_ptr(out->logits, 16))
+    return fail(c, SB_EINVAL, "out->logits misaligned");
+  return is_bf16(c) ? verify_impl<bf16_t>(c, seqs, tree, target_kv, out, S_(stream))
+                    : verify_impl<float>(c, seqs, tree, target_kv, out, S_(stream));
+}
+
+int sb_accept(sb_ctx* c, int32_t n_seqs, const sb_tree* tree,
+              const int32_t* argmax, sb_accept_out* out, void* stream) {
+  int rc = check_common(c);
+  if (rc) return rc;
+  if (n_seqs < 1 || n_seqs > c->cfg.max_seqs)
+    return fail(c, SB_ESHAPE, "n_seqs must be in 1..max_seqs");
+  if ((rc = check_tree(c, tree))) return rc;
+  if (bad_ptr(argmax, 4) || !out || bad_ptr(out->path, 4) ||
+      bad_ptr(out->n_accepted, 4) || bad_ptr(out->bonus, 4))
+    return fail(c, SB_EINVAL, "accept pointer NULL or misaligned");
+  launch_accept(tree_dims(c, n_seqs), *tree, argmax, *out, S_(stream));
+  return hip_check(c, "sb_accept");
+}
+
+int sb_commit(sb_ctx* c, sb_seqs* seqs, const sb_tree* tree,
+              const sb_verify_out* verify, const sb_accept_out* acc,
+              sb_kv* target_kv, sb_kv* draft_kv, void* stream) {
+  int rc = check_common(c);
+  if (rc) return rc;
+  if ((rc = check_seqs(c, seqs)) || (rc = check_tree(c, tree)) ||
+      (rc = check_kv(c, target_kv, c->D.L, "target_kv")) ||
+      (rc = check_kv(c, draft_kv, c->D.LD, "draft_kv")))
+    return rc;
+  if (!verify || bad_ptr(verify->taps, 4) || !acc || bad_ptr(acc->path, 4) ||
+      bad_ptr(acc->n_accepted, 4) || bad_ptr(acc->bonus, 4))
+    return fail(c, SB_EINVAL, "commit pointer NULL or misaligned");
+  return is_bf16(c) ? commit_impl<bf16_t>(c, seqs, tree, verify, acc, target_kv, draft_kv, S_(stream))
+                    : commit_impl<float>(c, seqs, tree, verify, acc, target_kv, draft_kv, S_(stream));
+}
+
+int sb_prefill(sb_ctx* c, const sb_seqs* seqs, const int32_t* prompt,
+               int32_t ld_prompt, const int32_t* lens, sb_kv* target_kv,
+               sb_kv* draft_kv, void* stream) {
+  int rc = check_common(c);
+  if (rc) return rc;
+  if ((rc = check_seqs(c, seqs)) || (rc = check_kv(c, target_kv, c->D.L, "target_kv")) ||
+      (rc = check_kv(c, draft_kv, c->D.LD, "draft_kv")))
+    return rc;
+  if (bad_ptr(prompt, 4) || !lens) return fail(c, SB_EINVAL, "prompt or lens NULL");
+  for (int s = 0; s < seqs->n_seqs; ++s) {
+    if (lens[s] < 1 || lens[s] > ld_prompt)
+      return fail(c, SB_ESHAPE, "prompt length out of range");
+    if (lens[s] + 1 > c->cfg.max_pages * 16)
+      return fail(c, SB_EBUDGET, "prompt does not fit max_pages");
+  }
+  return is_bf16(c) ? prefill_impl<bf16_t>(c, seqs, prompt, ld_prompt, lens, target_kv, draft_kv, S_(stream))
+                    : prefill_impl<float>(c, seqs, prompt, ld_prompt, lens, target_kv, draft_kv, S_(stream));
+}
+
+}  // extern "C"

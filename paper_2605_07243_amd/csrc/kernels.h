@@ -1,0 +1,185 @@
+// Internal launch interface between the C-ABI engine and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "specblock.h"
+
+#define SB_MAX_SEQS 64
+
+namespace sb {
+
+typedef uint16_t bf16_t;
+
+// Rows of one forward call, compacted sequence-major.  Device arrays of
+// capacity `cap` rows; the active count is read on the device from *n.
+struct CallPlan {
+  int* n;            // [1]
+  int* seq;          // [cap] sequence of the row
+  int* slot;         // [cap] the row's slot in its sequence's segment
+  int* pos;          // [cap] RoPE position
+  int* token;        // [cap] input token (target) / start token (drafter)
+  uint32_t* vis;     // [cap][vis_words] segment slots the row attends to
+  int* k;            // [cap] drafter block position, 1-based
+  int* pred;         // [cap] call index of the shift partner (k-1, or self)
+  int* cond;         // [cap] row of the condition matrix (-1: zero vector)
+  int* seq_off;      // [max_seqs + 1] first call row of each sequence
+  int* prefix_len;   // [max_seqs] committed entries visible to the sequence
+  int* seg_len;      // [max_seqs] valid segment slots of the sequence
+  int* out_row;      // [cap] destination index of per-row outputs (or -1)
+  int* kv_dst;       // [cap] cache entry the row's K/V is committed to (-1)
+  int cap;
+  int vis_words;
+  int n_seqs;        // host value: sequences with valid seq_off entries
+};
+
+// K/V addressing: paged prefix + per-sequence segment, both in the
+// [kvh][16][hd] (K) / [kvh][hd][16] (V) page layout, one layer at a time.
+struct KVView {
+  const void* k;            // layer base of the page pool
+  const void* v;
+  const int* page_table;    // [S][max_pages]
+  int max_pages;
+  int n_pages;              // pages in the pool (indices are clamped to it)
+  const void* seg_k;        // layer base of the segment pool [S][seg_pages]
+  const void* seg_v;
+  int seg_pages;            // pages per sequence in the segment pool
+};
+
+int gemm_ksplit(int N, int K, int ksplit_cap);
+template <typename T>
+int launch_gemm_xwt(const T* X, int ldx, const T* W, int N, int K, float* P,
+                    size_t part_stride, const int* m_count, int m_cap,
+                    int ksplit, hipStream_t st);
+
+template <typename T>
+void launch_embed(const CallPlan& p, const T* embed, int d, float* x,
+                  hipStream_t st);
+template <typename T>
+void launch_rmsnorm(const float* x, const int* n, int cap, int d,
+                    const float* g, float eps, T* out, int ldo,
+                    hipStream_t st);
+// x = (accumulate ? x : 0) + sum_ks P[ks]; then optionally out = rmsnorm(x)*g
+// and taps[out_row][j] = x for every bit j of tap_mask.
+template <typename T>
+void launch_residual(float* x, const float* P, int ks, size_t part_stride,
+                     const int* n, int cap, int d, bool accumulate,
+                     const float* g, float eps, T* out, int ldo, float* taps,
+                     int tap_mask, const int* out_row, hipStream_t st);
+template <typename T>
+void launch_qkv_post(const float* P, int ks, size_t part_stride,
+                     const CallPlan& p, int H, int Hkv, int hd, float theta,
+                     T* q, void* seg_k, void* seg_v, int seg_pages,
+                     hipStream_t st);
+template <typename T>
+void launch_swiglu(const float* P, int ks, size_t part_stride, const int* n,
+                   int cap, int F, T* out, hipStream_t st);
+template <typename T>
+void launch_shift_prep(const float* h, const CallPlan& p, int d, T* out,
+                       hipStream_t st);
+template <typename T>
+void launch_fuse_prep(const float* cond, const CallPlan& p, const T* embed,
+                      const T* pos_query, const float* gc, const float* ge,
+                      const float* gq, float eps, int d, T* out,
+                      hipStream_t st);
+// out[i] = T(src[idx[i]]) rows of width w (idx == nullptr: identity).
+template <typename T>
+void launch_rows_to_elem(const float* src, const int* idx, const int* n,
+                         int cap, int w, T* out, hipStream_t st);
+
+// Tree attention over paged prefix + masked segment.
+template <typename T>
+void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
+                      int rows_per_seq_cap, int H, int Hkv, int hd,
+                      int n_split, int max_prefix, float* o_part, float* ml,
+                      T* out, hipStream_t st);
+
+// Vocabulary reductions over fp32 logits [cap][V].
+void launch_vocab_partial(const float* logits, const int* n, int cap, int V,
+                          int n_chunks, int topk, float* part,
+                          hipStream_t st);
+struct DraftRowOut {
+  int* topk_id;
+  float* topk_logit;
+  float* lse;
+  float* psi;
+  int* bucket;
+  int* branch;
+  float* h_last;        // tree h_last [S][row_cap][d] (also the rank-head input)
+  int row_cap;
+};
+void launch_draft_finalize(const float* part, int n_chunks, const CallPlan& p,
+                           const float* x, const float* rank_w,
+                           const float* rank_b, int d, int4 bmap,
+                           DraftRowOut o, hipStream_t st);
+void launch_verify_finalize(const float* part, int n_chunks, const int* n,
+                            int cap, const int* out_row, int* argmax,
+                            hipStream_t st);
+
+// Tree kernels.
+struct TreeDims {
+  int S, K, M, B_max, budget;
+  int bw;        // ancestor words per node
+  int row_cap;   // drafter rows per sequence per iteration
+  int rw;        // visibility words per drafter row
+  int d;
+};
+struct CommitInfo {
+  int* T_old;
+  int* a;
+  int* cur;
+  int* cont;
+};
+// Whole cache pools (all layers): pages [L][n_pages][Hkv][16][hd] and the
+// per-sequence segment scratch [L][S][seg_pages][Hkv][16][hd].
+struct KVPools {
+  void* k;
+  void* v;
+  const int* page_table;
+  int max_pages;
+  int n_pages;
+  void* seg_k;
+  void* seg_v;
+  int seg_pages;
+};
+void launch_block1_reset(const TreeDims& td, const sb_tree& t, const int* root,
+                         int* n_aux, hipStream_t st);
+void launch_plan_block(const TreeDims& td, int m, const sb_tree& t,
+                       const int* T, const CallPlan& p, int* blk_row0,
+                       int* blk_nst, hipStream_t st);
+void launch_attach(const TreeDims& td, const sb_tree& t, const sb_draft_out& o,
+                   const int* blk_row0, const int* blk_nst, hipStream_t st);
+void launch_plan_verify(const TreeDims& td, const sb_tree& t, const int* T,
+                        const CallPlan& p, hipStream_t st);
+void launch_accept(const TreeDims& td, const sb_tree& t, const int* argmax,
+                   const sb_accept_out& o, hipStream_t st);
+void launch_commit_plan(const TreeDims& td, const sb_tree& t,
+                        const sb_accept_out& acc, const int* T,
+                        const CommitInfo& ci, const CallPlan& fb,
+                        int* taps_idx, int* n_aux, hipStream_t st);
+template <typename T>
+void launch_commit_copy(const TreeDims& td, const sb_tree& t,
+                        const sb_accept_out& acc, const CommitInfo& ci,
+                        bool drafter, const KVPools& kv, int pool_seqs,
+                        int n_layers, int Hkv, int hd, hipStream_t st);
+template <typename T>
+void launch_seg_to_cache(const CallPlan& p, const KVPools& kv, int S,
+                         int n_layers, int Hkv, int hd, hipStream_t st);
+void launch_commit_state(const TreeDims& td, const sb_seqs& sq,
+                         const sb_accept_out& acc, const CommitInfo& ci,
+                         const float* taps, hipStream_t st);
+void launch_plan_prefill_target(int S, int s, int a, int n, const int* prompt,
+                                int ld, const CallPlan& p, hipStream_t st);
+void launch_plan_prefill_draft(int S, int s, int a, int n, const int* prompt,
+                               int ld, const CallPlan& p, int* n_aux,
+                               hipStream_t st);
+void launch_prefill_finish(const sb_seqs& sq, int s, int len, int d,
+                           const float* taps_pf, int n_last,
+                           const int* root_arg, hipStream_t st);
+void launch_copy_f32(float* dst, const float* src, int n, hipStream_t st);
+void launch_set_int(int* p, int v, hipStream_t st);
+void launch_export_rows(const CallPlan& p, int out_cap, int* call_seq,
+                        int* call_row, int* n_call, hipStream_t st);
+
+}  // namespace sb

@@ -1,0 +1,661 @@
+// Tree bookkeeping on the device: row plans for each forward call, rank-
+// guided sibling attachment and next-block starts (Sec. 3.2, Alg. 2), the
+// greedy acceptance walk and the commit copies.  Small single-workgroup or
+// one-wave-per-sequence kernels; nothing here synchronises with the host.
+#include <float.h>
+
+#include "common.h"
+#include "kernels.h"
+#include "specblock.h"
+
+namespace sb {
+
+__device__ __forceinline__ int wave_excl_scan(int v, int& total) {
+  const int lane = threadIdx.x & 63;
+  int incl = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int t = __shfl_up(incl, o, SB_WAVE);
+    if (lane >= o) incl += t;
+  }
+  total = __shfl(incl, 63, SB_WAVE);
+  return incl - v;
+}
+
+// ---------------------------------------------------------------------------
+// Block 1: reset the tree to the root (node 0, one start) and count the
+// W_cond rows (one per sequence).
+__global__ void block1_reset_kernel(TreeDims td, sb_tree t,
+                                    const int* __restrict__ root,
+                                    int* __restrict__ n_aux) {
+  for (int s = threadIdx.x; s < td.S; s += blockDim.x) {
+    const size_t b = (size_t)s * td.budget;
+    t.n_nodes[s] = 1;
+    t.token[b] = root[s];
+    t.parent[b] = -1;
+    t.depth[b] = 0;
+    t.row[b] = -1;
+    t.rank[b] = 0;
+    t.logp[b] = 0.f;
+    t.cum_logp[b] = 0.f;
+    for (int w = 0; w < td.bw; ++w) t.anc[b * td.bw + w] = (w == 0) ? 1u : 0u;
+    t.n_rows[s] = 0;
+    t.n_starts[s] = 1;
+    t.starts[(size_t)s * td.B_max] = 0;
+  }
+  if (threadIdx.x == 0) *n_aux = td.S;
+}
+
+// Rows of one block expansion: start b of sequence s gets rows k = 1..K at
+// positions pos(start) + k; they see the rows visible to the row that
+// proposed the start plus their own block's rows <= k.
+__global__ void plan_block_kernel(TreeDims td, int m, sb_tree t,
+                                  const int* __restrict__ T, CallPlan p,
+                                  int* __restrict__ blk_row0,
+                                  int* __restrict__ blk_nst) {
+  __shared__ int cnt[SB_MAX_SEQS], old[SB_MAX_SEQS], off[SB_MAX_SEQS];
+  const int K = td.K, rw = td.rw;
+  if (threadIdx.x == 0) {
+    int o = 0;
+    for (int s = 0; s < td.S; ++s) {
+      const int n_old = t.n_rows[s];
+      int nst = min(t.n_starts[s], td.B_max);
+      nst = max(0, min(nst, (td.row_cap - n_old) / K));
+      cnt[s] = nst * K;
+      old[s] = n_old;
+      off[s] = o;
+      p.seq_off[s] = o;
+      p.prefix_len[s] = T[s];
+      p.seg_len[s] = n_old + nst * K;
+      blk_row0[s] = n_old;
+      blk_nst[s] = nst;
+      o += nst * K;
+    }
+    p.seq_off[td.S] = o;
+    *p.n = o;
+  }
+  __syncthreads();
+  for (int s = 0; s < td.S; ++s) {
+    for (int j = threadIdx.x; j < cnt[s]; j += blockDim.x) {
+      const int b = j / K, k = j % K + 1;
+      const int i = off[s] + j;
+      const int lr = old[s] + j;
+      const int sn = t.starts[(size_t)s * td.B_max + b];
+      const size_t nidx = (size_t)s * td.budget + sn;
+      const int srow = t.row[nidx];
+      p.seq[i] = s;
+      p.slot[i] = lr;
+      p.pos[i] = T[s] + t.depth[nidx] + k;
+      p.token[i] = t.token[nidx];
+      p.k[i] = k;
+      p.pred[i] = k > 1 ? i - 1 : i;
+      p.cond[i] = (m == 1 || srow < 0) ? s : s * td.row_cap + srow;
+      p.out_row[i] = s * td.row_cap + lr;
+      p.kv_dst[i] = -1;
+      const size_t rbase = (size_t)s * td.row_cap;
+      for (int w = 0; w < rw; ++w) {
+        uint32_t bits = (m > 1 && srow >= 0) ? t.row_vis[(rbase + srow) * rw + w] : 0u;
+        // own block rows lr-k+1 .. lr
+        for (int q = lr - k + 1; q <= lr; ++q)
+          if ((q >> 5) == w) bits |= 1u << (q & 31);
+        t.row_vis[(rbase + lr) * rw + w] = bits;
+        p.vis[(size_t)i * p.vis_words + w] = bits;
+      }
+      t.row_block[rbase + lr] = m;
+      t.row_start[rbase + lr] = sn;
+      t.row_k[rbase + lr] = k;
+      t.row_pos[rbase + lr] = p.pos[i];
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0)
+    for (int s = 0; s < td.S; ++s) t.n_rows[s] = old[s] + cnt[s];
+}
+
+// Sibling attachment of one block in (k, start, rank) order within the
+// budget, then the next block's starts.  One wave per sequence; lane b owns
+// start b of the block.
+__global__ __launch_bounds__(64) void attach_kernel(
+    TreeDims td, sb_tree t, const int* __restrict__ topk_id,
+    const float* __restrict__ topk_logit, const float* __restrict__ lse,
+    const int* __restrict__ bucket, const int* __restrict__ branch,
+    const int* __restrict__ blk_row0, const int* __restrict__ blk_nst) {
+  const int s = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int K = td.K, budget = td.budget, bw = td.bw;
+  const int nst = blk_nst[s];
+  const int row0 = blk_row0[s];
+  const size_t nb = (size_t)s * budget;
+  const size_t rb = (size_t)s * td.row_cap;
+  const bool mine = lane < nst;
+  int chain = mine ? t.starts[(size_t)s * td.B_max + lane] : 0;
+  bool alive = mine;
+  int chain_depth = 0;
+  float chain_cum = 0.f;
+  uint32_t chain_anc[SB_MAX_ANC_WORDS];
+#pragma unroll
+  for (int w = 0; w < SB_MAX_ANC_WORDS; ++w) chain_anc[w] = 0u;
+  if (mine) {
+    chain_depth = t.depth[nb + chain];
+    chain_cum = t.cum_logp[nb + chain];
+#pragma unroll
+    for (int w = 0; w < SB_MAX_ANC_WORDS; ++w)
+      if (w < bw) chain_anc[w] = t.anc[(nb + chain) * bw + w];
+  }
+  int nn = t.n_nodes[s];
+  const int first_new = nn;
+  for (int k = 1; k <= K; ++k) {
+    const int r = row0 + lane * K + (k - 1);
+    const int want = (mine && alive) ? branch[rb + r] : 0;
+    int total;
+    const int excl = wave_excl_scan(want, total);
+    const int id0 = nn + excl;
+    if (mine && alive) {
+      for (int rank = 1; rank <= want; ++rank) {
+        const int id = id0 + rank - 1;
+        if (id >= budget) break;
+        const size_t o = (rb + r) * SB_TOPK_K + (rank - 1);
+        const float lp = topk_logit[o] - lse[rb + r];
+        t.token[nb + id] = topk_id[o];
+        t.parent[nb + id] = chain;
+        t.depth[nb + id] = chain_depth + 1;
+        t.row[nb + id] = r;
+        t.rank[nb + id] = rank;
+        t.logp[nb + id] = lp;
+        t.cum_logp[nb + id] = chain_cum + lp;
+#pragma unroll
+        for (int w = 0; w < SB_MAX_ANC_WORDS; ++w)
+          if (w < bw)
+            t.anc[(nb + id) * bw + w] =
+                chain_anc[w] | ((id >> 5) == w ? (1u << (id & 31)) : 0u);
+      }
+      if (want >= 1 && id0 < budget) {
+        const size_t o = (rb + r) * SB_TOPK_K;
+        chain = id0;
+        chain_depth += 1;
+        chain_cum += topk_logit[o] - lse[rb + r];
+#pragma unroll
+        for (int w = 0; w < SB_MAX_ANC_WORDS; ++w)
+          if ((id0 >> 5) == w) chain_anc[w] |= 1u << (id0 & 31);
+      } else {
+        alive = false;
+      }
+    }
+    nn = min(budget, nn + total);
+  }
+  if (lane == 0) t.n_nodes[s] = nn;
+  __syncthreads();   // node writes of all lanes visible below
+  // next-block starts: chain ends first, then rank >= 2 siblings of b1/b2
+  // rows by cumulative log-probability (ties: lower node id)
+  int* out = t.starts + (size_t)s * td.B_max;
+  if (nn >= budget) {
+    if (lane == 0) t.n_starts[s] = 0;
+    return;
+  }
+  int n_ends;
+  const int is_end = (mine && alive) ? 1 : 0;
+  const int e_excl = wave_excl_scan(is_end, n_ends);
+  if (is_end && e_excl < td.B_max) out[e_excl] = chain;
+  int taken = min(n_ends, td.B_max);
+  // candidate mask per lane: node first_new + lane + 64 q
+  uint32_t cand = 0u;
+  for (int q = 0; q < 8; ++q) {
+    const int id = first_new + lane + 64 * q;
+    if (id < nn && t.rank[nb + id] >= 2) {
+      const int bk = bucket[rb + t.row[nb + id]];
+      if (bk == 1 || bk == 2) cand |= 1u << q;
+    }
+  }
+  while (taken < td.B_max) {
+    float bv = -FLT_MAX;
+    int bi = 0x7FFFFFFF;
+    for (int q = 0; q < 8; ++q) {
+      if (cand & (1u << q)) {
+        const int id = first_new + lane + 64 * q;
+        const float v = t.cum_logp[nb + id];
+        if (better(v, id, bv, bi)) {
+          bv = v;
+          bi = id;
+        }
+      }
+    }
+    float v = bv;
+    int id = bi;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float v2 = __shfl_xor(v, o, SB_WAVE);
+      const int i2 = __shfl_xor(id, o, SB_WAVE);
+      if (better(v2, i2, v, id)) {
+        v = v2;
+        id = i2;
+      }
+    }
+    if (id == 0x7FFFFFFF) break;
+    if (lane == 0) out[taken] = id;
+    if (((id - first_new) & 63) == lane) cand &= ~(1u << ((id - first_new) >> 6));
+    ++taken;
+  }
+  if (lane == 0) t.n_starts[s] = taken;
+}
+
+// Verification rows: every node of every tree at T + depth, seeing its
+// ancestors-or-self.
+__global__ void plan_verify_kernel(TreeDims td, sb_tree t,
+                                   const int* __restrict__ T, CallPlan p) {
+  __shared__ int off[SB_MAX_SEQS + 1];
+  if (threadIdx.x == 0) {
+    int o = 0;
+    for (int s = 0; s < td.S; ++s) {
+      off[s] = o;
+      p.seq_off[s] = o;
+      p.prefix_len[s] = T[s];
+      const int n = min(t.n_nodes[s], td.budget);
+      p.seg_len[s] = n;
+      o += n;
+    }
+    off[td.S] = o;
+    p.seq_off[td.S] = o;
+    *p.n = o;
+  }
+  __syncthreads();
+  for (int s = 0; s < td.S; ++s) {
+    const int n = off[s + 1] - off[s];
+    for (int j = threadIdx.x; j < n; j += blockDim.x) {
+      const int i = off[s] + j;
+      const size_t nidx = (size_t)s * td.budget + j;
+      p.seq[i] = s;
+      p.slot[i] = j;
+      p.pos[i] = T[s] + t.depth[nidx];
+      p.token[i] = t.token[nidx];
+      p.k[i] = 1;
+      p.pred[i] = i;
+      p.cond[i] = -1;
+      p.out_row[i] = s * td.budget + j;
+      p.kv_dst[i] = -1;
+      for (int w = 0; w < p.vis_words; ++w)
+        p.vis[(size_t)i * p.vis_words + w] = w < td.bw ? t.anc[nidx * td.bw + w] : 0u;
+    }
+  }
+}
+
+// Greedy acceptance walk, one wave per sequence.
+__global__ __launch_bounds__(64) void accept_kernel(TreeDims td, sb_tree t,
+                                                    const int* __restrict__ argmax,
+                                                    sb_accept_out out) {
+  const int s = blockIdx.x;
+  const int lane = threadIdx.x;
+  const size_t nb = (size_t)s * td.budget;
+  const int nn = min(t.n_nodes[s], td.budget);
+  const int path_cap = td.M * td.K;
+  int cur = 0, a = 0;
+  while (a < path_cap) {
+    const int g = argmax[nb + cur];
+    int best = 0x7FFFFFFF;
+    for (int j = 1 + lane; j < nn; j += 64)
+      if (t.parent[nb + j] == cur && t.token[nb + j] == g) best = min(best, j);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) best = min(best, __shfl_xor(best, o, SB_WAVE));
+    if (best == 0x7FFFFFFF) break;
+    if (lane == 0) out.path[(size_t)s * path_cap + a] = best;
+    cur = best;
+    ++a;
+  }
+  if (lane == 0) {
+    out.n_accepted[s] = a;
+    out.bonus[s] = argmax[nb + cur];
+  }
+}
+
+// Commit planning: last accepted node, the drafter row continuing it (or a
+// catch-up row when the tree has none) and the catch-up call plan.
+__global__ void commit_plan_kernel(TreeDims td, sb_tree t, sb_accept_out acc,
+                                   const int* __restrict__ T, CommitInfo ci,
+                                   CallPlan fb, int* __restrict__ taps_idx,
+                                   int* __restrict__ n_aux) {
+  const int path_cap = td.M * td.K;
+  for (int s = threadIdx.x; s < td.S; s += blockDim.x) {
+    const size_t nb = (size_t)s * td.budget;
+    const size_t rb = (size_t)s * td.row_cap;
+    const int a = acc.n_accepted[s];
+    const int cur = a > 0 ? acc.path[(size_t)s * path_cap + a - 1] : 0;
+    int cont = -1;
+    const int nrows = t.n_rows[s];
+    if (cur == 0) {
+      if (nrows > 0) cont = 0;
+    } else {
+      const int r = t.row[nb + cur];
+      if (t.rank[nb + cur] == 1 && t.row_k[rb + r] < td.K && r + 1 < nrows)
+        cont = r + 1;
+    }
+    if (cont < 0) {
+      for (int j = 0; j < nrows; ++j)
+        if (t.row_start[rb + j] == cur && t.row_k[rb + j] == 1) {
+          cont = j;
+          break;
+        }
+    }
+    ci.T_old[s] = T[s];
+    ci.a[s] = a;
+    ci.cur[s] = cur;
+    ci.cont[s] = cont;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int o = 0;
+    for (int s = 0; s < td.S; ++s) {
+      fb.seq_off[s] = o;
+      const int a = ci.a[s];
+      fb.prefix_len[s] = ci.T_old[s] + a;   // drafter entries 1..T+a
+      if (ci.cont[s] < 0) {
+        const int cur = ci.cur[s];
+        const size_t nb = (size_t)s * td.budget;
+        fb.seq[o] = s;
+        fb.slot[o] = 0;
+        fb.pos[o] = ci.T_old[s] + a + 1;
+        fb.token[o] = t.token[nb + cur];
+        fb.k[o] = 1;
+        fb.pred[o] = o;
+        fb.cond[o] = o;
+        fb.out_row[o] = -1;
+        fb.kv_dst[o] = ci.T_old[s] + a;
+        for (int w = 0; w < fb.vis_words; ++w)
+          fb.vis[(size_t)o * fb.vis_words + w] = (w == 0) ? 1u : 0u;
+        fb.seg_len[s] = 1;
+        taps_idx[o] = s * td.budget + max(t.parent[nb + cur], 0);
+        ++o;
+      } else {
+        fb.seg_len[s] = 0;
+      }
+    }
+    fb.seq_off[td.S] = o;
+    *fb.n = o;
+    *n_aux = o;
+  }
+}
+
+// Copy committed K/V entries.  Target: the root and accepted nodes (verify
+// scratch slot = node id) to entries T .. T+a.  Drafter: the rows that
+// proposed the accepted nodes to entries T .. T+a-1 (positions T+1 ..
+// T+a), and the continuing row, if any, to entry T+a.
+template <typename T>
+__global__ void commit_copy_kernel(TreeDims td, sb_tree t, sb_accept_out acc,
+                                   CommitInfo ci, int drafter, KVPools kv,
+                                   int pool_seqs, int Hkv, int hd) {
+  const int s = blockIdx.x;
+  const int j = blockIdx.y;               // 0 .. M K
+  const int l = blockIdx.z / Hkv, kh = blockIdx.z % Hkv;
+  const int a = ci.a[s];
+  const int T0 = ci.T_old[s];
+  const int path_cap = td.M * td.K;
+  int src_slot, dst;
+  if (!drafter) {
+    if (j > a) return;
+    src_slot = j == 0 ? 0 : acc.path[(size_t)s * path_cap + j - 1];
+    dst = T0 + j;
+  } else {
+    if (j < a) {
+      const int node = acc.path[(size_t)s * path_cap + j];
+      src_slot = t.row[(size_t)s * td.budget + node];
+      dst = T0 + j;
+    } else if (j == a && ci.cont[s] >= 0) {
+      src_slot = ci.cont[s];
+      dst = T0 + a;
+    } else {
+      return;
+    }
+  }
+  const int page_i = dst >> 4;
+  if (page_i >= kv.max_pages) return;
+  const int page = min(max(kv.page_table[(size_t)s * kv.max_pages + page_i], 0),
+                       kv.n_pages - 1);
+  const int sl = dst & 15;
+  const int sp = src_slot >> 4, ss = src_slot & 15;
+  if (sp >= kv.seg_pages) return;
+  const size_t lay = (size_t)l;
+  const size_t src_page = ((lay * pool_seqs + s) * kv.seg_pages + sp) * Hkv + kh;
+  const size_t dst_page = (lay * kv.n_pages + page) * Hkv + kh;
+  const T* sk = static_cast<const T*>(kv.seg_k) + src_page * 16 * hd;
+  const T* sv = static_cast<const T*>(kv.seg_v) + src_page * 16 * hd;
+  T* dk = static_cast<T*>(kv.k) + dst_page * 16 * hd;
+  T* dv = static_cast<T*>(kv.v) + dst_page * 16 * hd;
+  for (int e = threadIdx.x; e < hd; e += blockDim.x) {
+    dk[sl * hd + e] = sk[ss * hd + e];
+    dv[e * 16 + sl] = sv[e * 16 + ss];
+  }
+}
+
+// Rows of a plan whose kv_dst >= 0: segment slot -> cache entry kv_dst.
+template <typename T>
+__global__ void seg_to_cache_kernel(CallPlan p, KVPools kv, int S, int Hkv,
+                                    int hd) {
+  const int i = blockIdx.x;
+  if (i >= *p.n) return;
+  const int dst = p.kv_dst[i];
+  if (dst < 0) return;
+  const int l = blockIdx.y / Hkv, kh = blockIdx.y % Hkv;
+  const int s = p.seq[i], slot = p.slot[i];
+  const int page_i = dst >> 4;
+  if (page_i >= kv.max_pages) return;
+  const int page = min(max(kv.page_table[(size_t)s * kv.max_pages + page_i], 0),
+                       kv.n_pages - 1);
+  const int sl = dst & 15;
+  const int sp = slot >> 4, ss = slot & 15;
+  if (sp >= kv.seg_pages) return;
+  const size_t src_page = (((size_t)l * S + s) * kv.seg_pages + sp) * Hkv + kh;
+  const size_t dst_page = ((size_t)l * kv.n_pages + page) * Hkv + kh;
+  const T* sk = static_cast<const T*>(kv.seg_k) + src_page * 16 * hd;
+  const T* sv = static_cast<const T*>(kv.seg_v) + src_page * 16 * hd;
+  T* dk = static_cast<T*>(kv.k) + dst_page * 16 * hd;
+  T* dv = static_cast<T*>(kv.v) + dst_page * 16 * hd;
+  for (int e = threadIdx.x; e < hd; e += blockDim.x) {
+    dk[sl * hd + e] = sk[ss * hd + e];
+    dv[e * 16 + sl] = sv[e * 16 + ss];
+  }
+}
+
+__global__ void commit_state_kernel(TreeDims td, sb_seqs sq, sb_accept_out acc,
+                                    CommitInfo ci, const float* __restrict__ taps) {
+  const int s = blockIdx.x;
+  const int cur = ci.cur[s];
+  const float* src = taps + ((size_t)s * td.budget + cur) * 3 * td.d;
+  float* dst = sq.cond_taps + (size_t)s * 3 * td.d;
+  for (int e = threadIdx.x; e < 3 * td.d; e += blockDim.x) dst[e] = src[e];
+  if (threadIdx.x == 0) {
+    sq.T[s] = ci.T_old[s] + ci.a[s] + 1;
+    sq.root[s] = acc.bonus[s];
+  }
+}
+
+// Prefill of sequence s, chunk [a, a + n): target rows (causal chain).
+__global__ void plan_prefill_target_kernel(int S, int s, int a, int n,
+                                           const int* __restrict__ prompt,
+                                           int ld, CallPlan p) {
+  if (threadIdx.x == 0) {
+    for (int q = 0; q <= S; ++q) p.seq_off[q] = q <= s ? 0 : n;
+    for (int q = 0; q < S; ++q) {
+      p.prefix_len[q] = q == s ? a : 0;
+      p.seg_len[q] = q == s ? n : 0;
+    }
+    *p.n = n;
+  }
+  for (int j = threadIdx.x; j < n; j += blockDim.x) {
+    p.seq[j] = s;
+    p.slot[j] = j;
+    p.pos[j] = a + j;
+    p.token[j] = prompt[(size_t)s * ld + a + j];
+    p.k[j] = 1;
+    p.pred[j] = j;
+    p.cond[j] = -1;
+    p.out_row[j] = 1 + j;          // taps slot in the prefill tap buffer
+    p.kv_dst[j] = a + j;
+    for (int w = 0; w < p.vis_words; ++w) {
+      uint32_t bits = 0u;
+      for (int q = 32 * w; q < 32 * w + 32 && q <= j; ++q) bits |= 1u << (q & 31);
+      p.vis[(size_t)j * p.vis_words + w] = bits;
+    }
+  }
+}
+
+// Prefill drafter catch-up rows for positions a+1 .. a+n: row r is a K = 1
+// block started at position a + r with token x_{a+r}, conditioned on the
+// target taps of position a + r - 1 (tap buffer slot r; none for position 1).
+__global__ void plan_prefill_draft_kernel(int S, int s, int a, int n,
+                                          const int* __restrict__ prompt,
+                                          int ld, CallPlan p,
+                                          int* __restrict__ n_aux) {
+  if (threadIdx.x == 0) {
+    for (int q = 0; q <= S; ++q) p.seq_off[q] = q <= s ? 0 : n;
+    for (int q = 0; q < S; ++q) {
+      p.prefix_len[q] = q == s ? a : 0;
+      p.seg_len[q] = q == s ? n : 0;
+    }
+    *p.n = n;
+    *n_aux = n;
+  }
+  for (int r = threadIdx.x; r < n; r += blockDim.x) {
+    p.seq[r] = s;
+    p.slot[r] = r;
+    p.pos[r] = a + 1 + r;
+    p.token[r] = prompt[(size_t)s * ld + a + r];
+    p.k[r] = 1;
+    p.pred[r] = r;
+    p.cond[r] = (a + r >= 1) ? r : -1;
+    p.out_row[r] = -1;
+    p.kv_dst[r] = a + r;
+    for (int w = 0; w < p.vis_words; ++w) {
+      uint32_t bits = 0u;
+      for (int q = 32 * w; q < 32 * w + 32 && q <= r; ++q) bits |= 1u << (q & 31);
+      p.vis[(size_t)r * p.vis_words + w] = bits;
+    }
+  }
+}
+
+// Prefill end of sequence s: T = len, root = argmax of the last row,
+// cond_taps = taps of position len - 1 (tap buffer slot n_last).
+__global__ void prefill_finish_kernel(sb_seqs sq, int s, int len, int d,
+                                      const float* __restrict__ taps_pf,
+                                      int n_last, const int* __restrict__ root_arg) {
+  float* dst = sq.cond_taps + (size_t)s * 3 * d;
+  const float* src = taps_pf + (size_t)n_last * 3 * d;
+  for (int e = threadIdx.x; e < 3 * d; e += blockDim.x) dst[e] = src[e];
+  if (threadIdx.x == 0) {
+    sq.T[s] = len;
+    sq.root[s] = root_arg[0];
+  }
+}
+
+__global__ void copy_f32_kernel(float* __restrict__ dst, const float* __restrict__ src,
+                                int n) {
+  for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < n; e += gridDim.x * blockDim.x)
+    dst[e] = src[e];
+}
+
+__global__ void set_int_kernel(int* __restrict__ p, int v) { *p = v; }
+
+__global__ void export_rows_kernel(CallPlan p, int out_cap,
+                                   int* __restrict__ call_seq,
+                                   int* __restrict__ call_row,
+                                   int* __restrict__ n_call) {
+  const int n = *p.n;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < out_cap;
+       i += gridDim.x * blockDim.x) {
+    call_seq[i] = i < n ? p.seq[i] : -1;
+    call_row[i] = i < n ? p.slot[i] : -1;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) *n_call = n;
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+
+void launch_block1_reset(const TreeDims& td, const sb_tree& t, const int* root,
+                         int* n_aux, hipStream_t st) {
+  block1_reset_kernel<<<1, 64, 0, st>>>(td, t, root, n_aux);
+}
+void launch_plan_block(const TreeDims& td, int m, const sb_tree& t,
+                       const int* T, const CallPlan& p, int* blk_row0,
+                       int* blk_nst, hipStream_t st) {
+  plan_block_kernel<<<1, 256, 0, st>>>(td, m, t, T, p, blk_row0, blk_nst);
+}
+void launch_attach(const TreeDims& td, const sb_tree& t, const sb_draft_out& o,
+                   const int* blk_row0, const int* blk_nst, hipStream_t st) {
+  attach_kernel<<<td.S, 64, 0, st>>>(td, t, o.topk_id, o.topk_logit, o.lse,
+                                     o.bucket, o.branch, blk_row0, blk_nst);
+}
+void launch_plan_verify(const TreeDims& td, const sb_tree& t, const int* T,
+                        const CallPlan& p, hipStream_t st) {
+  plan_verify_kernel<<<1, 256, 0, st>>>(td, t, T, p);
+}
+void launch_accept(const TreeDims& td, const sb_tree& t, const int* argmax,
+                   const sb_accept_out& o, hipStream_t st) {
+  accept_kernel<<<td.S, 64, 0, st>>>(td, t, argmax, o);
+}
+void launch_commit_plan(const TreeDims& td, const sb_tree& t,
+                        const sb_accept_out& acc, const int* T,
+                        const CommitInfo& ci, const CallPlan& fb,
+                        int* taps_idx, int* n_aux, hipStream_t st) {
+  commit_plan_kernel<<<1, 64, 0, st>>>(td, t, acc, T, ci, fb, taps_idx, n_aux);
+}
+template <typename T>
+void launch_commit_copy(const TreeDims& td, const sb_tree& t,
+                        const sb_accept_out& acc, const CommitInfo& ci,
+                        bool drafter, const KVPools& kv, int pool_seqs,
+                        int n_layers, int Hkv, int hd, hipStream_t st) {
+  dim3 grid(td.S, td.M * td.K + 1, n_layers * Hkv);
+  commit_copy_kernel<T><<<grid, 128, 0, st>>>(td, t, acc, ci, drafter ? 1 : 0,
+                                              kv, pool_seqs, Hkv, hd);
+}
+template <typename T>
+void launch_seg_to_cache(const CallPlan& p, const KVPools& kv, int S,
+                         int n_layers, int Hkv, int hd, hipStream_t st) {
+  dim3 grid(p.cap, n_layers * Hkv);
+  seg_to_cache_kernel<T><<<grid, 128, 0, st>>>(p, kv, S, Hkv, hd);
+}
+void launch_commit_state(const TreeDims& td, const sb_seqs& sq,
+                         const sb_accept_out& acc, const CommitInfo& ci,
+                         const float* taps, hipStream_t st) {
+  commit_state_kernel<<<td.S, 256, 0, st>>>(td, sq, acc, ci, taps);
+}
+void launch_plan_prefill_target(int S, int s, int a, int n, const int* prompt,
+                                int ld, const CallPlan& p, hipStream_t st) {
+  plan_prefill_target_kernel<<<1, 256, 0, st>>>(S, s, a, n, prompt, ld, p);
+}
+void launch_plan_prefill_draft(int S, int s, int a, int n, const int* prompt,
+                               int ld, const CallPlan& p, int* n_aux,
+                               hipStream_t st) {
+  plan_prefill_draft_kernel<<<1, 256, 0, st>>>(S, s, a, n, prompt, ld, p, n_aux);
+}
+void launch_prefill_finish(const sb_seqs& sq, int s, int len, int d,
+                           const float* taps_pf, int n_last,
+                           const int* root_arg, hipStream_t st) {
+  prefill_finish_kernel<<<1, 256, 0, st>>>(sq, s, len, d, taps_pf, n_last,
+                                           root_arg);
+}
+void launch_copy_f32(float* dst, const float* src, int n, hipStream_t st) {
+  copy_f32_kernel<<<(n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024, 256, 0,
+                    st>>>(dst, src, n);
+}
+void launch_set_int(int* p, int v, hipStream_t st) {
+  set_int_kernel<<<1, 1, 0, st>>>(p, v);
+}
+void launch_export_rows(const CallPlan& p, int out_cap, int* call_seq,
+                        int* call_row, int* n_call, hipStream_t st) {
+  export_rows_kernel<<<(out_cap + 255) / 256, 256, 0, st>>>(
+      p, out_cap, call_seq, call_row, n_call);
+}
+
+template void launch_commit_copy<float>(const TreeDims&, const sb_tree&,
+                                        const sb_accept_out&, const CommitInfo&,
+                                        bool, const KVPools&, int, int, int,
+                                        int, hipStream_t);
+template void launch_commit_copy<bf16_t>(const TreeDims&, const sb_tree&,
+                                         const sb_accept_out&,
+                                         const CommitInfo&, bool,
+                                         const KVPools&, int, int, int, int,
+                                         hipStream_t);
+template void launch_seg_to_cache<float>(const CallPlan&, const KVPools&, int,
+                                         int, int, int, hipStream_t);
+template void launch_seg_to_cache<bf16_t>(const CallPlan&, const KVPools&, int,
+                                          int, int, int, hipStream_t);
+
+}  // namespace sb

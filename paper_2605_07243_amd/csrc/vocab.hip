@@ -1,0 +1,308 @@
+// Vocabulary-wide reductions over fp32 logits: top-k with ties to the
+// smaller id, max, sum exp(z - max) and sum exp(z - max) z, merged exactly
+// across chunks; then psi (App. B), the rank head (Eq. 4) and branching for
+// drafter rows, or the greedy argmax for verified nodes.
+#include <float.h>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace sb {
+
+// Partial record per (row, chunk): KT values, KT ids (int bits), m, s, u.
+template <int KT>
+__device__ __forceinline__ void topk_insert(float (&tv)[KT], int (&ti)[KT],
+                                            float v, int id) {
+  if (!better(v, id, tv[KT - 1], ti[KT - 1])) return;
+  tv[KT - 1] = v;
+  ti[KT - 1] = id;
+#pragma unroll
+  for (int j = KT - 1; j > 0; --j) {
+    if (better(tv[j], ti[j], tv[j - 1], ti[j - 1])) {
+      const float a = tv[j];
+      tv[j] = tv[j - 1];
+      tv[j - 1] = a;
+      const int b = ti[j];
+      ti[j] = ti[j - 1];
+      ti[j - 1] = b;
+    }
+  }
+}
+
+__device__ __forceinline__ void stats_merge(float& m, float& s, float& u,
+                                            float m2, float s2, float u2) {
+  const float M = fmaxf(m, m2);
+  const float a = (s > 0.f) ? __expf(m - M) : 0.f;
+  const float b = (s2 > 0.f) ? __expf(m2 - M) : 0.f;
+  s = s * a + s2 * b;
+  u = u * a + u2 * b;
+  m = M;
+}
+
+// Wave-wide best (value, smaller id); every lane gets the winner.
+__device__ __forceinline__ void wave_best(float& v, int& id) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float v2 = __shfl_xor(v, o, SB_WAVE);
+    const int i2 = __shfl_xor(id, o, SB_WAVE);
+    if (better(v2, i2, v, id)) {
+      v = v2;
+      id = i2;
+    }
+  }
+}
+
+// Pops the wave-wide top KT of per-lane sorted lists into (bv, bi).
+template <int KT>
+__device__ __forceinline__ void wave_topk(float (&tv)[KT], int (&ti)[KT],
+                                          float (&bv)[KT], int (&bi)[KT]) {
+#pragma unroll
+  for (int k = 0; k < KT; ++k) {
+    float v = tv[0];
+    int id = ti[0];
+    wave_best(v, id);
+    bv[k] = v;
+    bi[k] = id;
+    if (ti[0] == id && tv[0] == v) {      // the owner pops its head
+#pragma unroll
+      for (int j = 0; j < KT - 1; ++j) {
+        tv[j] = tv[j + 1];
+        ti[j] = ti[j + 1];
+      }
+      tv[KT - 1] = -FLT_MAX;
+      ti[KT - 1] = 0x7FFFFFFF;
+    }
+  }
+}
+
+template <int KT>
+__global__ __launch_bounds__(256) void vocab_partial_kernel(
+    const float* __restrict__ logits, const int* __restrict__ n, int V,
+    int chunk, float* __restrict__ part) {
+  const int i = blockIdx.y;
+  if (i >= *n) return;
+  const int c = blockIdx.x;
+  const int v0 = c * chunk, v1 = min(V, v0 + chunk);
+  const float* z = logits + (size_t)i * V;
+  float tv[KT];
+  int ti[KT];
+#pragma unroll
+  for (int k = 0; k < KT; ++k) {
+    tv[k] = -FLT_MAX;
+    ti[k] = 0x7FFFFFFF;
+  }
+  float m = -FLT_MAX, s = 0.f, u = 0.f;
+  for (int j = v0 + threadIdx.x; j < v1; j += blockDim.x) {
+    const float x = z[j];
+    if (x > m) {
+      const float a = __expf(m - x);
+      s = s * a + 1.f;
+      u = u * a + x;
+      m = x;
+    } else {
+      const float e = __expf(x - m);
+      s += e;
+      u += e * x;
+    }
+    topk_insert<KT>(tv, ti, x, j);
+  }
+  // block merge: stats via LDS, top-k wave by wave
+  __shared__ float sm[4], ss[4], su[4];
+  __shared__ float cv[4][KT];
+  __shared__ int ci[4][KT];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float m2 = __shfl_xor(m, o, SB_WAVE);
+    const float s2 = __shfl_xor(s, o, SB_WAVE);
+    const float u2 = __shfl_xor(u, o, SB_WAVE);
+    stats_merge(m, s, u, m2, s2, u2);
+  }
+  float bv[KT];
+  int bi[KT];
+  wave_topk<KT>(tv, ti, bv, bi);
+  if (lane == 0) {
+    sm[w] = m;
+    ss[w] = s;
+    su[w] = u;
+#pragma unroll
+    for (int k = 0; k < KT; ++k) {
+      cv[w][k] = bv[k];
+      ci[w][k] = bi[k];
+    }
+  }
+  __syncthreads();
+  if (w == 0) {
+    // lanes 0..3 hold the four waves' sorted lists
+    float lv[KT];
+    int li[KT];
+#pragma unroll
+    for (int k = 0; k < KT; ++k) {
+      lv[k] = lane < 4 ? cv[lane][k] : -FLT_MAX;
+      li[k] = lane < 4 ? ci[lane][k] : 0x7FFFFFFF;
+    }
+    wave_topk<KT>(lv, li, bv, bi);
+    if (lane == 0) {
+      float M = sm[0], S = ss[0], U = su[0];
+      for (int q = 1; q < 4; ++q) stats_merge(M, S, U, sm[q], ss[q], su[q]);
+      float* o = part + ((size_t)i * gridDim.x + c) * (2 * KT + 3);
+#pragma unroll
+      for (int k = 0; k < KT; ++k) {
+        o[k] = bv[k];
+        o[KT + k] = __int_as_float(bi[k]);
+      }
+      o[2 * KT] = M;
+      o[2 * KT + 1] = S;
+      o[2 * KT + 2] = U;
+    }
+  }
+}
+
+void launch_vocab_partial(const float* logits, const int* n, int cap, int V,
+                          int n_chunks, int topk, float* part,
+                          hipStream_t st) {
+  const int chunk = (V + n_chunks - 1) / n_chunks;
+  dim3 grid(n_chunks, cap);
+  if (topk == 1)
+    vocab_partial_kernel<1><<<grid, 256, 0, st>>>(logits, n, V, chunk, part);
+  else
+    vocab_partial_kernel<SB_TOPK_K><<<grid, 256, 0, st>>>(logits, n, V, chunk,
+                                                          part);
+}
+
+// Merge the chunk records of row i inside wave 0: top KT, m, s, u.
+template <int KT>
+__device__ __forceinline__ void merge_row(const float* __restrict__ part,
+                                          int n_chunks, float (&bv)[KT],
+                                          int (&bi)[KT], float& M, float& S,
+                                          float& U) {
+  const int lane = threadIdx.x & 63;
+  float tv[KT];
+  int ti[KT];
+#pragma unroll
+  for (int k = 0; k < KT; ++k) {
+    tv[k] = -FLT_MAX;
+    ti[k] = 0x7FFFFFFF;
+  }
+  float m = -FLT_MAX, s = 0.f, u = 0.f;
+  for (int c = lane; c < n_chunks; c += SB_WAVE) {
+    const float* o = part + (size_t)c * (2 * KT + 3);
+#pragma unroll
+    for (int k = 0; k < KT; ++k) topk_insert<KT>(tv, ti, o[k], __float_as_int(o[KT + k]));
+    stats_merge(m, s, u, o[2 * KT], o[2 * KT + 1], o[2 * KT + 2]);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float m2 = __shfl_xor(m, o, SB_WAVE);
+    const float s2 = __shfl_xor(s, o, SB_WAVE);
+    const float u2 = __shfl_xor(u, o, SB_WAVE);
+    stats_merge(m, s, u, m2, s2, u2);
+  }
+  wave_topk<KT>(tv, ti, bv, bi);
+  M = m;
+  S = s;
+  U = u;
+}
+
+// Drafter rows: psi = [log p of top-10, z1-z2, z1-z3, z1-z5, p1, entropy],
+// rank-head scores W_r [h^(L), psi] + b_r, bucket = argmax (ties low),
+// branch = map[bucket].  Also stores h^(L) into the tree's row cache.
+__global__ __launch_bounds__(256) void draft_finalize_kernel(
+    const float* __restrict__ part, int n_chunks, CallPlan p,
+    const float* __restrict__ x, const float* __restrict__ rank_w,
+    const float* __restrict__ rank_b, int d, int4 bmap, DraftRowOut out) {
+  __shared__ float psi_s[SB_PSI];
+  __shared__ float red[4][4];
+  const int i = blockIdx.x;
+  if (i >= *p.n) return;
+  const int o = p.out_row[i];
+  if (threadIdx.x < 64) {
+    float bv[SB_TOPK_K];
+    int bi[SB_TOPK_K];
+    float M, S, U;
+    merge_row<SB_TOPK_K>(part + (size_t)i * n_chunks * (2 * SB_TOPK_K + 3),
+                         n_chunks, bv, bi, M, S, U);
+    if (threadIdx.x == 0) {
+      const float lse = M + logf(S);
+      const float ent = lse - U / S;
+      for (int k = 0; k < SB_TOPK_K; ++k) {
+        out.topk_id[(size_t)o * SB_TOPK_K + k] = bi[k];
+        out.topk_logit[(size_t)o * SB_TOPK_K + k] = bv[k];
+        psi_s[k] = bv[k] - lse;
+      }
+      psi_s[10] = bv[0] - bv[1];
+      psi_s[11] = bv[0] - bv[2];
+      psi_s[12] = bv[0] - bv[4];
+      psi_s[13] = __expf(bv[0] - lse);
+      psi_s[14] = ent;
+      out.lse[o] = lse;
+      for (int k = 0; k < SB_PSI; ++k) out.psi[(size_t)o * SB_PSI + k] = psi_s[k];
+    }
+  }
+  __syncthreads();
+  const float* xr = x + (size_t)i * d;
+  float* hl = out.h_last + (size_t)o * d;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  const int ld = d + SB_PSI;
+  for (int j = threadIdx.x; j < d; j += blockDim.x) {
+    const float v = xr[j];
+    hl[j] = v;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[b] += rank_w[(size_t)b * ld + j] * v;
+  }
+  if (threadIdx.x < SB_PSI) {
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+      acc[b] += rank_w[(size_t)b * ld + d + threadIdx.x] * psi_s[threadIdx.x];
+  }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const float t = wave_sum(acc[b]);
+    if (lane == 0) red[w][b] = t;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int best = 0;
+    float bs = 0.f;
+    for (int b = 0; b < 4; ++b) {
+      const float sc = red[0][b] + red[1][b] + red[2][b] + red[3][b] + rank_b[b];
+      if (b == 0 || sc > bs) {
+        bs = sc;
+        best = b;
+      }
+    }
+    const int map[4] = {bmap.x, bmap.y, bmap.z, bmap.w};
+    out.bucket[o] = best;
+    out.branch[o] = map[best];
+  }
+}
+
+void launch_draft_finalize(const float* part, int n_chunks, const CallPlan& p,
+                           const float* x, const float* rank_w,
+                           const float* rank_b, int d, int4 bmap,
+                           DraftRowOut o, hipStream_t st) {
+  draft_finalize_kernel<<<p.cap, 256, 0, st>>>(part, n_chunks, p, x, rank_w,
+                                               rank_b, d, bmap, o);
+}
+
+__global__ __launch_bounds__(64) void verify_finalize_kernel(
+    const float* __restrict__ part, int n_chunks, const int* __restrict__ n,
+    const int* __restrict__ out_row, int* __restrict__ argmax) {
+  const int i = blockIdx.x;
+  if (i >= *n) return;
+  float bv[1];
+  int bi[1];
+  float M, S, U;
+  merge_row<1>(part + (size_t)i * n_chunks * 5, n_chunks, bv, bi, M, S, U);
+  if (threadIdx.x == 0 && out_row[i] >= 0) argmax[out_row[i]] = bi[0];
+}
+
+void launch_verify_finalize(const float* part, int n_chunks, const int* n,
+                            int cap, const int* out_row, int* argmax,
+                            hipStream_t st) {
+  verify_finalize_kernel<<<cap, 64, 0, st>>>(part, n_chunks, n, out_row,
+                                             argmax);
+}
+
+}  // namespace sb
