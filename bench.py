@@ -1,0 +1,273 @@
+#!/usr/bin/env python
+"""SpecBlock hot-path benchmark on one MI355X.
+
+A step is one verifier iteration of the whole hot path on the
+Llama-3-8B-shaped workload (random-init bf16 target, 32 layers, d 4096,
+32/8 heads, MLP 14336, vocab 128256; one-layer drafter of the same shape;
+K = 4, M = 2 block expansions, tree budget 60, batch 1, prompt of 1024
+uniform-random ids): M sb_draft_block_expand calls, sb_tree_verify,
+sb_accept and sb_commit, with inputs resident in HBM.
+
+Prints one JSON line: value = committed (accepted + bonus) tokens per second
+over the timed steps; block-expansion steps/s and tree-attention HBM GB/s
+from HIP events on the library's stream; the roofline of the dominant
+kernel (the weight-streaming projection GEMM); and the CPU oracle timed on a
+bounded sample of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = ("block-expansion steps/s + tree-attn HBM GB/s; accepted tokens/s "
+          "(8B-shape)")
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def attn_bytes(w, T_avg, n_nodes, rows_block, es):
+    """Algorithmic bytes of the tree-attention launches of one iteration:
+    every prefix K/V entry and every segment entry read once per layer, Q
+    read and O written once per row."""
+    s = w.target
+    kv_entry = 2 * s.n_kv_heads * s.head_dim * es
+    q_row = s.n_heads * s.head_dim * es * 2
+    verify = s.n_layers * (T_avg * kv_entry + n_nodes * kv_entry
+                           + n_nodes * q_row)
+    draft = 0.0
+    for rows in rows_block:
+        draft += w.drafter_layers * (T_avg * kv_entry + rows * kv_entry
+                                     + rows * q_row)
+    return verify + draft
+
+
+def cpu_baseline(w, T, budget_s=30.0):
+    """Time the CPU oracle on a bounded sample of the workload: one block-1
+    and one block-2 expansion (the real drafter shape, prefix T), one verify
+    decoder layer over a budget-sized tree and the target LM head over the
+    same rows; the iteration time is the drafter time + n_layers x layer time
+    + LM head time (the other layers repeat the measured one)."""
+    import dataclasses
+
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import synth
+    from oracle import specdec
+    from oracle.model import Drafter, Target, decoder_layer
+    from oracle.numerics import rmsnorm
+
+    w1 = synth.with_layers(w, 1)
+    w1 = dataclasses.replace(w1, target=dataclasses.replace(w1.target),
+                             prompt_len=(T, T))
+    t0 = time.perf_counter()
+    tw = synth.target_weights(w1, seed=0)
+    dw = synth.drafter_weights(w1, seed=0)
+    tgt = Target(tw, w1.target, w1.dtype, (0, 0, 0))
+    dr = Drafter(dw, w1.target, w1.dtype, w1.drafter_layers, tgt.embed)
+    del tw, dw
+    log(f"cpu baseline: weights ready in {time.perf_counter() - t0:.1f}s")
+    s = w1.target
+    rng = np.random.default_rng(7)
+    st = specdec.SeqState([], T, int(rng.integers(s.vocab)),
+                          tgt.new_prefix(), dr.new_prefix(),
+                          rng.standard_normal((3, s.d_model)))
+    k, v = synth.random_kv(1, "bench.t", T, s, w1.dtype)
+    st.tkv.k[0], st.tkv.v[0] = k.astype(np.float64), v.astype(np.float64)
+    k, v = synth.random_kv(1, "bench.d", T, s, w1.dtype)
+    st.dkv.k[0], st.dkv.v[0] = k.astype(np.float64), v.astype(np.float64)
+    # drafter: M expansions of the real iteration
+    tree = specdec.DraftTree(st.root, w1.budget)
+    rows = []
+    seg = dr.new_segment(w1.rows_per_seq)
+    starts = [specdec.Start(0, st.root, st.T, dr.cond_from_taps(st.cond_taps),
+                            [])]
+    t_draft = 0.0
+    for m in range(1, w1.M + 1):
+        if not starts:
+            break
+        t = time.perf_counter()
+        rec = specdec.expand_block(dr, st, tree, rows, seg, starts, w1.K, m,
+                                   w1.branch_map)
+        if m < w1.M:
+            picks = specdec.select_starts(tree, rows, rec["alive"],
+                                          rec["chain"], rec["first_new"],
+                                          w1.B_max)
+            starts = [specdec.start_from_node(tree, rows, st, n)
+                      for n in picks]
+        t_draft += time.perf_counter() - t
+    # one verify layer over the tree, then the LM head over the same rows
+    n = len(tree)
+    tseg = tgt.new_segment(n)
+    x = tgt.embed[[nd.token for nd in tree.nodes]]
+    pos = np.array([st.T + nd.depth for nd in tree.nodes])
+    t = time.perf_counter()
+    x = decoder_layer(tgt.layers[0], x, pos, np.arange(n),
+                      [tree.anc_or_self(i) for i in range(n)], st.tkv.k[0],
+                      st.tkv.v[0], tseg.k[0], tseg.v[0], s, tgt.num)
+    t_layer = time.perf_counter() - t
+    t = time.perf_counter()
+    z = tgt.num.act(rmsnorm(x, tgt.final_norm, s.norm_eps)) @ tgt.lm_head.T
+    _ = [specdec.argmax_low(r) for r in z]
+    t_lm = time.perf_counter() - t
+    t_iter = t_draft + w.target.n_layers * t_layer + t_lm
+    blas = [i.get("num_threads") for i in threadpool_info()
+            if i.get("user_api") == "blas"]
+    cores = int(max(blas)) if blas else 1
+    measured = t_draft + t_layer + t_lm
+    return {
+        "value": round(1.0 / t_iter, 4),
+        "unit": "tokens/s",
+        "cores": cores,
+        "kind": "oracle",
+        "sample": (f"float64 oracle, {w1.M} block expansions ({len(rows)} "
+                   f"drafter rows, prefix {T}) + 1 of {w.target.n_layers} "
+                   f"verify layers over {n} nodes + LM head, measured "
+                   f"{measured:.1f}s; iteration = drafter + "
+                   f"{w.target.n_layers} x layer + LM head = {t_iter:.1f}s, "
+                   f"1 committed token per iteration (random weights)"),
+        "block_expansion_steps_per_s": round(w1.M / t_draft, 4),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama3-8b-k4")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (got --gpus "
+              f"{args.gpus}); the multi-GPU sharding plan is design-only",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import synth
+    from paper_2605_07243_amd.runtime import Runtime
+
+    w = synth.WORKLOADS[args.workload]
+    es = 2 if w.dtype == "bf16" else 4
+    log(f"workload {w.name}: allocating and generating weights on device")
+    t = time.perf_counter()
+    rt = Runtime(w, None, seed=0)
+    torch.cuda.synchronize()
+    log(f"weights + buffers in {time.perf_counter() - t:.1f}s")
+    prompts = synth.prompts(w)
+    t = time.perf_counter()
+    rt.prefill(prompts)
+    torch.cuda.synchronize()
+    log(f"prefill {sum(len(p) for p in prompts)} tokens in "
+        f"{time.perf_counter() - t:.2f}s")
+    for i in range(args.warmup):
+        rt.iteration()
+    torch.cuda.synchronize()
+    log("warmup done")
+
+    stream = torch.cuda.current_stream()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)]
+          for _ in range(args.steps)]
+    T0 = rt.T.clone()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        for m in range(1, w.M + 1):
+            rt.expand(m)
+        ev[i][1].record(stream)
+        rt.verify()
+        rt.accept()
+        rt.commit()
+        ev[i][2].record(stream)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    committed = int((rt.T - T0).sum())
+    draft_ms = sum(e[0].elapsed_time(e[1]) for e in ev)
+    rest_ms = sum(e[1].elapsed_time(e[2]) for e in ev)
+    log(f"timed {args.steps} steps in {dt:.3f}s: {committed} tokens, "
+        f"draft {draft_ms / args.steps:.3f} ms/step, verify+accept+commit "
+        f"{rest_ms / args.steps:.3f} ms/step")
+
+    # second pass over the same work with per-kernel HIP events
+    Tp0 = rt.T.clone()
+    rows_block = []
+    rt.profile(True)
+    for i in range(args.steps):
+        for m in range(1, w.M + 1):
+            rt.expand(m)
+            rows_block.append(int(rt.dout["n_call"][0]))
+        rt.verify()
+        rt.accept()
+        rt.commit()
+    torch.cuda.synchronize()
+    rt.profile(False)
+    prof = rt.profile_read()
+    Tp1 = rt.T.clone()
+    T_avg = float((Tp0.sum() + Tp1.sum()) / 2 / rt.S)
+    n_nodes = int(rt.tree["n_nodes"].sum())
+    gemm = prof["gemm"]
+    gemm_gbps = gemm["bytes"] / (gemm["ms"] * 1e-3) / 1e9
+    ab = sum(attn_bytes(w, T_avg, n_nodes, rows_block[i * w.M:(i + 1) * w.M],
+                        es) for i in range(args.steps))
+    attn = prof["tree_attn"]
+    attn_gbps = ab / (attn["ms"] * 1e-3) / 1e9
+    log(f"gemm {gemm['launches']} launches {gemm['ms']:.2f} ms "
+        f"{gemm_gbps:.0f} GB/s; tree-attn {attn['launches']} launches "
+        f"{attn['ms']:.2f} ms {attn_gbps:.0f} GB/s; vocab "
+        f"{prof['vocab']['ms']:.2f} ms")
+
+    out = {
+        "metric": METRIC,
+        "value": round(committed / dt, 3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(dt * 1e3 / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic: random-init N(0,0.02) weights, uniform random "
+                "prompt ids",
+        "config": {"workload": w.name, "target": "Llama-3-8B-shaped",
+                   "n_seqs": w.n_seqs, "prompt_len": list(w.prompt_len),
+                   "K": w.K, "M": w.M, "B_max": w.B_max,
+                   "budget": w.budget, "branch_map": list(w.branch_map),
+                   "buckets": "natural (random rank head)"},
+        "block_expansion_steps_per_s": round(w.M * args.steps /
+                                             (draft_ms * 1e-3), 2),
+        "tree_attn_gbps": round(attn_gbps, 1),
+        "tree_attn_frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
+        "accepted_tokens_per_s": round(committed / dt, 3),
+        "tau": round(committed / (args.steps * rt.S), 3),
+        "roofline": {"kernel": "gemm_xwt (weight-streaming projections)",
+                     "bound": "hbm", "achieved": round(gemm_gbps, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(gemm_gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": None,
+                     "launches_per_step": gemm["launches"] // args.steps,
+                     "avg_launch_us": round(gemm["ms"] * 1e3 /
+                                            max(gemm["launches"], 1), 2)},
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        try:
+            out["cpu_baseline"] = cpu_baseline(w, max(w.prompt_len))
+        except MemoryError as e:
+            out["cpu_baseline"] = {"error": f"oracle sample did not fit: {e}"}
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -267,6 +267,25 @@ int sb_commit(sb_ctx* ctx, sb_seqs* seqs, const sb_tree* tree,
               const sb_verify_out* verify, const sb_accept_out* acc,
               sb_kv* target_kv, sb_kv* draft_kv, void* stream);
 
+/* Kernel timing.  While enabled, the library brackets every launch of the
+ * projection GEMM, the tree attention (split kernel + merge) and the
+ * vocabulary reduction with HIP events on the call's stream and accumulates
+ * per class: launches, event-measured milliseconds and, for the GEMM, the
+ * algorithmic bytes (weights + activation rows in + fp32 rows out, counted
+ * at the call's row capacity) and flops.  sb_profile(ctx, 1) resets and
+ * starts, sb_profile(ctx, 0) stops; sb_profile_read waits for the recorded
+ * events and fills out[SB_PROF_N]. */
+enum sb_prof_class { SB_PROF_GEMM = 0, SB_PROF_ATTN = 1, SB_PROF_VOCAB = 2,
+                     SB_PROF_N = 3 };
+typedef struct sb_kernel_stat {
+  int64_t launches;
+  double total_ms;
+  double bytes;
+  double flops;
+} sb_kernel_stat;
+int sb_profile(sb_ctx* ctx, int32_t enable);
+int sb_profile_read(sb_ctx* ctx, sb_kernel_stat* out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -87,9 +87,17 @@ class AcceptOut(C.Structure):
     _fields_ = [("path", vp), ("n_accepted", vp), ("bonus", vp)]
 
 
+class KernelStat(C.Structure):
+    _fields_ = [("launches", C.c_int64), ("total_ms", C.c_double),
+                ("bytes", C.c_double), ("flops", C.c_double)]
+
+
+PROF_CLASSES = ("gemm", "tree_attn", "vocab")
+
 EXPORTS = ["sb_row_capacity", "sb_workspace_bytes", "sb_create", "sb_destroy",
            "sb_last_error", "sb_bind", "sb_prefill", "sb_draft_block_expand",
-           "sb_tree_verify", "sb_accept", "sb_commit"]
+           "sb_tree_verify", "sb_accept", "sb_commit", "sb_profile",
+           "sb_profile_read"]
 
 _lib = None
 
@@ -131,6 +139,10 @@ def load(path: str = LIB_PATH):
     lib.sb_commit.argtypes = [vp, P(Seqs), P(Tree), P(VerifyOut),
                               P(AcceptOut), P(KV), P(KV), vp]
     lib.sb_commit.restype = C.c_int
+    lib.sb_profile.argtypes = [vp, i32]
+    lib.sb_profile.restype = C.c_int
+    lib.sb_profile_read.argtypes = [vp, P(KernelStat)]
+    lib.sb_profile_read.restype = C.c_int
     _lib = lib
     return lib
 

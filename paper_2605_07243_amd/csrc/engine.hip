@@ -121,6 +121,19 @@ struct sb_ctx {
   void* dseg_k = nullptr;
   void* dseg_v = nullptr;
   int* zero = nullptr;
+  // kernel timing
+  struct ProfRec {
+    int cls;
+    hipEvent_t a, b;
+    double bytes, flops;
+  };
+  bool prof = false;
+  std::vector<hipEvent_t> ev_pool;
+  size_t ev_used = 0;
+  std::vector<ProfRec> recs;
+  ~sb_ctx() {
+    for (hipEvent_t e : ev_pool) (void)hipEventDestroy(e);
+  }
 };
 
 static thread_local std::string g_create_err;
@@ -395,10 +408,44 @@ int hip_check(sb_ctx* c, const char* where) {
   return SB_OK;
 }
 
+hipEvent_t next_event(sb_ctx* c) {
+  if (c->ev_used == c->ev_pool.size()) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    c->ev_pool.push_back(e);
+  }
+  return c->ev_pool[c->ev_used++];
+}
+
+// Brackets one or more launches with events when profiling is on.
+struct ProfScope {
+  sb_ctx* c;
+  hipStream_t st;
+  int cls;
+  double bytes, flops;
+  hipEvent_t a = nullptr;
+  ProfScope(sb_ctx* c_, hipStream_t st_, int cls_, double bytes_ = 0,
+            double flops_ = 0)
+      : c(c_), st(st_), cls(cls_), bytes(bytes_), flops(flops_) {
+    if (c->prof && (a = next_event(c)) != nullptr) (void)hipEventRecord(a, st);
+  }
+  ~ProfScope() {
+    if (!a) return;
+    hipEvent_t b = next_event(c);
+    if (!b) return;
+    (void)hipEventRecord(b, st);
+    c->recs.push_back({cls, a, b, bytes, flops});
+  }
+};
+
 template <typename T>
 int gemm(sb_ctx* c, const void* X, int ldx, const void* W, int N, int K,
          const int* n, int m_cap, hipStream_t st) {
   const int ks = gemm_ksplit(N, K, c->D.ksplit_cap);
+  const double es = sizeof(T);
+  ProfScope ps(c, st, SB_PROF_GEMM,
+               (double)N * K * es + (double)m_cap * K * es + (double)m_cap * N * 4,
+               2.0 * m_cap * N * K);
   return launch_gemm_xwt<T>(static_cast<const T*>(X), ldx,
                             static_cast<const T*>(W), N, K, c->P,
                             (size_t)c->D.R_cap * N, n, m_cap, ks, st);
@@ -441,9 +488,12 @@ void layer_body(sb_ctx* c, const sb_layer_weights& lw, int layer,
   kv.seg_pages = pf.seg_pages;
   const int max_prefix = c->cfg.max_pages * 16;
   const int n_split = std::max(1, std::min(D.n_split, ceil_div(max_prefix, 256)));
-  launch_tree_attn<T>(static_cast<const T*>(c->q), p, kv, rows_per_seq, D.H,
-                      D.Hkv, D.hd, n_split, max_prefix, c->o_part, c->ml, A,
-                      st);
+  {
+    ProfScope ps(c, st, SB_PROF_ATTN);
+    launch_tree_attn<T>(static_cast<const T*>(c->q), p, kv, rows_per_seq, D.H,
+                        D.Hkv, D.hd, n_split, max_prefix, c->o_part, c->ml, A,
+                        st);
+  }
   ks = gemm<T>(c, A, D.H * D.hd, lw.w_o, D.d, D.H * D.hd, p.n, R, st);
   launch_residual<T>(c->x, c->P, ks, (size_t)D.R_cap * D.d, p.n, R, D.d, true,
                      lw.mlp_norm ? static_cast<const float*>(lw.mlp_norm) : nullptr,
@@ -531,6 +581,10 @@ template <typename T>
 void lm_head(sb_ctx* c, const void* A, const void* W, float* logits,
              const int* n, int cap, hipStream_t st) {
   const Dims& D = c->D;
+  const double es = sizeof(T);
+  ProfScope ps(c, st, SB_PROF_GEMM,
+               (double)D.V * D.d * es + (double)cap * D.d * es + (double)cap * D.V * 4,
+               2.0 * cap * D.V * D.d);
   launch_gemm_xwt<T>(static_cast<const T*>(A), D.d, static_cast<const T*>(W),
                      D.V, D.d, logits, (size_t)cap * D.V, n, cap, 1, st);
 }
@@ -560,16 +614,19 @@ int draft_expand_impl(sb_ctx* c, int m, const sb_seqs* sq, const sb_kv* dkv,
   drafter_forward<T>(c, p, cond_base, pf, D.B_max * D.K, true, st);
   float* logits = o->logits ? o->logits : c->logits;
   lm_head<T>(c, c->A, c->dw.lm_head, logits, p.n, p.cap, st);
-  launch_vocab_partial(logits, p.n, p.cap, D.V, D.n_chunks, SB_TOPK, c->vpart,
-                       st);
-  const DraftRowOut ro{o->topk_id, o->topk_logit, o->lse, o->psi, o->bucket,
-                       o->branch, t->h_last, D.row_cap};
-  const int4 bmap = make_int4(c->cfg.branch_map[0], c->cfg.branch_map[1],
-                              c->cfg.branch_map[2], c->cfg.branch_map[3]);
-  launch_draft_finalize(c->vpart, D.n_chunks, p, c->x,
-                        static_cast<const float*>(c->dw.rank_w),
-                        static_cast<const float*>(c->dw.rank_b), D.d, bmap, ro,
-                        st);
+  {
+    ProfScope ps(c, st, SB_PROF_VOCAB);
+    launch_vocab_partial(logits, p.n, p.cap, D.V, D.n_chunks, SB_TOPK,
+                         c->vpart, st);
+    const DraftRowOut ro{o->topk_id, o->topk_logit, o->lse, o->psi,
+                         o->bucket, o->branch, t->h_last, D.row_cap};
+    const int4 bmap = make_int4(c->cfg.branch_map[0], c->cfg.branch_map[1],
+                                c->cfg.branch_map[2], c->cfg.branch_map[3]);
+    launch_draft_finalize(c->vpart, D.n_chunks, p, c->x,
+                          static_cast<const float*>(c->dw.rank_w),
+                          static_cast<const float*>(c->dw.rank_b), D.d, bmap,
+                          ro, st);
+  }
   launch_attach(td, *t, *o, c->blk_row0, c->blk_nst, st);
   return hip_check(c, "sb_draft_block_expand");
 }
@@ -586,9 +643,12 @@ int verify_impl(sb_ctx* c, const sb_seqs* sq, const sb_tree* t,
   target_forward<T>(c, p, pf, D.budget, out->taps, st);
   float* logits = out->logits ? out->logits : c->logits;
   lm_head<T>(c, c->A, c->tw.lm_head, logits, p.n, p.cap, st);
-  launch_vocab_partial(logits, p.n, p.cap, D.V, D.n_chunks, 1, c->vpart, st);
-  launch_verify_finalize(c->vpart, D.n_chunks, p.n, p.cap, p.out_row,
-                         out->argmax, st);
+  {
+    ProfScope ps(c, st, SB_PROF_VOCAB);
+    launch_vocab_partial(logits, p.n, p.cap, D.V, D.n_chunks, 1, c->vpart, st);
+    launch_verify_finalize(c->vpart, D.n_chunks, p.n, p.cap, p.out_row,
+                           out->argmax, st);
+  }
   return hip_check(c, "sb_tree_verify");
 }
 
@@ -788,6 +848,38 @@ int sb_prefill(sb_ctx* c, const sb_seqs* seqs, const int32_t* prompt,
   }
   return is_bf16(c) ? prefill_impl<bf16_t>(c, seqs, prompt, ld_prompt, lens, target_kv, draft_kv, S_(stream))
                     : prefill_impl<float>(c, seqs, prompt, ld_prompt, lens, target_kv, draft_kv, S_(stream));
+}
+
+}  // extern "C"
+
+extern "C" {
+
+int sb_profile(sb_ctx* c, int32_t enable) {
+  if (!c) return SB_EINVAL;
+  if (enable) {
+    c->recs.clear();
+    c->ev_used = 0;
+  }
+  c->prof = enable != 0;
+  return SB_OK;
+}
+
+int sb_profile_read(sb_ctx* c, sb_kernel_stat* out) {
+  if (!c || !out) return SB_EINVAL;
+  for (int i = 0; i < SB_PROF_N; ++i) out[i] = sb_kernel_stat{0, 0.0, 0.0, 0.0};
+  for (const auto& r : c->recs) {
+    if (hipEventSynchronize(r.b) != hipSuccess)
+      return fail(c, SB_EHIP, "hipEventSynchronize failed");
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess)
+      return fail(c, SB_EHIP, "hipEventElapsedTime failed");
+    sb_kernel_stat& k = out[r.cls];
+    k.launches += 1;
+    k.total_ms += ms;
+    k.bytes += r.bytes;
+    k.flops += r.flops;
+  }
+  return SB_OK;
 }
 
 }  // extern "C"

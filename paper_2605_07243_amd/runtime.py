@@ -277,6 +277,16 @@ class Runtime:
         self.accept()
         self.commit()
 
+    def profile(self, enable: bool):
+        self._check(self.lib.sb_profile(self.ctx, 1 if enable else 0))
+
+    def profile_read(self) -> dict:
+        arr = (B.KernelStat * 3)()
+        self._check(self.lib.sb_profile_read(self.ctx, arr))
+        return {name: dict(launches=arr[i].launches, ms=arr[i].total_ms,
+                           bytes=arr[i].bytes, flops=arr[i].flops)
+                for i, name in enumerate(B.PROF_CLASSES)}
+
     # ------------------------------------------------------------------
     # cache access for tests (host <-> device copies of single entries)
     def _pool(self, which):
