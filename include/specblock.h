@@ -267,6 +267,14 @@ int sb_commit(sb_ctx* ctx, sb_seqs* seqs, const sb_tree* tree,
               const sb_verify_out* verify, const sb_accept_out* acc,
               sb_kv* target_kv, sb_kv* draft_kv, void* stream);
 
+/* Upper bound of T over all sequences, used to size the tree-attention
+ * split of the committed prefix.  sb_prefill sets it to the longest prompt
+ * + 1 and every sb_commit raises it by M K + 1; a caller that writes T or
+ * the caches itself must call this with a valid bound, or with 0 (unknown:
+ * the page-table capacity max_pages * 16 is assumed).  A bound below the
+ * true T makes attention skip the entries beyond it. */
+int sb_set_length_bound(sb_ctx* ctx, int32_t max_T);
+
 /* Kernel timing.  While enabled, the library brackets every launch of the
  * projection GEMM, the tree attention (split kernel + merge) and the
  * vocabulary reduction with HIP events on the call's stream and accumulates

@@ -96,8 +96,8 @@ PROF_CLASSES = ("gemm", "tree_attn", "vocab")
 
 EXPORTS = ["sb_row_capacity", "sb_workspace_bytes", "sb_create", "sb_destroy",
            "sb_last_error", "sb_bind", "sb_prefill", "sb_draft_block_expand",
-           "sb_tree_verify", "sb_accept", "sb_commit", "sb_profile",
-           "sb_profile_read"]
+           "sb_tree_verify", "sb_accept", "sb_commit", "sb_set_length_bound",
+           "sb_profile", "sb_profile_read"]
 
 _lib = None
 
@@ -139,6 +139,8 @@ def load(path: str = LIB_PATH):
     lib.sb_commit.argtypes = [vp, P(Seqs), P(Tree), P(VerifyOut),
                               P(AcceptOut), P(KV), P(KV), vp]
     lib.sb_commit.restype = C.c_int
+    lib.sb_set_length_bound.argtypes = [vp, i32]
+    lib.sb_set_length_bound.restype = C.c_int
     lib.sb_profile.argtypes = [vp, i32]
     lib.sb_profile.restype = C.c_int
     lib.sb_profile_read.argtypes = [vp, P(KernelStat)]

@@ -13,7 +13,7 @@
 // query - exactly the B operand of O^T += V^T P^T - so the online softmax
 // needs only a 4-lane reduction and P never leaves registers.  V pages are
 // stored transposed ([hd][16 slots]) so the V^T operand is two 8/16-byte
-// loads.  Splits are combined by attn_merge with log-sum-exp weights.
+// loads.  Splits are combined with log-sum-exp weights.
 #include "common.h"
 #include "kernels.h"
 
@@ -21,114 +21,39 @@ namespace sb {
 
 #define SB_NEG (-1.0e30f)
 
-template <typename T, int HD>
-__device__ __forceinline__ void attn_tile(
-    const T* __restrict__ k_base0, const T* __restrict__ k_base1,
-    const T* __restrict__ v_base0, const T* __restrict__ v_base1,
-    bool ok0, bool ok1, const Frag8<T> (&qf)[HD / 32], uint32_t valid_bits,
-    float scale, float& m_run, float& l_run, f32x4_t (&acc)[HD / 16]) {
-  const int lane = threadIdx.x & 63;
-  const int r = lane & 15, g = lane >> 4;
-  // S^T for the two 16-key halves
-  f32x4_t s[2];
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    s[h] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    const T* kb = h ? k_base1 : k_base0;
-    const bool ok = h ? ok1 : ok0;
-#pragma unroll
-    for (int c = 0; c < HD / 32; ++c) {
-      Frag8<T> kf;
-      if (ok)
-        kf.load(kb + (size_t)r * HD + c * 32 + g * 8);
-      else
-        kf.zero();
-      s[h] = mma_16x16x32(kf, qf[c], s[h]);
-    }
-  }
-  // lane holds keys 16h + 4g + rr for query r; bit (16h + 4g + rr) of
-  // valid_bits says whether that key is visible to this lane's query.
-  float sc[8];
-  float mx = SB_NEG;
-#pragma unroll
-  for (int h = 0; h < 2; ++h)
-#pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
-      const int kk = 16 * h + 4 * g + rr;
-      const bool v = (valid_bits >> kk) & 1u;
-      const float x = v ? s[h][rr] * scale : SB_NEG;
-      sc[h * 4 + rr] = x;
-      mx = fmaxf(mx, x);
-    }
-  mx = fmaxf(mx, __shfl_xor(mx, 16, SB_WAVE));
-  mx = fmaxf(mx, __shfl_xor(mx, 32, SB_WAVE));
-  const float m_new = fmaxf(m_run, mx);
-  const float alpha = __expf(m_run - m_new);
-  float p[8];
-  float ps = 0.f;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int kk = 16 * (e >> 2) + 4 * g + (e & 3);
-    const bool v = (valid_bits >> kk) & 1u;
-    p[e] = v ? __expf(sc[e] - m_new) : 0.f;
-    ps += p[e];
-  }
-  ps += __shfl_xor(ps, 16, SB_WAVE);
-  ps += __shfl_xor(ps, 32, SB_WAVE);
-  l_run = l_run * alpha + ps;
-  m_run = m_new;
-#pragma unroll
-  for (int c = 0; c < HD / 16; ++c) acc[c] *= alpha;
-  // P^T operand (keys {4g..4g+3, 16+4g..16+4g+3} x query r)
-  Frag8<T> pf;
-  if constexpr (sizeof(T) == 2) {
-    uint32_t w[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
-      w[e] = (uint32_t)f32_to_bf16(p[2 * e]) |
-             ((uint32_t)f32_to_bf16(p[2 * e + 1]) << 16);
-    pf.v = make_uint4(w[0], w[1], w[2], w[3]);
-  } else {
-    pf.a = make_float4(p[0], p[1], p[2], p[3]);
-    pf.b = make_float4(p[4], p[5], p[6], p[7]);
-  }
-  // V^T operand: hd row 16c + r, the same 8 keys
-#pragma unroll
-  for (int c = 0; c < HD / 16; ++c) {
-    Frag8<T> vf;
-    const size_t off = ((size_t)(16 * c + r)) * 16 + 4 * g;
-    if constexpr (sizeof(T) == 2) {
-      uint2 a = ok0 ? *reinterpret_cast<const uint2*>(v_base0 + off)
-                    : make_uint2(0, 0);
-      uint2 b = ok1 ? *reinterpret_cast<const uint2*>(v_base1 + off)
-                    : make_uint2(0, 0);
-      vf.v = make_uint4(a.x, a.y, b.x, b.y);
-    } else {
-      vf.a = ok0 ? *reinterpret_cast<const float4*>(v_base0 + off)
-                 : make_float4(0.f, 0.f, 0.f, 0.f);
-      vf.b = ok1 ? *reinterpret_cast<const float4*>(v_base1 + off)
-                 : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-    acc[c] = mma_16x16x32(vf, pf, acc[c]);
-  }
-}
-
-template <typename T, int HD>
-__global__ __launch_bounds__(64) void tree_attn_kernel(
-    const T* __restrict__ q, CallPlan p, KVView kv, int n_seqs, int H,
-    int Hkv, int split_tokens, float scale, float* __restrict__ o_part,
-    float* __restrict__ ml) {
+// One workgroup = NQ waves = NQ q-tiles of 16 query vectors of one KV head,
+// one split of the prefix (the last split also takes the segment).  K and V
+// tiles of 32 keys are staged once per workgroup in LDS (double buffered;
+// global loads run four tiles ahead in registers) and read by every wave.
+// With several splits each workgroup writes (O, m, l) partials that
+// attn_merge combines; with one split the kernel writes the output.
+template <typename T, int HD, int NQ>
+__global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
+    const T* __restrict__ q, CallPlan p, KVView kv, int H, int Hkv,
+    int split_tokens, float scale, float* __restrict__ o_part,
+    float* __restrict__ ml, T* __restrict__ out) {
+  constexpr int ES = sizeof(T);
+  constexpr int LDK = HD + 16 / ES;                 // padded K row
+  constexpr int LDV = 32 + 16 / ES;                 // padded V^T row
+  constexpr int KCH = 32 * HD * ES / 16;            // 16-byte chunks per K tile
+  constexpr int VCH = HD * 32 * ES / 16;            // ... per V tile
+  constexpr int CPR = HD * ES / 16;                 // chunks per K row
+  constexpr int VCR = 16 * ES / 16;                 // chunks per V page row
+  constexpr int NT = NQ * 64;
+  constexpr int PER = (KCH + VCH + NT - 1) / NT;
+  __shared__ __attribute__((aligned(16))) T ksh[2][32][LDK];
+  __shared__ __attribute__((aligned(16))) T vsh[2][HD][LDV];
   const int s = blockIdx.y / Hkv, kh = blockIdx.y % Hkv;
-  if (s >= n_seqs) return;
   const int G = H / Hkv;
   const int row0 = p.seq_off[s];
-  const int nrows = p.seq_off[s + 1] - row0;
-  const int qv0 = blockIdx.x * 16;
-  if (qv0 >= nrows * G) return;
-  const int lane = threadIdx.x;
+  const int nq = (p.seq_off[s + 1] - row0) * G;
+  const int qg = blockIdx.x;
+  if (qg * NQ * 16 >= nq) return;                   // uniform for the group
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int r = lane & 15, g = lane >> 4;
-  const int qv = qv0 + r;
-  const bool qvalid = qv < nrows * G;
+  const int qv = (qg * NQ + wave) * 16 + r;
+  const bool qvalid = qv < nq;
+  const bool wave_live = (qg * NQ + wave) * 16 < nq;
   const int qrow = row0 + (qvalid ? qv / G : 0);
   const int qh = kh * G + (qvalid ? qv % G : 0);
 
@@ -143,91 +68,295 @@ __global__ __launch_bounds__(64) void tree_attn_kernel(
 #pragma unroll
   for (int c = 0; c < HD / 16; ++c) acc[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  const size_t page_elems = (size_t)Hkv * 16 * HD;
   const T* kpool = static_cast<const T*>(kv.k);
   const T* vpool = static_cast<const T*>(kv.v);
+  const T* skp = static_cast<const T*>(kv.seg_k);
+  const T* svp = static_cast<const T*>(kv.seg_v);
   const int* ptab = kv.page_table + (size_t)s * kv.max_pages;
   const int Tp = min(p.prefix_len[s], kv.max_pages * 16);
   const int t0 = blockIdx.z * split_tokens;
   const int t1 = min(Tp, t0 + split_tokens);
-  // the lane's query sees every prefix key < Tp: one bit per key of a tile
-  for (int k0 = t0; k0 < t1; k0 += 32) {
-    const int pg0 = k0 >> 4, pg1 = pg0 + 1;
-    const bool ok0 = k0 < t1, ok1 = k0 + 16 < t1;
-    const int pa = min(max(ok0 ? ptab[pg0] : 0, 0), kv.n_pages - 1);
-    const int pb = min(max(ok1 ? ptab[pg1] : 0, 0), kv.n_pages - 1);
-    const size_t b0 = ((size_t)pa * Hkv + kh) * 16 * HD;
-    const size_t b1 = ((size_t)pb * Hkv + kh) * 16 * HD;
-    const int nvalid = t1 - k0;
-    const uint32_t bits = nvalid >= 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
-    attn_tile<T, HD>(kpool + b0, kpool + b1, vpool + b0, vpool + b1, ok0,
-                     ok1, qf, bits, scale, m_run, l_run, acc);
-  }
-  if (blockIdx.z == gridDim.z - 1) {
-    const int L = min(p.seg_len[s], kv.seg_pages * 16);
-    const T* sk = static_cast<const T*>(kv.seg_k);
-    const T* sv = static_cast<const T*>(kv.seg_v);
+  const bool last_split = blockIdx.z == gridDim.z - 1;
+  const int L = last_split ? min(p.seg_len[s], kv.seg_pages * 16) : 0;
+  const int n_pre = t1 > t0 ? (t1 - t0 + 31) / 32 : 0;
+  const int n_tiles = n_pre + (L + 31) / 32;
+  // this lane's visibility words (segment tile j uses word j) and the
+  // split's page-table entries, read once so that no tile fetch waits on a
+  // dependent global load
+  uint32_t vw[SB_MAX_ANC_WORDS];
+  {
     const uint32_t* vis = p.vis + (size_t)qrow * p.vis_words;
-    for (int k0 = 0; k0 < L; k0 += 32) {
-      const int pg0 = k0 >> 4, pg1 = pg0 + 1;
-      const bool ok0 = pg0 < kv.seg_pages, ok1 = pg1 < kv.seg_pages && k0 + 16 < L;
-      const size_t b0 =
-          (((size_t)s * kv.seg_pages + (ok0 ? pg0 : 0)) * Hkv + kh) * 16 * HD;
-      const size_t b1 =
-          (((size_t)s * kv.seg_pages + (ok1 ? pg1 : 0)) * Hkv + kh) * 16 * HD;
+#pragma unroll
+    for (int w = 0; w < SB_MAX_ANC_WORDS; ++w)
+      vw[w] = (qvalid && w < p.vis_words && L > 0) ? vis[w] : 0u;
+  }
+  constexpr int MAXP = 512;
+  __shared__ int pg_sh[MAXP];
+  const int pg0 = t0 >> 4;
+  const int n_pg = t1 > t0 ? ((t1 + 15) >> 4) - pg0 : 0;
+  for (int j = tid; j < n_pg && j < MAXP; j += NT)
+    pg_sh[j] = min(max(ptab[pg0 + j], 0), kv.n_pages - 1);
+  __syncthreads();
+
+  // page base (element offset) of half h of tile i, or -1 when empty
+  auto page_base = [&](int i, int h) -> long long {
+    if (i < n_pre) {
+      const int k = t0 + i * 32 + h * 16;
+      if (k >= t1) return -1;
+      const int j = (k >> 4) - pg0;
+      const int pg = j < MAXP ? pg_sh[j]
+                              : min(max(ptab[k >> 4], 0), kv.n_pages - 1);
+      return ((long long)pg * Hkv + kh) * 16 * HD;
+    }
+    const int k = (i - n_pre) * 32 + h * 16;
+    if (k >= L || (k >> 4) >= kv.seg_pages) return -1;
+    return (((long long)s * kv.seg_pages + (k >> 4)) * Hkv + kh) * 16 * HD;
+  };
+  // register ring of DEPTH tiles in flight; slot = tile index mod DEPTH
+  constexpr int DEPTH = 4;
+  uint4 stg[DEPTH][PER];
+  auto fetch = [&](int i, uint4 (&dst)[PER]) {
+    const bool seg = i >= n_pre;
+    const T* kp = seg ? skp : kpool;
+    const T* vp = seg ? svp : vpool;
+    const long long b0 = page_base(i, 0), b1 = page_base(i, 1);
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      const int c = tid + e * NT;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (c < KCH) {
+        const int key = c / CPR, part = c % CPR;
+        const long long b = key < 16 ? b0 : b1;
+        if (b >= 0)
+          v = *reinterpret_cast<const uint4*>(kp + b + (key & 15) * HD + part * (16 / ES));
+      } else if (c < KCH + VCH) {
+        const int cc = c - KCH;
+        const int hd = cc / (2 * VCR), rem = cc % (2 * VCR);
+        const int h = rem / VCR, part = rem % VCR;
+        const long long b = h ? b1 : b0;
+        if (b >= 0)
+          v = *reinterpret_cast<const uint4*>(vp + b + hd * 16 + part * (16 / ES));
+      }
+      dst[e] = v;
+    }
+  };
+  auto stash = [&](int buf, const uint4 (&src)[PER]) {
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      const int c = tid + e * NT;
+      if (c < KCH) {
+        const int key = c / CPR, part = c % CPR;
+        *reinterpret_cast<uint4*>(&ksh[buf][key][part * (16 / ES)]) = src[e];
+      } else if (c < KCH + VCH) {
+        const int cc = c - KCH;
+        const int hd = cc / (2 * VCR), rem = cc % (2 * VCR);
+        const int h = rem / VCR, part = rem % VCR;
+        *reinterpret_cast<uint4*>(&vsh[buf][hd][h * 16 + part * (16 / ES)]) = src[e];
+      }
+    }
+  };
+  auto compute = [&](int i, int buf) {
+    uint32_t bits;
+    if (i < n_pre) {
+      const int nvalid = t1 - (t0 + i * 32);
+      bits = nvalid >= 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
+    } else {
+      const int k0 = (i - n_pre) * 32;
       const int nvalid = L - k0;
-      uint32_t bits = nvalid >= 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
-      bits &= qvalid ? vis[k0 >> 5] : 0u;
-      attn_tile<T, HD>(sk + b0, sk + b1, sv + b0, sv + b1, ok0, ok1, qf, bits,
-                       scale, m_run, l_run, acc);
+      bits = nvalid >= 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
+      uint32_t word = 0u;
+#pragma unroll
+      for (int w = 0; w < SB_MAX_ANC_WORDS; ++w)
+        if (w == (k0 >> 5)) word = vw[w];
+      bits &= word;
+    }
+    if (!wave_live) return;
+    // S^T = K Q^T for the two 16-key halves
+    f32x4_t sc4[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      sc4[h] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < HD / 32; ++c) {
+        Frag8<T> kf;
+        kf.load(&ksh[buf][h * 16 + r][c * 32 + g * 8]);
+        sc4[h] = mma_16x16x32(kf, qf[c], sc4[h]);
+      }
+    }
+    float sc[8];
+    float mx = SB_NEG;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int kk = 16 * (e >> 2) + 4 * g + (e & 3);
+      const bool v = (bits >> kk) & 1u;
+      sc[e] = v ? sc4[e >> 2][e & 3] * scale : SB_NEG;
+      mx = fmaxf(mx, sc[e]);
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, SB_WAVE));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, SB_WAVE));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = __expf(m_run - m_new);
+    float pv[8];
+    float ps = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int kk = 16 * (e >> 2) + 4 * g + (e & 3);
+      pv[e] = ((bits >> kk) & 1u) ? __expf(sc[e] - m_new) : 0.f;
+      ps += pv[e];
+    }
+    ps += __shfl_xor(ps, 16, SB_WAVE);
+    ps += __shfl_xor(ps, 32, SB_WAVE);
+    l_run = l_run * alpha + ps;
+    m_run = m_new;
+#pragma unroll
+    for (int c = 0; c < HD / 16; ++c) acc[c] *= alpha;
+    Frag8<T> pf;
+    if constexpr (ES == 2) {
+      uint32_t w[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        w[e] = (uint32_t)f32_to_bf16(pv[2 * e]) |
+               ((uint32_t)f32_to_bf16(pv[2 * e + 1]) << 16);
+      pf.v = make_uint4(w[0], w[1], w[2], w[3]);
+    } else {
+      pf.a = make_float4(pv[0], pv[1], pv[2], pv[3]);
+      pf.b = make_float4(pv[4], pv[5], pv[6], pv[7]);
+    }
+#pragma unroll
+    for (int c = 0; c < HD / 16; ++c) {
+      Frag8<T> vf;
+      const T* vr = &vsh[buf][16 * c + r][4 * g];
+      if constexpr (ES == 2) {
+        const uint2 a = *reinterpret_cast<const uint2*>(vr);
+        const uint2 b = *reinterpret_cast<const uint2*>(vr + 16);
+        vf.v = make_uint4(a.x, a.y, b.x, b.y);
+      } else {
+        vf.a = *reinterpret_cast<const float4*>(vr);
+        vf.b = *reinterpret_cast<const float4*>(vr + 16);
+      }
+      acc[c] = mma_16x16x32(vf, pf, acc[c]);
+    }
+  };
+#pragma unroll
+  for (int d = 0; d < DEPTH; ++d)
+    if (d < n_tiles) fetch(d, stg[d]);
+  if (n_tiles > 0) stash(0, stg[0]);
+  __syncthreads();
+  // tile i lives in slot i % DEPTH; after it is stashed, the slot is refilled
+  // with tile i + DEPTH
+  for (int i0 = 0; i0 < n_tiles; i0 += DEPTH) {
+#pragma unroll
+    for (int d = 0; d < DEPTH; ++d) {
+      const int i = i0 + d;
+      if (i < n_tiles) {
+        if (i + DEPTH < n_tiles) fetch(i + DEPTH, stg[d]);
+        compute(i, i & 1);
+        if (i + 1 < n_tiles) stash((i + 1) & 1, stg[(d + 1) % DEPTH]);
+        __syncthreads();
+      }
     }
   }
-  if (!qvalid) return;
-  const size_t cap = p.cap;
-  float* o = o_part + (((size_t)blockIdx.z * cap + qrow) * H + qh) * HD;
+  (void)page_elems;
+
+  const int n_split = gridDim.z;
+  if (n_split == 1) {
+    if (!qvalid) return;
+    const float il = l_run > 0.f ? 1.0f / l_run : 0.f;
+    T* o = out + (size_t)qrow * H * HD + (size_t)qh * HD;
 #pragma unroll
-  for (int c = 0; c < HD / 16; ++c)
-    *reinterpret_cast<float4*>(o + 16 * c + 4 * g) =
-        make_float4(acc[c][0], acc[c][1], acc[c][2], acc[c][3]);
-  if (g == 0) {
-    float* mlp = ml + (((size_t)blockIdx.z * cap + qrow) * H + qh) * 2;
-    mlp[0] = m_run;
-    mlp[1] = l_run;
+    for (int c = 0; c < HD / 16; ++c)
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr)
+        o[16 * c + 4 * g + rr] = Elem<T>::from_f32(acc[c][rr] * il);
+    return;
+  }
+  const size_t cap = p.cap;
+  if (qvalid) {
+    float* o = o_part + (((size_t)blockIdx.z * cap + qrow) * H + qh) * HD;
+#pragma unroll
+    for (int c = 0; c < HD / 16; ++c)
+      *reinterpret_cast<float4*>(o + 16 * c + 4 * g) =
+          make_float4(acc[c][0], acc[c][1], acc[c][2], acc[c][3]);
+    if (g == 0) {
+      float* mlp = ml + (((size_t)blockIdx.z * cap + qrow) * H + qh) * 2;
+      mlp[0] = m_run;
+      mlp[1] = l_run;
+    }
   }
 }
 
+
 // Combine the splits of every (row, head): out = sum_z w_z O_z / sum_z w_z l_z
-// with w_z = exp(m_z - max m).
-template <typename T>
-__global__ __launch_bounds__(256) void attn_merge_kernel(
+// with w_z = exp(m_z - max m).  A separate launch: the kernel boundary
+// orders the partial writes of every XCD before the reads.
+template <int NS>
+__global__ __launch_bounds__(256) void attn_merge_kernel_t(
     const float* __restrict__ o_part, const float* __restrict__ ml,
     const int* __restrict__ n, int cap, int H, int hd, int n_split,
-    T* __restrict__ out) {
-  __shared__ float wgt[64][32];
+    void* out_v, int es) {
+  __shared__ float wgt[64][NS];
   __shared__ float inv_l[64];
   const int i = blockIdx.x;
   if (i >= *n) return;
   for (int h = threadIdx.x; h < H; h += blockDim.x) {
+    float mz[NS], lz[NS];
     float mx = SB_NEG;
-    for (int z = 0; z < n_split; ++z)
-      mx = fmaxf(mx, ml[(((size_t)z * cap + i) * H + h) * 2]);
+#pragma unroll
+    for (int z = 0; z < NS; ++z) {
+      float2 e = make_float2(SB_NEG, 0.f);
+      if (z < n_split)
+        e = *reinterpret_cast<const float2*>(ml + (((size_t)z * cap + i) * H + h) * 2);
+      mz[z] = e.x;
+      lz[z] = e.y;
+      if (e.y > 0.f) mx = fmaxf(mx, e.x);
+    }
     float L = 0.f;
-    for (int z = 0; z < n_split; ++z) {
-      const float* e = ml + (((size_t)z * cap + i) * H + h) * 2;
-      const float w = (e[1] > 0.f) ? __expf(e[0] - mx) : 0.f;
+#pragma unroll
+    for (int z = 0; z < NS; ++z) {
+      const float w = lz[z] > 0.f ? __expf(mz[z] - mx) : 0.f;
       wgt[h][z] = w;
-      L += w * e[1];
+      L += w * lz[z];
     }
     inv_l[h] = L > 0.f ? 1.0f / L : 0.f;
   }
   __syncthreads();
-  for (int j = threadIdx.x; j < H * hd; j += blockDim.x) {
-    const int h = j / hd;
-    float v = 0.f;
-    for (int z = 0; z < n_split; ++z)
-      if (wgt[h][z] != 0.f) v += wgt[h][z] * o_part[((size_t)z * cap + i) * H * hd + j];
-    out[(size_t)i * H * hd + j] = Elem<T>::from_f32(v * inv_l[h]);
+  const size_t zs = (size_t)cap * H * hd;
+  for (int c = threadIdx.x; c < (H * hd) >> 2; c += blockDim.x) {
+    const int j = 4 * c, h = j / hd;
+    const float* base = o_part + (size_t)i * H * hd + j;
+    float4 o[NS];
+#pragma unroll
+    for (int z = 0; z < NS; ++z)
+      o[z] = z < n_split ? *reinterpret_cast<const float4*>(base + z * zs)
+                         : make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int z = 0; z < NS; ++z) {
+      const float w = wgt[h][z];
+      v.x += w * o[z].x;
+      v.y += w * o[z].y;
+      v.z += w * o[z].z;
+      v.w += w * o[z].w;
+    }
+    const float il = inv_l[h];
+    v = make_float4(v.x * il, v.y * il, v.z * il, v.w * il);
+    const size_t off = (size_t)i * H * hd + j;
+    if (es == 2) {
+      uint2 u;
+      u.x = (uint32_t)f32_to_bf16(v.x) | ((uint32_t)f32_to_bf16(v.y) << 16);
+      u.y = (uint32_t)f32_to_bf16(v.z) | ((uint32_t)f32_to_bf16(v.w) << 16);
+      *reinterpret_cast<uint2*>(static_cast<bf16_t*>(out_v) + off) = u;
+    } else {
+      *reinterpret_cast<float4*>(static_cast<float*>(out_v) + off) = v;
+    }
   }
 }
+
+template <typename T>
+void launch_attn_merge(const CallPlan& p, int H, int hd, int n_split,
+                       const float* o_part, const float* ml, T* out,
+                       hipStream_t st);
 
 template <typename T>
 void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
@@ -235,22 +364,47 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
                       int n_split, int max_prefix, float* o_part, float* ml,
                       T* out, hipStream_t st) {
   const int G = H / Hkv;
+  const int qtiles = (rows_per_seq_cap * G + 15) / 16;
+  const int nq = qtiles >= 8 ? 8 : (qtiles >= 4 ? 4 : (qtiles >= 2 ? 2 : 1));
+  const int n_qgroups = (qtiles + nq - 1) / nq;
   int split_tokens = (max_prefix + n_split - 1) / n_split;
   split_tokens = ((split_tokens + 31) / 32) * 32;
   if (split_tokens == 0) split_tokens = 32;
-  const int n_seqs = p.n_seqs;
-  dim3 grid((rows_per_seq_cap * G + 15) / 16, n_seqs * Hkv, n_split);
+  const dim3 grid(n_qgroups, p.n_seqs * Hkv, n_split);
   const float scale = 1.0f / sqrtf((float)hd);
-  if (hd == 128)
-    tree_attn_kernel<T, 128><<<grid, 64, 0, st>>>(q, p, kv, n_seqs, H, Hkv,
-                                                   split_tokens, scale, o_part,
-                                                   ml);
-  else
-    tree_attn_kernel<T, 64><<<grid, 64, 0, st>>>(q, p, kv, n_seqs, H, Hkv,
-                                                  split_tokens, scale, o_part,
-                                                  ml);
-  attn_merge_kernel<T><<<p.cap, 256, 0, st>>>(o_part, ml, p.n, p.cap, H, hd,
-                                              n_split, out);
+#define SB_ATTN(HD_, NQ_)                                                      \
+  if (hd == HD_ && nq == NQ_) {                                               \
+    tree_attn_kernel<T, HD_, NQ_><<<grid, NQ_ * 64, 0, st>>>(                 \
+        q, p, kv, H, Hkv, split_tokens, scale, o_part, ml, out);              \
+    if (n_split > 1) launch_attn_merge<T>(p, H, hd, n_split, o_part, ml, out, st); \
+    return;                                                                   \
+  }
+  SB_ATTN(128, 8) SB_ATTN(128, 4) SB_ATTN(128, 2) SB_ATTN(128, 1)
+  SB_ATTN(64, 8) SB_ATTN(64, 4) SB_ATTN(64, 2) SB_ATTN(64, 1)
+#undef SB_ATTN
+}
+
+template <typename T>
+void launch_attn_merge(const CallPlan& p, int H, int hd, int n_split,
+                       const float* o_part, const float* ml, T* out,
+                       hipStream_t st) {
+  // every split's (m, l) and partial row is loaded at once (no dependent
+  // chain); the template size is n_split rounded up, extra slots read as
+  // empty splits
+#define SB_MERGE(NS_)                                                          \
+  if (n_split <= NS_) {                                                       \
+    attn_merge_kernel_t<NS_><<<p.cap, 256, 0, st>>>(                          \
+        o_part, ml, p.n, p.cap, H, hd, n_split, out, sizeof(T));              \
+    return;                                                                   \
+  }
+  SB_MERGE(2) SB_MERGE(4) SB_MERGE(8) SB_MERGE(16) SB_MERGE(32)
+#undef SB_MERGE
+}
+
+int attn_qgroups(int rows_per_seq_cap, int G) {
+  const int qtiles = (rows_per_seq_cap * G + 15) / 16;
+  const int nq = qtiles >= 8 ? 8 : (qtiles >= 4 ? 4 : (qtiles >= 2 ? 2 : 1));
+  return (qtiles + nq - 1) / nq;
 }
 
 template void launch_tree_attn<float>(const float*, const CallPlan&,

@@ -58,12 +58,52 @@ void launch_rmsnorm(const float* x, const int* n, int cap, int d,
   rmsnorm_kernel<T><<<cap, 256, 0, st>>>(x, n, d, g, eps, out, ldo);
 }
 
+// Sum of the split-K partials (+ the residual stream), optionally the next
+// RMSNorm as the following projection's operand and the tap copies.  Each
+// thread keeps its float4 columns in registers between the two passes.
+template <typename T>
+__device__ __forceinline__ void store4(T* p, float4 v);
+template <>
+__device__ __forceinline__ void store4<float>(float* p, float4 v) {
+  *reinterpret_cast<float4*>(p) = v;
+}
+template <>
+__device__ __forceinline__ void store4<bf16_t>(bf16_t* p, float4 v) {
+  uint2 u;
+  u.x = (uint32_t)f32_to_bf16(v.x) | ((uint32_t)f32_to_bf16(v.y) << 16);
+  u.y = (uint32_t)f32_to_bf16(v.z) | ((uint32_t)f32_to_bf16(v.w) << 16);
+  *reinterpret_cast<uint2*>(p) = u;
+}
+
+__device__ __forceinline__ float4 add4(float4 a, float4 b) {
+  return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+}
+
+// sum_{s < ks} P[s] at float4 offset `off` (ks <= 16)
+__device__ __forceinline__ float4 sum_parts(const float* __restrict__ P,
+                                            size_t part_stride, int ks,
+                                            size_t off) {
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+  int s = 0;
+  for (; s + 4 <= ks; s += 4) {
+    const float4 p0 = *reinterpret_cast<const float4*>(P + (s + 0) * part_stride + off);
+    const float4 p1 = *reinterpret_cast<const float4*>(P + (s + 1) * part_stride + off);
+    const float4 p2 = *reinterpret_cast<const float4*>(P + (s + 2) * part_stride + off);
+    const float4 p3 = *reinterpret_cast<const float4*>(P + (s + 3) * part_stride + off);
+    a = add4(a, add4(add4(p0, p1), add4(p2, p3)));
+  }
+  for (; s < ks; ++s)
+    a = add4(a, *reinterpret_cast<const float4*>(P + s * part_stride + off));
+  return a;
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void residual_kernel(
     float* __restrict__ x, const float* __restrict__ P, int ks,
     size_t part_stride, const int* __restrict__ n, int d, int accumulate,
     const float* __restrict__ g, float eps, T* __restrict__ out, int ldo,
     float* __restrict__ taps, int tap_mask, const int* __restrict__ out_row) {
+  constexpr int MAXV = 8;   // d <= 8192 with 256 threads
   __shared__ float red[4];
   const int i = blockIdx.x;
   if (i >= *n) return;
@@ -71,19 +111,37 @@ __global__ __launch_bounds__(256) void residual_kernel(
   float* tr = nullptr;
   if (taps != nullptr && tap_mask != 0 && out_row[i] >= 0)
     tr = taps + (size_t)out_row[i] * 3 * d;
-  for (int j = threadIdx.x; j < d; j += blockDim.x) {
-    float v = accumulate ? xr[j] : 0.f;
-    for (int s = 0; s < ks; ++s) v += P[s * part_stride + (size_t)i * d + j];
-    xr[j] = v;
-    if (tr) {
-      if (tap_mask & 1) tr[j] = v;
-      if (tap_mask & 2) tr[d + j] = v;
-      if (tap_mask & 4) tr[2 * d + j] = v;
+  const int nv = d >> 2;
+  float4 v[MAXV];
+  float ss = 0.f;
+#pragma unroll
+  for (int q = 0; q < MAXV; ++q) {
+    const int c = threadIdx.x + q * 256;
+    if (c < nv) {
+      float4 a = sum_parts(P, part_stride, ks, (size_t)i * d + 4 * c);
+      if (accumulate) a = add4(a, reinterpret_cast<const float4*>(xr)[c]);
+      reinterpret_cast<float4*>(xr)[c] = a;
+      if (tr) {
+        if (tap_mask & 1) reinterpret_cast<float4*>(tr)[c] = a;
+        if (tap_mask & 2) reinterpret_cast<float4*>(tr + d)[c] = a;
+        if (tap_mask & 4) reinterpret_cast<float4*>(tr + 2 * d)[c] = a;
+      }
+      ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
+      v[q] = a;
     }
   }
-  if (g != nullptr) {
-    __syncthreads();
-    norm_row<T>(xr, d, g, eps, out + (size_t)i * ldo, red);
+  if (g == nullptr) return;
+  ss = block_sum(ss, red);
+  const float rs = 1.0f / sqrtf(ss / (float)d + eps);
+  T* o = out + (size_t)i * ldo;
+#pragma unroll
+  for (int q = 0; q < MAXV; ++q) {
+    const int c = threadIdx.x + q * 256;
+    if (c < nv) {
+      const float4 gg = reinterpret_cast<const float4*>(g)[c];
+      store4<T>(o + 4 * c, make_float4(v[q].x * rs * gg.x, v[q].y * rs * gg.y,
+                                       v[q].z * rs * gg.z, v[q].w * rs * gg.w));
+    }
   }
 }
 
@@ -99,56 +157,63 @@ void launch_residual(float* x, const float* P, int ks, size_t part_stride,
 
 // RoPE (rotate-half pairs (j, j + hd/2), angle pos * theta^(-2j/hd)) on the
 // Q and K heads of the summed QKV projection; Q -> q [cap][H][hd], K and V ->
-// the row's slot of its sequence's segment pages.
+// the row's slot of its sequence's segment pages.  Four pairs per thread.
 template <typename T>
 __global__ __launch_bounds__(256) void qkv_post_kernel(
     const float* __restrict__ P, int ks, size_t part_stride, CallPlan p, int H,
     int Hkv, int hd, float theta, T* __restrict__ q, T* __restrict__ seg_k,
     T* __restrict__ seg_v, int seg_pages) {
-  __shared__ float cs[128], sn[128];
+  __shared__ __attribute__((aligned(16))) float cs[128];
+  __shared__ __attribute__((aligned(16))) float sn[128];
   const int i = blockIdx.x;
   if (i >= *p.n) return;
   const int half = hd >> 1;
   const int ncol = (H + 2 * Hkv) * hd;
   const double pos = (double)p.pos[i];
   for (int j = threadIdx.x; j < half; j += blockDim.x) {
+    // angle in double, reduced to [-pi, pi] before the fp32 sincos
     const double inv = exp(-((double)(2 * j) / (double)hd) * log((double)theta));
-    double s, c;
-    sincos(pos * inv, &s, &c);
-    cs[j] = (float)c;
-    sn[j] = (float)s;
+    const double ang = pos * inv;
+    const double two_pi = 6.283185307179586476925287;
+    const float red = (float)(ang - two_pi * rint(ang / two_pi));
+    float sv, cv;
+    sincosf(red, &sv, &cv);
+    cs[j] = cv;
+    sn[j] = sv;
   }
   __syncthreads();
-  const float* Pr = P + (size_t)i * ncol;
-  auto col = [&](int c) {
-    float v = 0.f;
-    for (int s = 0; s < ks; ++s) v += Pr[s * part_stride + c];
-    return v;
-  };
+  const size_t row = (size_t)i * ncol;
   const int seq = p.seq[i], slot = p.slot[i];
   const int page = slot >> 4, sl = slot & 15;
   const size_t page_base = (size_t)seq * seg_pages + page;
-  // rotated pairs of the H query heads and Hkv key heads
-  for (int idx = threadIdx.x; idx < (H + Hkv) * half; idx += blockDim.x) {
-    const int head = idx / half, j = idx % half;
-    const float a = col(head * hd + j), b = col(head * hd + j + half);
-    const float ra = a * cs[j] - b * sn[j];
-    const float rb = b * cs[j] + a * sn[j];
+  const int q4 = half >> 2;
+  for (int idx = threadIdx.x; idx < (H + Hkv) * q4; idx += blockDim.x) {
+    const int head = idx / q4, j = (idx % q4) * 4;
+    const float4 a = sum_parts(P, part_stride, ks, row + head * hd + j);
+    const float4 b = sum_parts(P, part_stride, ks, row + head * hd + j + half);
+    const float4 c4 = *reinterpret_cast<const float4*>(&cs[j]);
+    const float4 s4 = *reinterpret_cast<const float4*>(&sn[j]);
+    const float4 ra = make_float4(a.x * c4.x - b.x * s4.x, a.y * c4.y - b.y * s4.y,
+                                  a.z * c4.z - b.z * s4.z, a.w * c4.w - b.w * s4.w);
+    const float4 rb = make_float4(b.x * c4.x + a.x * s4.x, b.y * c4.y + a.y * s4.y,
+                                  b.z * c4.z + a.z * s4.z, b.w * c4.w + a.w * s4.w);
+    T* dst;
     if (head < H) {
-      T* qr = q + ((size_t)i * H + head) * hd;
-      qr[j] = Elem<T>::from_f32(ra);
-      qr[j + half] = Elem<T>::from_f32(rb);
+      dst = q + ((size_t)i * H + head) * hd;
     } else {
-      const int kh = head - H;
-      T* kr = seg_k + ((page_base * Hkv + kh) * 16 + sl) * hd;
-      kr[j] = Elem<T>::from_f32(ra);
-      kr[j + half] = Elem<T>::from_f32(rb);
+      dst = seg_k + ((page_base * Hkv + (head - H)) * 16 + sl) * hd;
     }
+    store4<T>(dst + j, ra);
+    store4<T>(dst + j + half, rb);
   }
-  for (int idx = threadIdx.x; idx < Hkv * hd; idx += blockDim.x) {
-    const int kh = idx / hd, j = idx % hd;
-    const float v = col((H + Hkv) * hd + idx);
-    seg_v[((page_base * Hkv + kh) * hd + j) * 16 + sl] = Elem<T>::from_f32(v);
+  for (int idx = threadIdx.x; idx < Hkv * (hd >> 2); idx += blockDim.x) {
+    const int kh = idx / (hd >> 2), j = (idx % (hd >> 2)) * 4;
+    const float4 v = sum_parts(P, part_stride, ks, row + (H + Hkv) * hd + kh * hd + j);
+    T* dv = seg_v + ((page_base * Hkv + kh) * hd + j) * 16 + sl;
+    dv[0] = Elem<T>::from_f32(v.x);
+    dv[16] = Elem<T>::from_f32(v.y);
+    dv[32] = Elem<T>::from_f32(v.z);
+    dv[48] = Elem<T>::from_f32(v.w);
   }
 }
 
@@ -162,28 +227,30 @@ void launch_qkv_post(const float* P, int ks, size_t part_stride,
                                             seg_pages);
 }
 
+// out = silu(gate) * up, four columns per thread; grid (rows, F / 1024).
 template <typename T>
 __global__ __launch_bounds__(256) void swiglu_kernel(
     const float* __restrict__ P, int ks, size_t part_stride,
     const int* __restrict__ n, int F, T* __restrict__ out) {
   const int i = blockIdx.x;
   if (i >= *n) return;
-  const float* Pr = P + (size_t)i * 2 * F;
-  for (int j = threadIdx.x; j < F; j += blockDim.x) {
-    float gt = 0.f, up = 0.f;
-    for (int s = 0; s < ks; ++s) {
-      gt += Pr[s * part_stride + j];
-      up += Pr[s * part_stride + F + j];
-    }
-    const float si = gt / (1.0f + expf(-gt));
-    out[(size_t)i * F + j] = Elem<T>::from_f32(si * up);
-  }
+  const int j = (blockIdx.y * 256 + threadIdx.x) * 4;
+  if (j >= F) return;
+  const size_t row = (size_t)i * 2 * F;
+  const float4 gt = sum_parts(P, part_stride, ks, row + j);
+  const float4 up = sum_parts(P, part_stride, ks, row + F + j);
+  const float4 r = make_float4(gt.x / (1.0f + expf(-gt.x)) * up.x,
+                               gt.y / (1.0f + expf(-gt.y)) * up.y,
+                               gt.z / (1.0f + expf(-gt.z)) * up.z,
+                               gt.w / (1.0f + expf(-gt.w)) * up.w);
+  store4<T>(out + (size_t)i * F + j, r);
 }
 
 template <typename T>
 void launch_swiglu(const float* P, int ks, size_t part_stride, const int* n,
                    int cap, int F, T* out, hipStream_t st) {
-  swiglu_kernel<T><<<cap, 256, 0, st>>>(P, ks, part_stride, n, F, out);
+  swiglu_kernel<T><<<dim3(cap, (F + 1023) / 1024), 256, 0, st>>>(
+      P, ks, part_stride, n, F, out);
 }
 
 // Layer-wise shift operand (Eq. 3): [h_k, h_{k-1}] with h_0 := h_1.

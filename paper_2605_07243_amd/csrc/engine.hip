@@ -68,8 +68,8 @@ Dims derive(const sb_config& c) {
   D.tpages = ceil_div(std::max(D.budget, D.chunk), 16);
   D.dpages = ceil_div(std::max(D.row_cap, D.chunk), 16);
   D.n_chunks = std::max(1, std::min(64, D.V / 2048));
-  D.ksplit_cap = 8;
-  D.n_split = 16;
+  D.ksplit_cap = 16;
+  D.n_split = 32;
   // partial-sum buffer: the largest ks * N over the projections
   size_t mx = 0;
   auto upd = [&](int N, int Kd) {
@@ -121,6 +121,8 @@ struct sb_ctx {
   void* dseg_k = nullptr;
   void* dseg_v = nullptr;
   int* zero = nullptr;
+  // running upper bound of every sequence's T (0: unknown)
+  int T_bound = 0;
   // kernel timing
   struct ProfRec {
     int cls;
@@ -441,7 +443,7 @@ struct ProfScope {
 template <typename T>
 int gemm(sb_ctx* c, const void* X, int ldx, const void* W, int N, int K,
          const int* n, int m_cap, hipStream_t st) {
-  const int ks = gemm_ksplit(N, K, c->D.ksplit_cap);
+  const int ks = 0;   // the shape's own split
   const double es = sizeof(T);
   ProfScope ps(c, st, SB_PROF_GEMM,
                (double)N * K * es + (double)m_cap * K * es + (double)m_cap * N * 4,
@@ -486,8 +488,17 @@ void layer_body(sb_ctx* c, const sb_layer_weights& lw, int layer,
   kv.seg_k = segk;
   kv.seg_v = segv;
   kv.seg_pages = pf.seg_pages;
-  const int max_prefix = c->cfg.max_pages * 16;
-  const int n_split = std::max(1, std::min(D.n_split, ceil_div(max_prefix, 256)));
+  // prefix length bound: the host-side running bound when known, else the
+  // page-table capacity
+  const int cap_tokens = c->cfg.max_pages * 16;
+  const int max_prefix = c->T_bound > 0 ? std::min(c->T_bound, cap_tokens)
+                                        : cap_tokens;
+  const int groups = attn_qgroups(rows_per_seq, D.H / D.Hkv) * p.n_seqs * D.Hkv;
+  // enough workgroups for the chip, splits of at least 128 keys (the
+  // kernel keeps four 32-key tiles in flight)
+  int n_split = std::max(1, ceil_div(512, groups));
+  n_split = std::min(n_split, std::max(1, max_prefix / 128));
+  n_split = std::min(n_split, D.n_split);
   {
     ProfScope ps(c, st, SB_PROF_ATTN);
     launch_tree_attn<T>(static_cast<const T*>(c->q), p, kv, rows_per_seq, D.H,
@@ -601,6 +612,7 @@ int draft_expand_impl(sb_ctx* c, int m, const sb_seqs* sq, const sb_kv* dkv,
   const TreeDims td = tree_dims(c, sq->n_seqs);
   CallPlan p = c->plan;
   p.n_seqs = sq->n_seqs;
+  p.cap = sq->n_seqs * (m == 1 ? D.K : D.B_max * D.K);   // rows this call
   const float* cond_base = t->h_last;
   if (m == 1) {
     launch_block1_reset(td, *t, sq->root, c->n_aux, st);
@@ -638,6 +650,7 @@ int verify_impl(sb_ctx* c, const sb_seqs* sq, const sb_tree* t,
   const TreeDims td = tree_dims(c, sq->n_seqs);
   CallPlan p = c->plan;
   p.n_seqs = sq->n_seqs;
+  p.cap = sq->n_seqs * D.budget;
   launch_plan_verify(td, *t, sq->T, p, st);
   const Prefix pf{tkv, c->tseg_k, c->tseg_v, D.tpages};
   target_forward<T>(c, p, pf, D.budget, out->taps, st);
@@ -673,9 +686,11 @@ int commit_impl(sb_ctx* c, sb_seqs* sq, const sb_tree* t,
   const Prefix pf{dkv, c->dseg_k, c->dseg_v, D.dpages};
   CallPlan fb = c->fb;
   fb.n_seqs = sq->n_seqs;
+  fb.cap = sq->n_seqs;
   drafter_forward<T>(c, fb, c->cond_buf, pf, 1, false, st);
   launch_seg_to_cache<T>(fb, dp, D.S, D.LD, D.Hkv, D.hd, st);
   launch_commit_state(td, *sq, *acc, c->ci, v->taps, st);
+  if (c->T_bound > 0) c->T_bound += D.M * D.K + 1;
   return hip_check(c, "sb_commit");
 }
 
@@ -683,7 +698,8 @@ template <typename T>
 int prefill_impl(sb_ctx* c, const sb_seqs* sq, const int32_t* prompt, int ld,
                  const int32_t* lens, sb_kv* tkv, sb_kv* dkv, hipStream_t st) {
   const Dims& D = c->D;
-  const CallPlan& p = c->plan;
+  CallPlan p = c->plan;
+  p.cap = D.chunk;
   const int S = D.S;
   launch_set_int(c->one, 1, st);
   launch_set_int(c->zero, 0, st);
@@ -694,6 +710,9 @@ int prefill_impl(sb_ctx* c, const sb_seqs* sq, const int32_t* prompt, int ld,
   const Prefix tpf{tkv, c->tseg_k, c->tseg_v, D.tpages};
   const Prefix dpf{dkv, c->dseg_k, c->dseg_v, D.dpages};
   const size_t tap_row = (size_t)3 * D.d;
+  int longest = 0;
+  for (int s = 0; s < sq->n_seqs; ++s) longest = std::max(longest, lens[s]);
+  c->T_bound = longest + 1;
   for (int s = 0; s < sq->n_seqs; ++s) {
     const int len = lens[s];
     for (int a = 0; a < len; a += D.chunk) {
@@ -853,6 +872,13 @@ int sb_prefill(sb_ctx* c, const sb_seqs* seqs, const int32_t* prompt,
 }  // extern "C"
 
 extern "C" {
+
+int sb_set_length_bound(sb_ctx* c, int32_t max_T) {
+  if (!c) return SB_EINVAL;
+  if (max_T < 0) return fail(c, SB_EINVAL, "max_T must be >= 0");
+  c->T_bound = max_T;
+  return SB_OK;
+}
 
 int sb_profile(sb_ctx* c, int32_t enable) {
   if (!c) return SB_EINVAL;

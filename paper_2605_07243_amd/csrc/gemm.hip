@@ -2,19 +2,126 @@
 //
 //   P[ks][m][n] = sum_{k in K-chunk ks} X[m][k] * W[n][k]
 //
-// X holds the few activation rows of a call (M <= 64 per m-chunk), W is a
-// row-major [N][K] weight matrix streamed from HBM exactly once per m-chunk.
-// One workgroup (4 waves) owns 16 output features and one K-chunk; its waves
-// split the chunk four ways and combine through LDS, so a weight row segment
-// is read by exactly one wave with 16-byte loads.  W rows are the MFMA A
-// operand (16 features x 32 k), activation rows the B operand, so a lane's
-// four results are four consecutive features of one row: one 16-byte store.
-// K-chunks (gridDim.y) write separate partial sums that the consumer kernel
-// adds, which keeps the result independent of scheduling order.
+// X holds the few activation rows of a call (<= 64 per m-chunk), W is a
+// row-major [N][K] weight matrix streamed from HBM once per m-chunk.  MFMA
+// 16x16x32 with weight rows as the A operand (16 features x 32 k) and
+// activation rows as the B operand, so a lane's four results are four
+// consecutive features of one row (one 16-byte store).  K-chunks
+// (gridDim.y) write separate partial sums that the consumer kernel adds,
+// which keeps results independent of scheduling order.
+//
+// bf16 path (gemm_stream_kernel): a workgroup of NW waves owns 16 NW
+// features and one K-chunk.  Each wave streams its own 16 weight rows with
+// row-contiguous 16-byte loads (a wave instruction covers 1 KiB of whole row
+// segments, so every HBM line is used by one instruction), one K-stage ahead
+// in registers, and transposes them into MFMA order through a wave-private
+// LDS tile.  The workgroup stages the activation K-slice in LDS once
+// (double buffered) and all its waves read it from there, so activation
+// traffic does not grow with the number of weight rows.  fp32 path
+// (gemm_xwt_kernel): weight fragments load straight into registers.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
 namespace sb {
+
+
+__device__ __forceinline__ uint4 load_stream16(const void* p) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+template <int MT, int NW, int KT>
+__global__ __launch_bounds__(NW * 64) void gemm_stream_kernel(
+    const bf16_t* __restrict__ X, int ldx, const bf16_t* __restrict__ W,
+    int K, float* __restrict__ P, int N, size_t part_stride,
+    const int* __restrict__ m_count, int k_chunk) {
+  constexpr int LD = KT + 8;                        // padded LDS row
+  constexpr int RPI = 1024 / (KT * 2);              // rows per wave load
+  constexpr int NI = 16 / RPI;                      // loads per stage
+  constexpr int XCH = MT * 16 * KT / 8;             // 16-byte X chunks
+  constexpr int XPT = (XCH + NW * 64 - 1) / (NW * 64);
+  __shared__ __attribute__((aligned(16))) bf16_t wl[NW][16][LD];
+  __shared__ __attribute__((aligned(16))) bf16_t xs[2][MT * 16][LD];
+  const int m_base = blockIdx.z * (MT * 16);
+  const int M = min(*m_count - m_base, MT * 16);
+  if (M <= 0) return;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int r = lane & 15, g = lane >> 4;
+  const int n0 = blockIdx.x * 16 * NW + wave * 16;
+  const int kc0 = blockIdx.y * k_chunk;
+  const int kc1 = min(K, kc0 + k_chunk);
+  const int nstage = (kc1 - kc0) / KT;
+  const int lrow = lane / (KT / 8), lcol = (lane % (KT / 8)) * 8;
+  const bf16_t* wsrc = W + (size_t)(n0 + lrow) * K + kc0 + lcol;
+  const bf16_t* xbase = X + (size_t)m_base * ldx + kc0;
+  f32x4_t acc[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  uint4 stg[NI];
+  uint4 xr[XPT];
+#pragma unroll
+  for (int i = 0; i < NI; ++i) stg[i] = load_stream16(wsrc + (size_t)(i * RPI) * K);
+  auto xfetch = [&](int st) {
+#pragma unroll
+    for (int q = 0; q < XPT; ++q) {
+      const int c = tid + q * NW * 64;
+      const int row = c / (KT / 8), col = (c % (KT / 8)) * 8;
+      xr[q] = (c < XCH && row < M)
+                  ? *reinterpret_cast<const uint4*>(xbase + (size_t)row * ldx +
+                                                    st * KT + col)
+                  : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto xstore = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < XPT; ++q) {
+      const int c = tid + q * NW * 64;
+      const int row = c / (KT / 8), col = (c % (KT / 8)) * 8;
+      if (c < XCH) *reinterpret_cast<uint4*>(&xs[buf][row][col]) = xr[q];
+    }
+  };
+  xfetch(0);
+  xstore(0);
+  __syncthreads();
+  for (int st = 0; st < nstage; ++st) {
+    const int buf = st & 1;
+    // this stage's weight rows into the wave's LDS tile, next stage's loads
+    // in flight during the MFMAs
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+      *reinterpret_cast<uint4*>(&wl[wave][i * RPI + lrow][lcol]) = stg[i];
+    if (st + 1 < nstage) {
+#pragma unroll
+      for (int i = 0; i < NI; ++i)
+        stg[i] = load_stream16(wsrc + (size_t)(i * RPI) * K + (size_t)(st + 1) * KT);
+      xfetch(st + 1);
+    }
+#pragma unroll
+    for (int j = 0; j < KT / 32; ++j) {
+      Frag8<bf16_t> wf;
+      wf.v = *reinterpret_cast<const uint4*>(&wl[wave][r][j * 32 + g * 8]);
+#pragma unroll
+      for (int t = 0; t < MT; ++t) {
+        Frag8<bf16_t> xf;
+        xf.v = *reinterpret_cast<const uint4*>(&xs[buf][t * 16 + r][j * 32 + g * 8]);
+        acc[t] = mma_16x16x32(wf, xf, acc[t]);
+      }
+    }
+    if (st + 1 < nstage) xstore(buf ^ 1);
+    __syncthreads();
+  }
+  float* out = P + (size_t)blockIdx.y * part_stride;
+#pragma unroll
+  for (int t = 0; t < MT; ++t) {
+    const int m = t * 16 + r;
+    if (m < M)
+      *reinterpret_cast<float4*>(out + (size_t)(m_base + m) * N + n0 + 4 * g) =
+          make_float4(acc[t][0], acc[t][1], acc[t][2], acc[t][3]);
+  }
+}
 
 template <typename T, int MT>
 __global__ __launch_bounds__(256) void gemm_xwt_kernel(
@@ -93,12 +200,69 @@ __global__ __launch_bounds__(256) void gemm_xwt_kernel(
   }
 }
 
+GemmPlan gemm_plan(int N, int K, int m_cap, int elem_bytes) {
+  GemmPlan g{};
+  g.mt = m_cap <= 16 ? 1 : (m_cap <= 32 ? 2 : 4);
+  if (elem_bytes == 2 && N % 64 == 0 && K % 128 == 0) {
+    g.stream = true;
+    g.kt = (g.mt == 4 || K % 256 != 0) ? 128 : 256;
+    g.nw = (g.mt == 4 && N >= 65536 && N % 128 == 0) ? 8 : 4;
+    const int tiles = N / (16 * g.nw);
+    g.ks = 1;
+    // enough workgroups to fill the chip; each K-chunk a whole number of
+    // stages and at least four of them
+    while (tiles * g.ks < 400 && g.ks < 16 && K % (g.ks * 2 * g.kt) == 0 &&
+           K / (g.ks * 2) >= 4 * g.kt)
+      g.ks *= 2;
+  } else {
+    g.stream = false;
+    const int tiles = N / 16;
+    g.ks = 1;
+    while (tiles * g.ks < 1024 && K / (32 * (g.ks * 2)) >= 32 && g.ks < 16)
+      g.ks *= 2;
+  }
+  return g;
+}
+
+int gemm_ksplit(int N, int K, int ksplit_cap) {
+  (void)ksplit_cap;
+  int mx = 1;
+  for (int mc : {16, 32, 64}) {
+    mx = std::max(mx, gemm_plan(N, K, mc, 2).ks);
+    mx = std::max(mx, gemm_plan(N, K, mc, 4).ks);
+  }
+  return mx;
+}
+
 template <typename T>
 int launch_gemm_xwt(const T* X, int ldx, const T* W, int N, int K, float* P,
                     size_t part_stride, const int* m_count, int m_cap,
                     int ksplit, hipStream_t st) {
+  const GemmPlan g = gemm_plan(N, K, m_cap, sizeof(T));
+  const int ks_req = ksplit > 0 ? std::min(ksplit, g.ks) : g.ks;
+  const int mz = (m_cap + 63) / 64;
+  if constexpr (sizeof(T) == 2) {
+    if (g.stream) {
+      const int ks = ks_req;
+      const int k_chunk = K / ks;
+      const dim3 grid(N / (16 * g.nw), ks, g.mt == 4 ? mz : 1);
+#define SB_LAUNCH(MT_, NW_, KT_)                                              \
+  if (g.mt == MT_ && g.nw == NW_ && g.kt == KT_) {                            \
+    gemm_stream_kernel<MT_, NW_, KT_><<<grid, NW_ * 64, 0, st>>>(             \
+        X, ldx, W, K, P, N, part_stride, m_count, k_chunk);                   \
+    return ks;                                                                \
+  }
+      SB_LAUNCH(1, 4, 256)
+      SB_LAUNCH(1, 4, 128)
+      SB_LAUNCH(2, 4, 256)
+      SB_LAUNCH(2, 4, 128)
+      SB_LAUNCH(4, 4, 128)
+      SB_LAUNCH(4, 8, 128)
+#undef SB_LAUNCH
+    }
+  }
   const int steps = K / 32;
-  const int per = (steps + ksplit - 1) / ksplit;
+  const int per = (steps + ks_req - 1) / ks_req;
   const int k_chunk = per * 32;
   const int ks = (K + k_chunk - 1) / k_chunk;
   dim3 block(256);
@@ -111,20 +275,10 @@ int launch_gemm_xwt(const T* X, int ldx, const T* W, int N, int K, float* P,
     gemm_xwt_kernel<T, 2><<<grid, block, 0, st>>>(X, ldx, W, K, P, N,
                                                   part_stride, m_count, k_chunk);
   } else {
-    dim3 grid(N / 16, ks, (m_cap + 63) / 64);
+    dim3 grid(N / 16, ks, mz);
     gemm_xwt_kernel<T, 4><<<grid, block, 0, st>>>(X, ldx, W, K, P, N,
                                                   part_stride, m_count, k_chunk);
   }
-  return ks;
-}
-
-int gemm_ksplit(int N, int K, int ksplit_cap) {
-  // Enough workgroups to cover the chip several times, K-chunks of at
-  // least 1024 (each wave then streams >= 256 elements per weight row).
-  const int tiles = N / 16;
-  int ks = 1;
-  while (tiles * ks < 1024 && K / (32 * (ks * 2)) >= 32 && ks * 2 <= ksplit_cap)
-    ks *= 2;
   return ks;
 }
 

@@ -47,7 +47,15 @@ struct KVView {
   int seg_pages;            // pages per sequence in the segment pool
 };
 
+struct GemmPlan {
+  bool stream;   // bf16 LDS-streamed kernel
+  int mt, nw, kt, ks;
+};
+GemmPlan gemm_plan(int N, int K, int m_cap, int elem_bytes);
+// Largest K-split any call of this shape may use (partial-buffer sizing).
 int gemm_ksplit(int N, int K, int ksplit_cap);
+// ksplit <= 0: the plan's split; otherwise at most ksplit K-chunks.
+// Returns the number of K-chunks written.
 template <typename T>
 int launch_gemm_xwt(const T* X, int ldx, const T* W, int N, int K, float* P,
                     size_t part_stride, const int* m_count, int m_cap,
@@ -89,11 +97,14 @@ void launch_rows_to_elem(const float* src, const int* idx, const int* n,
                          int cap, int w, T* out, hipStream_t st);
 
 // Tree attention over paged prefix + masked segment.
+// o_part / ml: split partials [n_split][cap][H][hd] / [n_split][cap][H][2]
+// (used when n_split > 1, then merged by a second launch).
 template <typename T>
 void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
                       int rows_per_seq_cap, int H, int Hkv, int hd,
                       int n_split, int max_prefix, float* o_part, float* ml,
                       T* out, hipStream_t st);
+int attn_qgroups(int rows_per_seq_cap, int G);
 
 // Vocabulary reductions over fp32 logits [cap][V].
 void launch_vocab_partial(const float* logits, const int* n, int cap, int V,

@@ -277,6 +277,11 @@ class Runtime:
         self.accept()
         self.commit()
 
+    def set_length_bound(self, max_T: int):
+        """Bound of T over all sequences (0: unknown); needed after writing
+        T or the caches directly."""
+        self._check(self.lib.sb_set_length_bound(self.ctx, int(max_T)))
+
     def profile(self, enable: bool):
         self._check(self.lib.sb_profile(self.ctx, 1 if enable else 0))
 

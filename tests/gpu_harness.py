@@ -35,6 +35,7 @@ def inject(rt, seq: int, st: specdec.SeqState):
     rt.root[seq] = int(st.root)
     rt.T[seq] = int(st.T)
     rt.cond_taps[seq] = torch.as_tensor(np.asarray(st.cond_taps, np.float32))
+    rt.set_length_bound(0)
     torch.cuda.synchronize()
 
 
