@@ -251,7 +251,7 @@ def main():
         "tree_attn_frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
         "accepted_tokens_per_s": round(committed / dt, 3),
         "tau": round(committed / (args.steps * rt.S), 3),
-        "roofline": {"kernel": "gemm_xwt (weight-streaming projections)",
+        "roofline": {"kernel": "gemm_stream_kernel (all projection GEMMs)",
                      "bound": "hbm", "achieved": round(gemm_gbps, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(gemm_gbps / HBM_PEAK_GBPS, 4),

@@ -72,7 +72,7 @@ typedef struct sb_config {
   int32_t M;                /* block expansions per verifier iteration        */
   int32_t B_max;            /* next-block starts per sequence                 */
   int32_t budget;           /* tree nodes per sequence, root included (<=512) */
-  int32_t branch_map[4];    /* bucket -> branching b(.) (App. A.4), 0..10     */
+  int32_t branch_map[4];    /* bucket -> branching b(.) (App. A.5), 0..10     */
   int32_t dtype;            /* enum sb_dtype                                  */
   int32_t max_seqs;         /* sequences per call                             */
   int32_t page_size;        /* K/V page size in tokens; must be 16            */

@@ -15,7 +15,7 @@ Decoding with Dynamic Tree Drafting):
                 (Sec. 3.1, Eq. 1-3) over explicit rows with explicit visibility;
 * ``rank``      the 15-dim distribution summary psi (App. B), the rank head
                 (Eq. 4), the rank-to-bucket rule (Sec. 3.3) and the
-                bucket-to-branching maps (App. A.4);
+                bucket-to-branching maps (App. A.5);
 * ``tree``      the draft tree, rank-guided sibling attachment and next-block
                 start selection (Sec. 3.2, Alg. 2);
 * ``specdec``   prefill, one verifier iteration (Alg. 2: M block expansions,

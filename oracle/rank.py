@@ -11,7 +11,7 @@ from .numerics import logsumexp
 PSI_DIM = 15
 TOPK = 10
 
-# Bucket-to-branching maps recommended in App. A.4 (inference procedure).
+# Bucket-to-branching maps recommended in App. A.5 (inference procedure).
 BRANCH_MAP_CONCENTRATE = (2, 4, 10, 0)
 BRANCH_MAP_FALLBACK = (2, 4, 6, 4)
 

@@ -1,0 +1,189 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every function include/specblock.h declares, and rejects invalid arguments
+with the documented codes before enqueueing any device work."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2605_07243_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "specblock.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(B.LIB_PATH):
+        from paper_2605_07243_amd import build
+        build.build()
+    return B.load()
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sb_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_function(lib):
+    names = header_functions()
+    assert "sb_draft_block_expand" in names and "sb_tree_verify" in names
+    assert set(names) == set(B.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def cfg(**kw):
+    c = B.Config()
+    c.target = B.ModelDims(2, 256, 4, 4, 64, 1024, 1024, 500000.0, 1e-5)
+    c.drafter_layers = 1
+    c.tap_layers[:] = [0, 1, 1]
+    c.K, c.M, c.B_max, c.budget = 4, 3, 4, 32
+    c.branch_map[:] = [2, 4, 6, 4]
+    c.dtype = B.SB_F32
+    c.max_seqs, c.page_size, c.max_pages, c.prefill_chunk = 1, 16, 16, 128
+    for k, v in kw.items():
+        if k.startswith("t_"):
+            setattr(c.target, k[2:], v)
+        else:
+            setattr(c, k, v)
+    return c
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=7), B.SB_EDTYPE),
+    (dict(t_head_dim=96), B.SB_ESHAPE),
+    (dict(t_n_kv_heads=3), B.SB_ESHAPE),
+    (dict(t_d_model=250), B.SB_ESHAPE),
+    (dict(t_vocab=1000), B.SB_ESHAPE),
+    (dict(K=0), B.SB_EINVAL),
+    (dict(B_max=65), B.SB_EINVAL),
+    (dict(budget=513), B.SB_EBUDGET),
+    (dict(page_size=32), B.SB_ESHAPE),
+    (dict(prefill_chunk=100), B.SB_EINVAL),
+    (dict(max_seqs=0), B.SB_EINVAL),
+    (dict(tap_layers=(C.c_int32 * 3)(0, 1, 2)), B.SB_ESHAPE),
+    (dict(t_rope_theta=0.0), B.SB_EINVAL),
+])
+def test_create_rejects_bad_configs(lib, kw, code):
+    c = cfg(**kw)
+    ctx = C.c_void_p()
+    assert lib.sb_create(C.byref(c), C.byref(ctx)) == code
+    assert not ctx.value
+    assert lib.sb_last_error(None)
+    assert lib.sb_workspace_bytes(C.byref(c)) == 0
+
+
+def test_capacities(lib):
+    c = cfg()
+    assert lib.sb_row_capacity(C.byref(c)) == 4 + 2 * 4 * 4
+    assert lib.sb_workspace_bytes(C.byref(c)) > 0
+
+
+class Fake:
+    """Aligned, never-dereferenced addresses (host tests enqueue nothing)."""
+
+    def __init__(self):
+        self.buf = (C.c_char * (1 << 16))()
+        base = C.addressof(self.buf)
+        self.p = C.c_void_p((base + 255) & ~255)
+
+    def at(self, off=0):
+        return C.c_void_p(self.p.value + off)
+
+
+@pytest.fixture
+def bound(lib):
+    c = cfg()
+    ctx = C.c_void_p()
+    assert lib.sb_create(C.byref(c), C.byref(ctx)) == B.SB_OK
+    f = Fake()
+    layers = (B.LayerWeights * 2)(*[B.LayerWeights(*[f.at()] * 6, None)
+                                    for _ in range(2)])
+    dl = (B.LayerWeights * 1)(B.LayerWeights(*[f.at()] * 7))
+    tw = B.TargetWeights(f.at(), layers, f.at(), f.at())
+    dw = B.DrafterWeights(f.at(), f.at(), f.at(), f.at(), f.at(), f.at(), dl,
+                          f.at(), f.at(), f.at(), f.at())
+    need = lib.sb_workspace_bytes(C.byref(c))
+    # too small, misaligned, then right: none of these touches the device
+    assert lib.sb_bind(ctx, C.byref(tw), C.byref(dw), f.at(), need - 1) == \
+        B.SB_EBUDGET
+    assert lib.sb_bind(ctx, C.byref(tw), C.byref(dw), f.at(8), need) == \
+        B.SB_EINVAL
+    bad = B.DrafterWeights(f.at(8), *([f.at()] * 5), dl, *([f.at()] * 4))
+    assert lib.sb_bind(ctx, C.byref(tw), C.byref(bad), f.at(), need) == \
+        B.SB_EINVAL     # bf16/fp32 matrices need 16-byte alignment
+    nos = (B.LayerWeights * 1)(B.LayerWeights(*[f.at()] * 6, None))
+    dw2 = B.DrafterWeights(*([f.at()] * 6), nos, *([f.at()] * 4))
+    assert lib.sb_bind(ctx, C.byref(tw), C.byref(dw2), f.at(), need) == \
+        B.SB_EINVAL     # drafter layers need W_shift
+    assert lib.sb_bind(ctx, C.byref(tw), C.byref(dw), f.at(), need) == B.SB_OK
+    yield lib, ctx, f
+    lib.sb_destroy(ctx)
+
+
+def test_calls_before_bind_are_refused(lib):
+    c = cfg()
+    ctx = C.c_void_p()
+    assert lib.sb_create(C.byref(c), C.byref(ctx)) == B.SB_OK
+    t = B.Tree()
+    assert lib.sb_accept(ctx, 1, C.byref(t), None, None, None) == B.SB_ESTATE
+    lib.sb_destroy(ctx)
+
+
+def _tree(f):
+    return B.Tree(*[f.at() for _ in B.TREE_FIELDS])
+
+
+def test_draft_call_validation(bound):
+    lib, ctx, f = bound
+    seqs = B.Seqs(1, f.at(), f.at(), f.at())
+    kv = B.KV(f.at(), f.at(), f.at(), 1, 4)
+    tree = _tree(f)
+    out = B.DraftOut(*[f.at() for _ in B.DRAFT_OUT_FIELDS])
+    call = lambda m, K, s=seqs, k=kv, t=tree, o=out: lib.sb_draft_block_expand(  # noqa
+        ctx, m, K, C.byref(s), C.byref(k), C.byref(t), C.byref(o), None)
+    assert call(1, 3) == B.SB_ESHAPE                   # K != cfg.K
+    assert call(0, 4) == B.SB_EINVAL                   # block index
+    assert call(4, 4) == B.SB_EINVAL                   # > M
+    assert call(1, 4, s=B.Seqs(2, f.at(), f.at(), f.at())) == B.SB_ESHAPE
+    assert call(1, 4, k=B.KV(f.at(), f.at(), f.at(), 2, 4)) == B.SB_ESHAPE
+    t2 = _tree(f)
+    t2.anc = None
+    assert call(1, 4, t=t2) == B.SB_EINVAL
+    o2 = B.DraftOut(*[f.at() for _ in B.DRAFT_OUT_FIELDS])
+    o2.logits = f.at(4)
+    assert call(1, 4, o=o2) == B.SB_EINVAL
+    assert b"logits" in lib.sb_last_error(ctx)
+
+
+def test_verify_accept_commit_validation(bound):
+    lib, ctx, f = bound
+    seqs = B.Seqs(1, f.at(), f.at(), f.at())
+    tkv = B.KV(f.at(), f.at(), f.at(), 2, 4)
+    dkv = B.KV(f.at(), f.at(), f.at(), 1, 4)
+    tree = _tree(f)
+    v = B.VerifyOut(None, f.at(), None)
+    assert lib.sb_tree_verify(ctx, C.byref(seqs), C.byref(tree),
+                              C.byref(tkv), C.byref(v), None) == B.SB_EINVAL
+    v = B.VerifyOut(f.at(), f.at(), None)
+    assert lib.sb_tree_verify(ctx, C.byref(seqs), C.byref(tree),
+                              C.byref(dkv), C.byref(v), None) == B.SB_ESHAPE
+    a = B.AcceptOut(f.at(), f.at(), None)
+    assert lib.sb_accept(ctx, 1, C.byref(tree), f.at(), C.byref(a),
+                         None) == B.SB_EINVAL
+    assert lib.sb_accept(ctx, 2, C.byref(tree), f.at(), C.byref(a),
+                         None) == B.SB_ESHAPE
+    a = B.AcceptOut(f.at(), f.at(), f.at())
+    assert lib.sb_commit(ctx, C.byref(seqs), C.byref(tree), C.byref(v),
+                         C.byref(a), C.byref(dkv), C.byref(dkv),
+                         None) == B.SB_ESHAPE
+    lens = (C.c_int32 * 1)(0)
+    assert lib.sb_prefill(ctx, C.byref(seqs), f.at(), 8, lens, C.byref(tkv),
+                          C.byref(dkv), None) == B.SB_ESHAPE
+    lens = (C.c_int32 * 1)(300)
+    assert lib.sb_prefill(ctx, C.byref(seqs), f.at(), 400, lens, C.byref(tkv),
+                          C.byref(dkv), None) == B.SB_EBUDGET
+    assert lib.sb_set_length_bound(ctx, -1) == B.SB_EINVAL
