@@ -48,6 +48,22 @@ def attn_bytes(w, T_avg, n_nodes, rows_block, es):
     return verify + draft
 
 
+def gemm_traffic(workload):
+    """Measured HBM bytes per projection-GEMM dispatch from the committed
+    counter summary of this workload, or None when there is none or the
+    GEMM sources changed since it was taken."""
+    from paper_2605_07243_amd.profile_summary import gemm_sources_sha256
+    path = os.path.join(ROOT, "profiles", f"gemm_traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("sources_sha256") != gemm_sources_sha256():
+        log("gemm traffic summary is stale (sources changed); traffic = null")
+        return None
+    return d["bytes_per_dispatch"]
+
+
 def cpu_baseline(w, T, budget_s=30.0):
     """Time the CPU oracle on a bounded sample of the workload: one block-1
     and one block-2 expansion (the real drafter shape, prefix T), one verify
@@ -144,6 +160,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama3-8b-k4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-mib", type=int, default=0,
+                    help="before warmup, run a plain elementwise copy "
+                         "(torch.neg) of this many MiB three times, to "
+                         "calibrate HBM byte counters against a kernel of "
+                         "known traffic")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (got --gpus "
@@ -169,6 +190,13 @@ def main():
     torch.cuda.synchronize()
     log(f"prefill {sum(len(p) for p in prompts)} tokens in "
         f"{time.perf_counter() - t:.2f}s")
+    if args.calib_mib:
+        src = torch.ones(args.calib_mib << 18, device=rt.dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
     for i in range(args.warmup):
         rt.iteration()
     torch.cuda.synchronize()
@@ -226,6 +254,9 @@ def main():
         f"{attn['ms']:.2f} ms {attn_gbps:.0f} GB/s; vocab "
         f"{prof['vocab']['ms']:.2f} ms")
 
+    traffic = gemm_traffic(w.name)
+    if traffic is not None:
+        traffic = round(traffic)
     out = {
         "metric": METRIC,
         "value": round(committed / dt, 3),
@@ -255,7 +286,9 @@ def main():
                      "bound": "hbm", "achieved": round(gemm_gbps, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(gemm_gbps / HBM_PEAK_GBPS, 4),
-                     "traffic": None,
+                     "traffic": traffic,
+                     "algorithmic_bytes_per_launch": round(
+                         gemm["bytes"] / max(gemm["launches"], 1)),
                      "launches_per_step": gemm["launches"] // args.steps,
                      "avg_launch_us": round(gemm["ms"] * 1e3 /
                                             max(gemm["launches"], 1), 2)},

@@ -121,21 +121,40 @@ def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
 # seeded draws
 # ----------------------------------------------------------------------------
 
-def _rng(seed: int, name: str) -> np.random.Generator:
-    return np.random.default_rng([seed, zlib.crc32(name.encode())])
+def _rng(seed: int, name: str, chunk: int = -1) -> np.random.Generator:
+    key = [seed, zlib.crc32(name.encode())]
+    return np.random.default_rng(key if chunk < 0 else key + [chunk])
+
+
+# Large tensors are drawn in fixed chunks, each from its own stream keyed by
+# (seed, name, chunk index), so the values do not depend on how many threads
+# fill them.
+CHUNK = 1 << 22
+
+
+def _fill_chunk(seed, name, flat, c, std, dtype):
+    part = flat[c * CHUNK:(c + 1) * CHUNK]
+    _rng(seed, name, c).standard_normal(out=part, dtype=np.float32)
+    part *= np.float32(std)
+    if dtype == "bf16":
+        part[...] = bf16_bits_to_f32(f32_to_bf16_bits(part))
 
 
 def normal(seed: int, name: str, shape, std: float = INIT_STD,
-           dtype: str = "f32") -> np.ndarray:
+           dtype: str = "f32", pool=None) -> np.ndarray:
     """N(0, std) float32 array; for dtype "bf16" the values are rounded to
-    bf16 (returned as float32 holding bf16-representable values)."""
+    bf16 (returned as float32 holding bf16-representable values).  ``pool``
+    (a concurrent.futures executor) fills the chunks in parallel."""
     n = int(np.prod(shape))
-    rng = _rng(seed, name)
-    x = rng.standard_normal(n, dtype=np.float32)
-    x *= np.float32(std)
-    if dtype == "bf16":
-        x = bf16_bits_to_f32(f32_to_bf16_bits(x))
-    return x.reshape(shape)
+    flat = np.empty(n, np.float32)
+    chunks = range((n + CHUNK - 1) // CHUNK)
+    if pool is None:
+        for c in chunks:
+            _fill_chunk(seed, name, flat, c, std, dtype)
+    else:
+        list(pool.map(lambda c: _fill_chunk(seed, name, flat, c, std, dtype),
+                      chunks))
+    return flat.reshape(shape)
 
 
 def _layer_specs(prefix: str, s: ModelShape):
@@ -188,20 +207,20 @@ def make_weights(specs, seed: int = 0, dtype: str = "f32",
     ``jitter`` > 0 draws norm gains as 1 + N(0, jitter) and the rank-head
     bias as N(0, jitter) instead of the constant 1 / 0, so that tests can
     tell the gains and biases apart."""
-    def one(spec):
+    def one(spec, ex):
         name, shape, kind = spec
         if kind == "ones":
             if jitter:
-                return name, (1.0 + normal(seed, name, shape, jitter)).astype(np.float32)
-            return name, np.ones(shape, np.float32)
+                return (1.0 + normal(seed, name, shape, jitter)).astype(np.float32)
+            return np.ones(shape, np.float32)
         if kind == "zeros":
             if jitter:
-                return name, normal(seed, name, shape, jitter)
-            return name, np.zeros(shape, np.float32)
+                return normal(seed, name, shape, jitter)
+            return np.zeros(shape, np.float32)
         dt = "f32" if name.startswith("d.rank_") else dtype
-        return name, normal(seed, name, shape, dtype=dt)
+        return normal(seed, name, shape, dtype=dt, pool=ex)
     with ThreadPoolExecutor(max_workers=threads) as ex:
-        return dict(ex.map(one, specs))
+        return {spec[0]: one(spec, ex) for spec in specs}
 
 
 def target_weights(w: Workload, seed: int = 0, jitter: float = 0.0) -> dict:

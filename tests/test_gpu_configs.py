@@ -1,0 +1,86 @@
+"""GPU parity at the per-layer shapes of the benchmark's workloads: 8B-shaped
+(d 4096, 32/8 heads, FFN 14336, vocabulary 128256) with K = 4 / budget 60,
+with K = 8 / B_max 16 / budget 128 over a 4096-token prefix, and with 16
+ragged paged sequences; 70B-shaped (d 8192, 64/8 heads, FFN 28672) with
+K = 6 / budget 96 over 4 sequences.  Every kernel runs in the launch
+configuration the benchmark times (same dims, budgets, row and page
+capacities); only the target is shallower (1-2 layers) so that the float64
+oracle can recompute every call.
+
+The committed prefix is synthetic (seeded random K/V of the workload's
+prompt lengths, the same on both sides).  One iteration is compared call by
+call on the oracle's inputs (see parity_checks), with a planted greedy path
+per sampled sequence so that acceptance and commit move real entries; for
+the batched workloads the oracle recomputes a sample of the sequences while
+the device runs them all.
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import specdec
+
+from gpu_harness import inject, models, runtime
+from parity_checks import Tally, oracle_iteration, run_and_compare
+
+pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
+TOL = 2e-2
+
+CASES = {
+    # name: (workload, target layers, sequences the oracle recomputes)
+    "8b-k4": ("llama3-8b-k4", 2, None),
+    "8b-k8-long": ("llama3-8b-k8-long", 1, None),
+    "8b-batch16-paged": ("llama3-8b-batch16-paged", 1, (0, 5, 10, 15)),
+    "70b-k6": ("llama3-70b-k6", 1, (0, 3)),
+}
+
+
+def synthetic_state(w, tgt, dr, seq, T, seed):
+    """Seeded committed state of one sequence: random K/V of T entries for
+    every target and drafter layer, a random root token and random taps."""
+    s = w.target
+    rng = np.random.default_rng([seed, seq])
+    st = specdec.SeqState([], T, int(rng.integers(s.vocab)), tgt.new_prefix(),
+                          dr.new_prefix(),
+                          rng.standard_normal((3, s.d_model)))
+    for layer in range(s.n_layers):
+        k, v = synth.random_kv(seed, f"t{seq}.{layer}", T, s, w.dtype)
+        st.tkv.k[layer] = k.astype(np.float64)
+        st.tkv.v[layer] = v.astype(np.float64)
+    for layer in range(w.drafter_layers):
+        k, v = synth.random_kv(seed, f"d{seq}.{layer}", T, s, w.dtype)
+        st.dkv.k[layer] = k.astype(np.float64)
+        st.dkv.v[layer] = v.astype(np.float64)
+    return st
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_iteration_full_layer_shape(name):
+    wname, layers, sample = CASES[name]
+    w = synth.with_layers(synth.WORKLOADS[wname], layers)
+    log(f"[{name}] weights")
+    weights, tgt, dr = models(w)
+    lens = synth.prompt_lengths(w)
+    sample = sample or tuple(range(w.n_seqs))
+    states = [synthetic_state(w, tgt, dr, s, int(lens[s]), 5)
+              for s in range(w.n_seqs)]
+    log(f"[{name}] runtime")
+    rt = runtime(w, weights, max_pages=(int(max(lens)) + w.M * w.K + 16) // 16)
+    del weights
+    for s, st in enumerate(states):
+        inject(rt, s, st)
+    seqs = {}
+    for s in sample:
+        depth = (w.K + 2 + 3 * s) % (2 * w.K + 1)
+        log(f"[{name}] oracle seq {s} (T {states[s].T}, planted depth {depth})")
+        seqs[s] = (states[s],) + oracle_iteration(tgt, dr, states[s], w, depth)
+    tally = Tally()
+    run_and_compare(rt, seqs, w, tgt, dr, TOL, tally,
+                    log=lambda m: log(f"[{name}] {m}"))
+    log(f"[{name}] {tally}; tau {[seqs[s][2]['tau'] for s in seqs]}")
+    assert tally.rows == sum(sum(e["R"] for e in seqs[s][2]["expansions"])
+                             for s in seqs)
