@@ -76,7 +76,8 @@ typedef struct sb_config {
   int32_t dtype;            /* enum sb_dtype                                  */
   int32_t max_seqs;         /* sequences per call                             */
   int32_t page_size;        /* K/V page size in tokens; must be 16            */
-  int32_t max_pages;        /* page-table row length (pages per sequence)     */
+  int32_t max_pages;        /* page-table row length (pages per sequence),
+                               1..16384                                       */
   int32_t prefill_chunk;    /* rows per prefill step (multiple of 16)         */
 } sb_config;
 

@@ -21,6 +21,27 @@ namespace sb {
 
 #define SB_NEG (-1.0e30f)
 
+// Elements of a 16-byte V chunk whose key slot (first + e) is at or past
+// nvalid are zeroed: slots that no call has written may hold anything, and
+// a zero probability times a non-finite value would still poison the
+// output (K needs no such care: masked scores are replaced, not scaled).
+template <int ES>
+__device__ __forceinline__ uint4 keep_slots(uint4 v, int first, int nvalid) {
+  constexpr int EPC = 16 / ES;                      // elements per chunk
+  if (first + EPC <= nvalid) return v;
+  if (first >= nvalid) return make_uint4(0, 0, 0, 0);
+  uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int e = 0; e < EPC; ++e) {
+    if (first + e < nvalid) continue;
+    if constexpr (ES == 2)
+      w[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+    else
+      w[e] = 0u;
+  }
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
 // One workgroup = NQ waves = NQ q-tiles of 16 query vectors of one KV head,
 // one split of the prefix (the last split also takes the segment).  K and V
 // tiles of 32 keys are staged once per workgroup in LDS (double buffered;
@@ -141,7 +162,12 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
       dst[e] = v;
     }
   };
-  auto stash = [&](int buf, const uint4 (&src)[PER]) {
+  // valid keys of tile i
+  auto n_valid = [&](int i) -> int {
+    return i < n_pre ? min(32, t1 - (t0 + i * 32)) : min(32, L - (i - n_pre) * 32);
+  };
+  auto stash = [&](int i, int buf, const uint4 (&src)[PER]) {
+    const int nv = n_valid(i);
 #pragma unroll
     for (int e = 0; e < PER; ++e) {
       const int c = tid + e * NT;
@@ -152,7 +178,8 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
         const int cc = c - KCH;
         const int hd = cc / (2 * VCR), rem = cc % (2 * VCR);
         const int h = rem / VCR, part = rem % VCR;
-        *reinterpret_cast<uint4*>(&vsh[buf][hd][h * 16 + part * (16 / ES)]) = src[e];
+        const int first = h * 16 + part * (16 / ES);
+        *reinterpret_cast<uint4*>(&vsh[buf][hd][first]) = keep_slots<ES>(src[e], first, nv);
       }
     }
   };
@@ -241,7 +268,7 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
 #pragma unroll
   for (int d = 0; d < DEPTH; ++d)
     if (d < n_tiles) fetch(d, stg[d]);
-  if (n_tiles > 0) stash(0, stg[0]);
+  if (n_tiles > 0) stash(0, 0, stg[0]);
   __syncthreads();
   // tile i lives in slot i % DEPTH; after it is stashed, the slot is refilled
   // with tile i + DEPTH
@@ -252,7 +279,7 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
       if (i < n_tiles) {
         if (i + DEPTH < n_tiles) fetch(i + DEPTH, stg[d]);
         compute(i, i & 1);
-        if (i + 1 < n_tiles) stash((i + 1) & 1, stg[(d + 1) % DEPTH]);
+        if (i + 1 < n_tiles) stash(i + 1, (i + 1) & 1, stg[(d + 1) % DEPTH]);
         __syncthreads();
       }
     }

@@ -79,32 +79,63 @@ __device__ __forceinline__ float4 add4(float4 a, float4 b) {
   return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
 }
 
-// sum_{s < ks} P[s] at float4 offset `off` (ks <= 16)
+// sum_{s < ks} P[s] at float4 offset `off` (ks <= 16).  The partials were
+// just written by the projection (most reads miss the local L2), so up to
+// eight loads are issued before the first add: one memory latency per eight
+// partials rather than one per partial.
 __device__ __forceinline__ float4 sum_parts(const float* __restrict__ P,
                                             size_t part_stride, int ks,
                                             size_t off) {
   float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
-  int s = 0;
-  for (; s + 4 <= ks; s += 4) {
-    const float4 p0 = *reinterpret_cast<const float4*>(P + (s + 0) * part_stride + off);
-    const float4 p1 = *reinterpret_cast<const float4*>(P + (s + 1) * part_stride + off);
-    const float4 p2 = *reinterpret_cast<const float4*>(P + (s + 2) * part_stride + off);
-    const float4 p3 = *reinterpret_cast<const float4*>(P + (s + 3) * part_stride + off);
-    a = add4(a, add4(add4(p0, p1), add4(p2, p3)));
+  for (int s0 = 0; s0 < ks; s0 += 8) {
+    float4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      v[u] = s0 + u < ks
+                 ? *reinterpret_cast<const float4*>(P + (s0 + u) * part_stride + off)
+                 : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) a = add4(a, v[u]);
   }
-  for (; s < ks; ++s)
-    a = add4(a, *reinterpret_cast<const float4*>(P + s * part_stride + off));
   return a;
 }
 
+// The same for two offsets at once (sixteen loads in flight).
+__device__ __forceinline__ void sum_parts2(const float* __restrict__ P,
+                                           size_t part_stride, int ks,
+                                           size_t off_a, size_t off_b,
+                                           float4& a, float4& b) {
+  a = make_float4(0.f, 0.f, 0.f, 0.f);
+  b = a;
+  for (int s0 = 0; s0 < ks; s0 += 8) {
+    float4 va[8], vb[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const bool ok = s0 + u < ks;
+      const float* q = P + (s0 + u) * part_stride;
+      va[u] = ok ? *reinterpret_cast<const float4*>(q + off_a)
+                 : make_float4(0.f, 0.f, 0.f, 0.f);
+      vb[u] = ok ? *reinterpret_cast<const float4*>(q + off_b)
+                 : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      a = add4(a, va[u]);
+      b = add4(b, vb[u]);
+    }
+  }
+}
+
+// One workgroup of 1024 threads per row: thread t owns float4 columns
+// t, t + 1024 (d <= 8192), summed over the partials in one pass.
 template <typename T>
-__global__ __launch_bounds__(256) void residual_kernel(
+__global__ __launch_bounds__(1024) void residual_kernel(
     float* __restrict__ x, const float* __restrict__ P, int ks,
     size_t part_stride, const int* __restrict__ n, int d, int accumulate,
     const float* __restrict__ g, float eps, T* __restrict__ out, int ldo,
     float* __restrict__ taps, int tap_mask, const int* __restrict__ out_row) {
-  constexpr int MAXV = 8;   // d <= 8192 with 256 threads
-  __shared__ float red[4];
+  constexpr int MAXV = 2;
+  __shared__ float red[16];
   const int i = blockIdx.x;
   if (i >= *n) return;
   float* xr = x + (size_t)i * d;
@@ -114,11 +145,21 @@ __global__ __launch_bounds__(256) void residual_kernel(
   const int nv = d >> 2;
   float4 v[MAXV];
   float ss = 0.f;
+  if (nv > 1024) {
+    // second column only where it exists (else a repeat of the first)
+    const int c1 = threadIdx.x + 1024 < nv ? threadIdx.x + 1024 : threadIdx.x;
+    sum_parts2(P, part_stride, ks, (size_t)i * d + 4 * threadIdx.x,
+               (size_t)i * d + 4 * c1, v[0], v[1]);
+  } else {
+    v[0] = threadIdx.x < nv
+               ? sum_parts(P, part_stride, ks, (size_t)i * d + 4 * threadIdx.x)
+               : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
 #pragma unroll
   for (int q = 0; q < MAXV; ++q) {
-    const int c = threadIdx.x + q * 256;
+    const int c = threadIdx.x + q * 1024;
     if (c < nv) {
-      float4 a = sum_parts(P, part_stride, ks, (size_t)i * d + 4 * c);
+      float4 a = v[q];
       if (accumulate) a = add4(a, reinterpret_cast<const float4*>(xr)[c]);
       reinterpret_cast<float4*>(xr)[c] = a;
       if (tr) {
@@ -136,7 +177,7 @@ __global__ __launch_bounds__(256) void residual_kernel(
   T* o = out + (size_t)i * ldo;
 #pragma unroll
   for (int q = 0; q < MAXV; ++q) {
-    const int c = threadIdx.x + q * 256;
+    const int c = threadIdx.x + q * 1024;
     if (c < nv) {
       const float4 gg = reinterpret_cast<const float4*>(g)[c];
       store4<T>(o + 4 * c, make_float4(v[q].x * rs * gg.x, v[q].y * rs * gg.y,
@@ -150,14 +191,16 @@ void launch_residual(float* x, const float* P, int ks, size_t part_stride,
                      const int* n, int cap, int d, bool accumulate,
                      const float* g, float eps, T* out, int ldo, float* taps,
                      int tap_mask, const int* out_row, hipStream_t st) {
-  residual_kernel<T><<<cap, 256, 0, st>>>(x, P, ks, part_stride, n, d,
-                                          accumulate ? 1 : 0, g, eps, out, ldo,
-                                          taps, tap_mask, out_row);
+  residual_kernel<T><<<cap, 1024, 0, st>>>(x, P, ks, part_stride, n, d,
+                                           accumulate ? 1 : 0, g, eps, out, ldo,
+                                           taps, tap_mask, out_row);
 }
 
 // RoPE (rotate-half pairs (j, j + hd/2), angle pos * theta^(-2j/hd)) on the
 // Q and K heads of the summed QKV projection; Q -> q [cap][H][hd], K and V ->
-// the row's slot of its sequence's segment pages.  Four pairs per thread.
+// the row's slot of its sequence's segment pages.  Grid (rows, item blocks):
+// an item is four rotation pairs of one Q/K head, or four V columns; one
+// item per thread, its partials summed in one pass.
 template <typename T>
 __global__ __launch_bounds__(256) void qkv_post_kernel(
     const float* __restrict__ P, int ks, size_t part_stride, CallPlan p, int H,
@@ -168,52 +211,59 @@ __global__ __launch_bounds__(256) void qkv_post_kernel(
   const int i = blockIdx.x;
   if (i >= *p.n) return;
   const int half = hd >> 1;
+  const int q4 = half >> 2;
+  const int n_rot = (H + Hkv) * q4;
+  const int n_items = n_rot + Hkv * (hd >> 2);
+  const int idx = blockIdx.y * blockDim.x + threadIdx.x;
   const int ncol = (H + 2 * Hkv) * hd;
+  const size_t row = (size_t)i * ncol;
+  const int seq = p.seq[i], slot = p.slot[i];
+  const int page = slot >> 4, sl = slot & 15;
+  const size_t page_base = (size_t)seq * seg_pages + page;
+  // issue this thread's partial loads before the angle table is built
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
+  int head = 0, j = 0;
+  if (idx < n_rot) {
+    head = idx / q4;
+    j = (idx % q4) * 4;
+    sum_parts2(P, part_stride, ks, row + head * hd + j,
+               row + head * hd + j + half, a, b);
+  } else if (idx < n_items) {
+    const int v = idx - n_rot;
+    head = v / (hd >> 2);
+    j = (v % (hd >> 2)) * 4;
+    a = sum_parts(P, part_stride, ks, row + (H + Hkv) * hd + head * hd + j);
+  }
   const double pos = (double)p.pos[i];
-  for (int j = threadIdx.x; j < half; j += blockDim.x) {
+  for (int t = threadIdx.x; t < half; t += blockDim.x) {
     // angle in double, reduced to [-pi, pi] before the fp32 sincos
-    const double inv = exp(-((double)(2 * j) / (double)hd) * log((double)theta));
+    const double inv = exp(-((double)(2 * t) / (double)hd) * log((double)theta));
     const double ang = pos * inv;
     const double two_pi = 6.283185307179586476925287;
     const float red = (float)(ang - two_pi * rint(ang / two_pi));
     float sv, cv;
     sincosf(red, &sv, &cv);
-    cs[j] = cv;
-    sn[j] = sv;
+    cs[t] = cv;
+    sn[t] = sv;
   }
   __syncthreads();
-  const size_t row = (size_t)i * ncol;
-  const int seq = p.seq[i], slot = p.slot[i];
-  const int page = slot >> 4, sl = slot & 15;
-  const size_t page_base = (size_t)seq * seg_pages + page;
-  const int q4 = half >> 2;
-  for (int idx = threadIdx.x; idx < (H + Hkv) * q4; idx += blockDim.x) {
-    const int head = idx / q4, j = (idx % q4) * 4;
-    const float4 a = sum_parts(P, part_stride, ks, row + head * hd + j);
-    const float4 b = sum_parts(P, part_stride, ks, row + head * hd + j + half);
+  if (idx < n_rot) {
     const float4 c4 = *reinterpret_cast<const float4*>(&cs[j]);
     const float4 s4 = *reinterpret_cast<const float4*>(&sn[j]);
     const float4 ra = make_float4(a.x * c4.x - b.x * s4.x, a.y * c4.y - b.y * s4.y,
                                   a.z * c4.z - b.z * s4.z, a.w * c4.w - b.w * s4.w);
     const float4 rb = make_float4(b.x * c4.x + a.x * s4.x, b.y * c4.y + a.y * s4.y,
                                   b.z * c4.z + a.z * s4.z, b.w * c4.w + a.w * s4.w);
-    T* dst;
-    if (head < H) {
-      dst = q + ((size_t)i * H + head) * hd;
-    } else {
-      dst = seg_k + ((page_base * Hkv + (head - H)) * 16 + sl) * hd;
-    }
+    T* dst = head < H ? q + ((size_t)i * H + head) * hd
+                      : seg_k + ((page_base * Hkv + (head - H)) * 16 + sl) * hd;
     store4<T>(dst + j, ra);
     store4<T>(dst + j + half, rb);
-  }
-  for (int idx = threadIdx.x; idx < Hkv * (hd >> 2); idx += blockDim.x) {
-    const int kh = idx / (hd >> 2), j = (idx % (hd >> 2)) * 4;
-    const float4 v = sum_parts(P, part_stride, ks, row + (H + Hkv) * hd + kh * hd + j);
-    T* dv = seg_v + ((page_base * Hkv + kh) * hd + j) * 16 + sl;
-    dv[0] = Elem<T>::from_f32(v.x);
-    dv[16] = Elem<T>::from_f32(v.y);
-    dv[32] = Elem<T>::from_f32(v.z);
-    dv[48] = Elem<T>::from_f32(v.w);
+  } else if (idx < n_items) {
+    T* dv = seg_v + ((page_base * Hkv + head) * hd + j) * 16 + sl;
+    dv[0] = Elem<T>::from_f32(a.x);
+    dv[16] = Elem<T>::from_f32(a.y);
+    dv[32] = Elem<T>::from_f32(a.z);
+    dv[48] = Elem<T>::from_f32(a.w);
   }
 }
 
@@ -222,9 +272,10 @@ void launch_qkv_post(const float* P, int ks, size_t part_stride,
                      const CallPlan& p, int H, int Hkv, int hd, float theta,
                      T* q, void* seg_k, void* seg_v, int seg_pages,
                      hipStream_t st) {
-  qkv_post_kernel<T><<<p.cap, 256, 0, st>>>(P, ks, part_stride, p, H, Hkv, hd,
-                                            theta, q, (T*)seg_k, (T*)seg_v,
-                                            seg_pages);
+  const int items = (H + Hkv) * (hd / 8) + Hkv * (hd / 4);
+  qkv_post_kernel<T><<<dim3(p.cap, (items + 255) / 256), 256, 0, st>>>(
+      P, ks, part_stride, p, H, Hkv, hd, theta, q, (T*)seg_k, (T*)seg_v,
+      seg_pages);
 }
 
 // out = silu(gate) * up, four columns per thread; grid (rows, F / 1024).

@@ -99,6 +99,7 @@ struct sb_ctx {
   // workspace
   float* x = nullptr;
   void* A = nullptr;
+  void* A2 = nullptr;   // SwiGLU output (down-projection operand)
   float* P = nullptr;
   void* q = nullptr;
   float* o_part = nullptr;
@@ -155,6 +156,7 @@ static size_t layout(const Dims& D, void* base, sb_ctx* c) {
   const int widest = std::max(std::max(3 * D.d, D.F), std::max(D.H * D.hd, 2 * D.d));
   float* x = cv.take<float>(R * D.d * 4);
   void* A = cv.take<char>(R * widest * es);
+  void* A2 = cv.take<char>(R * D.F * es);
   float* P = cv.take<float>(D.part_elems * 4);
   void* q = cv.take<char>(R * D.H * D.hd * es);
   float* o_part = cv.take<float>((size_t)D.n_split * R * D.H * D.hd * 4);
@@ -203,6 +205,7 @@ static size_t layout(const Dims& D, void* base, sb_ctx* c) {
   if (c) {
     c->x = x;
     c->A = A;
+    c->A2 = A2;
     c->P = P;
     c->q = q;
     c->o_part = o_part;
@@ -300,8 +303,8 @@ static int validate_cfg(const sb_config* c, std::string& msg) {
     msg = "page_size must be 16";
     return SB_ESHAPE;
   }
-  if (c->max_pages < 1) {
-    msg = "max_pages must be >= 1";
+  if (c->max_pages < 1 || c->max_pages > 16384) {
+    msg = "max_pages must be in 1..16384";
     return SB_EINVAL;
   }
   if (c->prefill_chunk < 16 || c->prefill_chunk % 16 || c->prefill_chunk > 512) {
@@ -453,6 +456,29 @@ int gemm(sb_ctx* c, const void* X, int ldx, const void* W, int N, int K,
                             (size_t)c->D.R_cap * N, n, m_cap, ks, st);
 }
 
+// Gate/up projection + SwiGLU into out; fused in the GEMM epilogue where the
+// shape allows, else the GEMM's partials and a separate SwiGLU pass.
+template <typename T>
+void gate_up_swiglu(sb_ctx* c, const void* X, const void* W, const int* n,
+                    int m_cap, T* out, hipStream_t st) {
+  const Dims& D = c->D;
+  if constexpr (sizeof(T) == 2) {
+    if (gemm_swiglu_fits(D.F, D.d, m_cap)) {
+      const double es = sizeof(T);
+      ProfScope ps(c, st, SB_PROF_GEMM,
+                   2.0 * D.F * D.d * es + (double)m_cap * D.d * es +
+                       (double)m_cap * D.F * es,
+                   2.0 * m_cap * 2 * D.F * D.d);
+      launch_gemm_swiglu(static_cast<const bf16_t*>(X), D.d,
+                         static_cast<const bf16_t*>(W), D.F, D.d, out, n,
+                         m_cap, st);
+      return;
+    }
+  }
+  const int ks = gemm<T>(c, X, D.d, W, 2 * D.F, D.d, n, m_cap, st);
+  launch_swiglu<T>(c->P, ks, (size_t)D.R_cap * 2 * D.F, n, m_cap, D.F, out, st);
+}
+
 struct Prefix {
   const sb_kv* kv;
   void* seg_k;   // all layers
@@ -498,6 +524,8 @@ void layer_body(sb_ctx* c, const sb_layer_weights& lw, int layer,
   // kernel keeps four 32-key tiles in flight)
   int n_split = std::max(1, ceil_div(512, groups));
   n_split = std::min(n_split, std::max(1, max_prefix / 128));
+  // a split spans at most 512 pages of 16 keys
+  n_split = std::max(n_split, ceil_div(max_prefix, 512 * 16));
   n_split = std::min(n_split, D.n_split);
   {
     ProfScope ps(c, st, SB_PROF_ATTN);
@@ -509,9 +537,9 @@ void layer_body(sb_ctx* c, const sb_layer_weights& lw, int layer,
   launch_residual<T>(c->x, c->P, ks, (size_t)D.R_cap * D.d, p.n, R, D.d, true,
                      lw.mlp_norm ? static_cast<const float*>(lw.mlp_norm) : nullptr,
                      eps, A, D.d, nullptr, 0, nullptr, st);
-  ks = gemm<T>(c, A, D.d, lw.w_gate_up, 2 * D.F, D.d, p.n, R, st);
-  launch_swiglu<T>(c->P, ks, (size_t)D.R_cap * 2 * D.F, p.n, R, D.F, A, st);
-  ks = gemm<T>(c, A, D.F, lw.w_down, D.d, D.F, p.n, R, st);
+  T* A2 = static_cast<T*>(c->A2);
+  gate_up_swiglu<T>(c, A, lw.w_gate_up, p.n, R, A2, st);
+  ks = gemm<T>(c, A2, D.F, lw.w_down, D.d, D.F, p.n, R, st);
   launch_residual<T>(c->x, c->P, ks, (size_t)D.R_cap * D.d, p.n, R, D.d, true,
                      next_g, eps, A, D.d, taps, tap_mask, p.out_row, st);
 }

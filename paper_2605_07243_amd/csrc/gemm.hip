@@ -33,11 +33,16 @@ __device__ __forceinline__ uint4 load_stream16(const void* p) {
   return make_uint4(v[0], v[1], v[2], v[3]);
 }
 
-template <int MT, int NW, int KT>
+// SWIGLU: the weight is [gate; up] ([2F][K]) and the workgroup owns gate
+// features j0 .. j0 + 8 NW - 1 (first NW/2 waves) and the matching up
+// features (last NW/2 waves); with one K-chunk the epilogue writes
+// act[m][j] = silu(gate) * up as bf16 instead of partial sums.
+template <int MT, int NW, int KT, bool SWIGLU>
 __global__ __launch_bounds__(NW * 64) void gemm_stream_kernel(
     const bf16_t* __restrict__ X, int ldx, const bf16_t* __restrict__ W,
     int K, float* __restrict__ P, int N, size_t part_stride,
-    const int* __restrict__ m_count, int k_chunk) {
+    const int* __restrict__ m_count, int k_chunk, bf16_t* __restrict__ act,
+    int F) {
   constexpr int LD = KT + 8;                        // padded LDS row
   constexpr int RPI = 1024 / (KT * 2);              // rows per wave load
   constexpr int NI = 16 / RPI;                      // loads per stage
@@ -50,7 +55,11 @@ __global__ __launch_bounds__(NW * 64) void gemm_stream_kernel(
   if (M <= 0) return;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int r = lane & 15, g = lane >> 4;
-  const int n0 = blockIdx.x * 16 * NW + wave * 16;
+  int n0 = blockIdx.x * 16 * NW + wave * 16;
+  if constexpr (SWIGLU) {
+    constexpr int HW = NW / 2;
+    n0 = blockIdx.x * 16 * HW + (wave % HW) * 16 + (wave >= HW ? F : 0);
+  }
   const int kc0 = blockIdx.y * k_chunk;
   const int kc1 = min(K, kc0 + k_chunk);
   const int nstage = (kc1 - kc0) / KT;
@@ -112,6 +121,38 @@ __global__ __launch_bounds__(NW * 64) void gemm_stream_kernel(
     }
     if (st + 1 < nstage) xstore(buf ^ 1);
     __syncthreads();
+  }
+  if constexpr (SWIGLU) {
+    // up waves hand their sums to the gate waves through LDS (the loop
+    // ended with a barrier, so the X tiles are free)
+    constexpr int HW = NW / 2;
+    f32x4_t* ex = reinterpret_cast<f32x4_t*>(&xs[0][0][0]);
+    static_assert(sizeof(xs) >= HW * MT * 64 * sizeof(f32x4_t), "LDS");
+    if (wave >= HW) {
+#pragma unroll
+      for (int t = 0; t < MT; ++t) ex[((wave - HW) * MT + t) * 64 + lane] = acc[t];
+    }
+    __syncthreads();
+    if (wave < HW) {
+#pragma unroll
+      for (int t = 0; t < MT; ++t) {
+        const int m = t * 16 + r;
+        const f32x4_t u = ex[(wave * MT + t) * 64 + lane];
+        float o[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float gt = acc[t][e];
+          o[e] = gt / (1.0f + expf(-gt)) * u[e];
+        }
+        if (m < M) {
+          uint2 pk;
+          pk.x = (uint32_t)f32_to_bf16(o[0]) | ((uint32_t)f32_to_bf16(o[1]) << 16);
+          pk.y = (uint32_t)f32_to_bf16(o[2]) | ((uint32_t)f32_to_bf16(o[3]) << 16);
+          *reinterpret_cast<uint2*>(act + (size_t)(m_base + m) * F + n0 + 4 * g) = pk;
+        }
+      }
+    }
+    return;
   }
   float* out = P + (size_t)blockIdx.y * part_stride;
 #pragma unroll
@@ -248,8 +289,8 @@ int launch_gemm_xwt(const T* X, int ldx, const T* W, int N, int K, float* P,
       const dim3 grid(N / (16 * g.nw), ks, g.mt == 4 ? mz : 1);
 #define SB_LAUNCH(MT_, NW_, KT_)                                              \
   if (g.mt == MT_ && g.nw == NW_ && g.kt == KT_) {                            \
-    gemm_stream_kernel<MT_, NW_, KT_><<<grid, NW_ * 64, 0, st>>>(             \
-        X, ldx, W, K, P, N, part_stride, m_count, k_chunk);                   \
+    gemm_stream_kernel<MT_, NW_, KT_, false><<<grid, NW_ * 64, 0, st>>>(      \
+        X, ldx, W, K, P, N, part_stride, m_count, k_chunk, nullptr, 0);       \
     return ks;                                                                \
   }
       SB_LAUNCH(1, 4, 256)
@@ -280,6 +321,34 @@ int launch_gemm_xwt(const T* X, int ldx, const T* W, int N, int K, float* P,
                                                   part_stride, m_count, k_chunk);
   }
   return ks;
+}
+
+bool gemm_swiglu_fits(int F, int K, int m_cap) {
+  const GemmPlan g = gemm_plan(2 * F, K, m_cap, 2);
+  return g.stream && g.ks == 1 && F % (8 * g.nw) == 0;
+}
+
+bool launch_gemm_swiglu(const bf16_t* X, int ldx, const bf16_t* W, int F,
+                        int K, bf16_t* act, const int* m_count, int m_cap,
+                        hipStream_t st) {
+  if (!gemm_swiglu_fits(F, K, m_cap)) return false;
+  const GemmPlan g = gemm_plan(2 * F, K, m_cap, 2);
+  const int mz = (m_cap + 63) / 64;
+  const dim3 grid(F / (8 * g.nw), 1, g.mt == 4 ? mz : 1);
+#define SB_LAUNCH_SW(MT_, NW_, KT_)                                           \
+  if (g.mt == MT_ && g.nw == NW_ && g.kt == KT_) {                            \
+    gemm_stream_kernel<MT_, NW_, KT_, true><<<grid, NW_ * 64, 0, st>>>(       \
+        X, ldx, W, K, nullptr, 2 * F, 0, m_count, K, act, F);                 \
+    return true;                                                              \
+  }
+  SB_LAUNCH_SW(1, 4, 256)
+  SB_LAUNCH_SW(1, 4, 128)
+  SB_LAUNCH_SW(2, 4, 256)
+  SB_LAUNCH_SW(2, 4, 128)
+  SB_LAUNCH_SW(4, 4, 128)
+  SB_LAUNCH_SW(4, 8, 128)
+#undef SB_LAUNCH_SW
+  return false;
 }
 
 template int launch_gemm_xwt<float>(const float*, int, const float*, int, int,

@@ -60,6 +60,14 @@ template <typename T>
 int launch_gemm_xwt(const T* X, int ldx, const T* W, int N, int K, float* P,
                     size_t part_stride, const int* m_count, int m_cap,
                     int ksplit, hipStream_t st);
+// Gate/up projection with SwiGLU fused into the epilogue (bf16, weight
+// [gate; up] of [2F][K], one K-chunk): act[m][j] = silu(gate) * up for the
+// first *m_count rows.  Returns false when the shape does not take this
+// path; the caller then runs launch_gemm_xwt and launch_swiglu.
+bool gemm_swiglu_fits(int F, int K, int m_cap);
+bool launch_gemm_swiglu(const bf16_t* X, int ldx, const bf16_t* W, int F,
+                        int K, bf16_t* act, const int* m_count, int m_cap,
+                        hipStream_t st);
 
 template <typename T>
 void launch_embed(const CallPlan& p, const T* embed, int d, float* x,

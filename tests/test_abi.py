@@ -64,6 +64,8 @@ def cfg(**kw):
     (dict(page_size=32), B.SB_ESHAPE),
     (dict(prefill_chunk=100), B.SB_EINVAL),
     (dict(max_seqs=0), B.SB_EINVAL),
+    (dict(max_pages=0), B.SB_EINVAL),
+    (dict(max_pages=16385), B.SB_EINVAL),
     (dict(tap_layers=(C.c_int32 * 3)(0, 1, 2)), B.SB_ESHAPE),
     (dict(t_rope_theta=0.0), B.SB_EINVAL),
 ])
