@@ -7,60 +7,98 @@
 
 namespace sb {
 
+// Four consecutive elements of a row as floats (16 B of float, 8 B of bf16).
 template <typename T>
-__global__ __launch_bounds__(256) void embed_kernel(const int* __restrict__ n,
-                                                    const int* __restrict__ tok,
-                                                    const T* __restrict__ E,
-                                                    int d, float* __restrict__ x) {
+__device__ __forceinline__ float4 load4(const T* p);
+template <>
+__device__ __forceinline__ float4 load4<float>(const float* p) {
+  return *reinterpret_cast<const float4*>(p);
+}
+template <>
+__device__ __forceinline__ float4 load4<bf16_t>(const bf16_t* p) {
+  const uint2 u = *reinterpret_cast<const uint2*>(p);
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u),
+                     __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xFFFF0000u));
+}
+
+__device__ __forceinline__ float sumsq4(float4 v) {
+  return v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+}
+
+__device__ __forceinline__ float4 scale4(float4 v, float r, float4 g) {
+  return make_float4(v.x * r * g.x, v.y * r * g.y, v.z * r * g.z, v.w * r * g.w);
+}
+
+// Row kernels below use 1024 threads per row: thread t owns float4 columns
+// t and t + 1024 (d <= 8192), loaded before any reduction.
+constexpr int kRowThreads = 1024;
+constexpr int kRowVec = 2;
+
+template <typename T>
+__global__ __launch_bounds__(kRowThreads) void embed_kernel(
+    const int* __restrict__ n, const int* __restrict__ tok,
+    const T* __restrict__ E, int d, float* __restrict__ x) {
   const int i = blockIdx.x;
   if (i >= *n) return;
   const T* e = E + (size_t)tok[i] * d;
-  float* xr = x + (size_t)i * d;
-  for (int j = threadIdx.x; j < d; j += blockDim.x) xr[j] = Elem<T>::to_f32(e[j]);
+  float4* xr = reinterpret_cast<float4*>(x + (size_t)i * d);
+  float4 v[kRowVec];
+#pragma unroll
+  for (int q = 0; q < kRowVec; ++q) {
+    const int c = threadIdx.x + q * kRowThreads;
+    if (c < d / 4) v[q] = load4<T>(e + 4 * c);
+  }
+#pragma unroll
+  for (int q = 0; q < kRowVec; ++q) {
+    const int c = threadIdx.x + q * kRowThreads;
+    if (c < d / 4) xr[c] = v[q];
+  }
 }
 
 template <typename T>
 void launch_embed(const CallPlan& p, const T* embed, int d, float* x,
                   hipStream_t st) {
-  embed_kernel<T><<<p.cap, 256, 0, st>>>(p.n, p.token, embed, d, x);
+  embed_kernel<T><<<p.cap, kRowThreads, 0, st>>>(p.n, p.token, embed, d, x);
 }
 
-// Writes rmsnorm(src) * g as T into out (d elements).
 template <typename T>
-__device__ __forceinline__ void norm_row(const float* __restrict__ src, int d,
-                                         const float* __restrict__ g, float eps,
-                                         T* __restrict__ out, float* red) {
+__device__ __forceinline__ void store4(T* p, float4 v);
+
+// out = rmsnorm(x) * g as T.
+template <typename T>
+__global__ __launch_bounds__(kRowThreads) void rmsnorm_kernel(
+    const float* __restrict__ x, const int* __restrict__ n, int d,
+    const float* __restrict__ g, float eps, T* __restrict__ out, int ldo) {
+  __shared__ float red[16];
+  const int i = blockIdx.x;
+  if (i >= *n) return;
+  const float4* xr = reinterpret_cast<const float4*>(x + (size_t)i * d);
+  float4 v[kRowVec];
   float ss = 0.f;
-  for (int j = threadIdx.x; j < d; j += blockDim.x) {
-    const float v = src[j];
-    ss += v * v;
+#pragma unroll
+  for (int q = 0; q < kRowVec; ++q) {
+    const int c = threadIdx.x + q * kRowThreads;
+    v[q] = c < d / 4 ? xr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+    ss += sumsq4(v[q]);
   }
   ss = block_sum(ss, red);
   const float r = 1.0f / sqrtf(ss / (float)d + eps);
-  for (int j = threadIdx.x; j < d; j += blockDim.x)
-    out[j] = Elem<T>::from_f32(src[j] * r * g[j]);
-}
-
-template <typename T>
-__global__ __launch_bounds__(256) void rmsnorm_kernel(
-    const float* __restrict__ x, const int* __restrict__ n, int d,
-    const float* __restrict__ g, float eps, T* __restrict__ out, int ldo) {
-  __shared__ float red[4];
-  const int i = blockIdx.x;
-  if (i >= *n) return;
-  norm_row<T>(x + (size_t)i * d, d, g, eps, out + (size_t)i * ldo, red);
+  T* o = out + (size_t)i * ldo;
+#pragma unroll
+  for (int q = 0; q < kRowVec; ++q) {
+    const int c = threadIdx.x + q * kRowThreads;
+    if (c < d / 4)
+      store4<T>(o + 4 * c, scale4(v[q], r, reinterpret_cast<const float4*>(g)[c]));
+  }
 }
 
 template <typename T>
 void launch_rmsnorm(const float* x, const int* n, int cap, int d,
                     const float* g, float eps, T* out, int ldo,
                     hipStream_t st) {
-  rmsnorm_kernel<T><<<cap, 256, 0, st>>>(x, n, d, g, eps, out, ldo);
+  rmsnorm_kernel<T><<<cap, kRowThreads, 0, st>>>(x, n, d, g, eps, out, ldo);
 }
 
-// Sum of the split-K partials (+ the residual stream), optionally the next
-// RMSNorm as the following projection's operand and the tap copies.  Each
-// thread keeps its float4 columns in registers between the two passes.
 template <typename T>
 __device__ __forceinline__ void store4(T* p, float4 v);
 template <>
@@ -306,56 +344,93 @@ void launch_swiglu(const float* P, int ks, size_t part_stride, const int* n,
 
 // Layer-wise shift operand (Eq. 3): [h_k, h_{k-1}] with h_0 := h_1.
 template <typename T>
-__global__ __launch_bounds__(256) void shift_prep_kernel(
+__global__ __launch_bounds__(kRowThreads) void shift_prep_kernel(
     const float* __restrict__ h, const int* __restrict__ n,
     const int* __restrict__ pred, int d, T* __restrict__ out) {
   const int i = blockIdx.x;
   if (i >= *n) return;
-  const float* a = h + (size_t)i * d;
-  const float* b = h + (size_t)pred[i] * d;
+  const float4* a = reinterpret_cast<const float4*>(h + (size_t)i * d);
+  const float4* b = reinterpret_cast<const float4*>(h + (size_t)pred[i] * d);
   T* o = out + (size_t)i * 2 * d;
-  for (int j = threadIdx.x; j < d; j += blockDim.x) {
-    o[j] = Elem<T>::from_f32(a[j]);
-    o[d + j] = Elem<T>::from_f32(b[j]);
+  float4 va[kRowVec], vb[kRowVec];
+#pragma unroll
+  for (int q = 0; q < kRowVec; ++q) {
+    const int c = threadIdx.x + q * kRowThreads;
+    if (c < d / 4) {
+      va[q] = a[c];
+      vb[q] = b[c];
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < kRowVec; ++q) {
+    const int c = threadIdx.x + q * kRowThreads;
+    if (c < d / 4) {
+      store4<T>(o + 4 * c, va[q]);
+      store4<T>(o + d + 4 * c, vb[q]);
+    }
   }
 }
 
 template <typename T>
 void launch_shift_prep(const float* h, const CallPlan& p, int d, T* out,
                        hipStream_t st) {
-  shift_prep_kernel<T><<<p.cap, 256, 0, st>>>(h, p.n, p.pred, d, out);
+  shift_prep_kernel<T><<<p.cap, kRowThreads, 0, st>>>(h, p.n, p.pred, d, out);
 }
 
 // Drafter input fusion operand (Eq. 2): [norm_c(c), norm_e(embed(x)),
-// norm_q(q_k)], each an RMSNorm with its own gain.
+// norm_q(q_k)], each an RMSNorm with its own gain; all three rows are
+// loaded at once and their sums of squares reduced together.
 template <typename T>
-__global__ __launch_bounds__(256) void fuse_prep_kernel(
+__global__ __launch_bounds__(kRowThreads) void fuse_prep_kernel(
     const float* __restrict__ cond, CallPlan p, const T* __restrict__ E,
     const T* __restrict__ Q, const float* __restrict__ gc,
     const float* __restrict__ ge, const float* __restrict__ gq, float eps,
     int d, T* __restrict__ out) {
-  __shared__ float red[4];
-  __shared__ float buf[8192];
+  __shared__ float red[3][16];
   const int i = blockIdx.x;
   if (i >= *p.n) return;
-  T* o = out + (size_t)i * 3 * d;
-  const int c = p.cond[i];
-  if (c >= 0) {
-    norm_row<T>(cond + (size_t)c * d, d, gc, eps, o, red);
-  } else {
-    for (int j = threadIdx.x; j < d; j += blockDim.x)
-      o[j] = Elem<T>::from_f32(0.f);
+  const int ci = p.cond[i];
+  const float4* cr = reinterpret_cast<const float4*>(cond + (size_t)max(ci, 0) * d);
+  const T* er = E + (size_t)p.token[i] * d;
+  const T* qr = Q + (size_t)(p.k[i] - 1) * d;
+  float4 vc[kRowVec], ve[kRowVec], vq[kRowVec];
+  float s[3] = {0.f, 0.f, 0.f};
+#pragma unroll
+  for (int q = 0; q < kRowVec; ++q) {
+    const int c = threadIdx.x + q * kRowThreads;
+    const bool ok = c < d / 4;
+    vc[q] = ok && ci >= 0 ? cr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+    ve[q] = ok ? load4<T>(er + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
+    vq[q] = ok ? load4<T>(qr + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
+    s[0] += sumsq4(vc[q]);
+    s[1] += sumsq4(ve[q]);
+    s[2] += sumsq4(vq[q]);
+  }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int j = 0; j < 3; ++j) {
+    const float t = wave_sum(s[j]);
+    if (lane == 0) red[j][w] = t;
   }
   __syncthreads();
-  const T* e = E + (size_t)p.token[i] * d;
-  for (int j = threadIdx.x; j < d; j += blockDim.x) buf[j] = Elem<T>::to_f32(e[j]);
-  __syncthreads();
-  norm_row<T>(buf, d, ge, eps, o + d, red);
-  __syncthreads();
-  const T* qk = Q + (size_t)(p.k[i] - 1) * d;
-  for (int j = threadIdx.x; j < d; j += blockDim.x) buf[j] = Elem<T>::to_f32(qk[j]);
-  __syncthreads();
-  norm_row<T>(buf, d, gq, eps, o + 2 * d, red);
+  float r[3];
+#pragma unroll
+  for (int j = 0; j < 3; ++j) {
+    float t = 0.f;
+    for (int q = 0; q < (int)(blockDim.x >> 6); ++q) t += red[j][q];
+    r[j] = 1.0f / sqrtf(t / (float)d + eps);
+  }
+  T* o = out + (size_t)i * 3 * d;
+#pragma unroll
+  for (int q = 0; q < kRowVec; ++q) {
+    const int c = threadIdx.x + q * kRowThreads;
+    if (c < d / 4) {
+      // a zero condition stays zero (0 * finite scale)
+      store4<T>(o + 4 * c, scale4(vc[q], r[0], reinterpret_cast<const float4*>(gc)[c]));
+      store4<T>(o + d + 4 * c, scale4(ve[q], r[1], reinterpret_cast<const float4*>(ge)[c]));
+      store4<T>(o + 2 * d + 4 * c, scale4(vq[q], r[2], reinterpret_cast<const float4*>(gq)[c]));
+    }
+  }
 }
 
 template <typename T>
@@ -363,25 +438,29 @@ void launch_fuse_prep(const float* cond, const CallPlan& p, const T* embed,
                       const T* pos_query, const float* gc, const float* ge,
                       const float* gq, float eps, int d, T* out,
                       hipStream_t st) {
-  fuse_prep_kernel<T><<<p.cap, 256, 0, st>>>(cond, p, embed, pos_query, gc, ge,
-                                             gq, eps, d, out);
+  fuse_prep_kernel<T><<<p.cap, kRowThreads, 0, st>>>(cond, p, embed, pos_query,
+                                                     gc, ge, gq, eps, d, out);
 }
 
+// out[i] = T(src[idx[i]]) (idx null: identity), rows of w floats; one
+// float4 per thread, grid (rows, w / 1024).
 template <typename T>
 __global__ __launch_bounds__(256) void rows_to_elem_kernel(
     const float* __restrict__ src, const int* __restrict__ idx,
     const int* __restrict__ n, int w, T* __restrict__ out) {
   const int i = blockIdx.x;
   if (i >= *n) return;
+  const int c = blockIdx.y * 256 + threadIdx.x;
+  if (c >= w / 4) return;
   const float* s = src + (size_t)(idx ? idx[i] : i) * w;
-  for (int j = threadIdx.x; j < w; j += blockDim.x)
-    out[(size_t)i * w + j] = Elem<T>::from_f32(s[j]);
+  store4<T>(out + (size_t)i * w + 4 * c, reinterpret_cast<const float4*>(s)[c]);
 }
 
 template <typename T>
 void launch_rows_to_elem(const float* src, const int* idx, const int* n,
                          int cap, int w, T* out, hipStream_t st) {
-  rows_to_elem_kernel<T><<<cap, 256, 0, st>>>(src, idx, n, w, out);
+  rows_to_elem_kernel<T><<<dim3(cap, (w / 4 + 255) / 256), 256, 0, st>>>(
+      src, idx, n, w, out);
 }
 
 #define SB_INST(T)                                                             \

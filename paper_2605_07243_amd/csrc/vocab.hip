@@ -92,17 +92,21 @@ __global__ __launch_bounds__(256) void vocab_partial_kernel(
     ti[k] = 0x7FFFFFFF;
   }
   float m = -FLT_MAX, s = 0.f, u = 0.f;
-  for (int j = v0 + threadIdx.x; j < v1; j += blockDim.x) {
-    const float x = z[j];
+  // the next element's load is issued before the current one is processed
+  int j = v0 + threadIdx.x;
+  float xn = j < v1 ? z[j] : 0.f;
+  for (; j < v1; j += 256) {
+    const float x = xn;
+    if (j + 256 < v1) xn = z[j + 256];
     if (x > m) {
       const float a = __expf(m - x);
       s = s * a + 1.f;
       u = u * a + x;
       m = x;
     } else {
-      const float e = __expf(x - m);
-      s += e;
-      u += e * x;
+      const float ex = __expf(x - m);
+      s += ex;
+      u += ex * x;
     }
     topk_insert<KT>(tv, ti, x, j);
   }
