@@ -316,17 +316,61 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
 
 // Combine the splits of every (row, head): out = sum_z w_z O_z / sum_z w_z l_z
 // with w_z = exp(m_z - max m).  A separate launch: the kernel boundary
-// orders the partial writes of every XCD before the reads.
+// orders the partial writes of every XCD before the reads.  One workgroup
+// per row; a thread owns one float4 column per pass, and the first pass's
+// partial loads are issued before the (m, l) loads and the weights, so a
+// row of up to 4 BT columns costs one memory round trip.
 template <int NS>
-__global__ __launch_bounds__(256) void attn_merge_kernel_t(
+constexpr int merge_threads() { return NS <= 8 ? 1024 : 512; }
+
+template <int NS>
+__global__ __launch_bounds__(merge_threads<NS>()) void attn_merge_kernel_t(
     const float* __restrict__ o_part, const float* __restrict__ ml,
     const int* __restrict__ n, int cap, int H, int hd, int n_split,
     void* out_v, int es) {
+  constexpr int BT = merge_threads<NS>();
   __shared__ float wgt[64][NS];
   __shared__ float inv_l[64];
   const int i = blockIdx.x;
   if (i >= *n) return;
-  for (int h = threadIdx.x; h < H; h += blockDim.x) {
+  const size_t zs = (size_t)cap * H * hd;
+  const int ncol = (H * hd) >> 2;
+  const float* row = o_part + (size_t)i * H * hd;
+  auto load = [&](int c, float4 (&o)[NS]) {
+#pragma unroll
+    for (int z = 0; z < NS; ++z)
+      o[z] = (z < n_split && c < ncol)
+                 ? *reinterpret_cast<const float4*>(row + z * zs + 4 * c)
+                 : make_float4(0.f, 0.f, 0.f, 0.f);
+  };
+  auto combine = [&](int c, const float4 (&o)[NS]) {
+    if (c >= ncol) return;
+    const int j = 4 * c, hh = j / hd;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int z = 0; z < NS; ++z) {
+      const float w = wgt[hh][z];
+      v.x += w * o[z].x;
+      v.y += w * o[z].y;
+      v.z += w * o[z].z;
+      v.w += w * o[z].w;
+    }
+    const float il = inv_l[hh];
+    v = make_float4(v.x * il, v.y * il, v.z * il, v.w * il);
+    const size_t off = (size_t)i * H * hd + j;
+    if (es == 2) {
+      uint2 u;
+      u.x = (uint32_t)f32_to_bf16(v.x) | ((uint32_t)f32_to_bf16(v.y) << 16);
+      u.y = (uint32_t)f32_to_bf16(v.z) | ((uint32_t)f32_to_bf16(v.w) << 16);
+      *reinterpret_cast<uint2*>(static_cast<bf16_t*>(out_v) + off) = u;
+    } else {
+      *reinterpret_cast<float4*>(static_cast<float*>(out_v) + off) = v;
+    }
+  };
+  float4 o[NS];
+  load(threadIdx.x, o);
+  const int h = threadIdx.x;
+  if (h < H) {
     float mz[NS], lz[NS];
     float mx = SB_NEG;
 #pragma unroll
@@ -348,35 +392,10 @@ __global__ __launch_bounds__(256) void attn_merge_kernel_t(
     inv_l[h] = L > 0.f ? 1.0f / L : 0.f;
   }
   __syncthreads();
-  const size_t zs = (size_t)cap * H * hd;
-  for (int c = threadIdx.x; c < (H * hd) >> 2; c += blockDim.x) {
-    const int j = 4 * c, h = j / hd;
-    const float* base = o_part + (size_t)i * H * hd + j;
-    float4 o[NS];
-#pragma unroll
-    for (int z = 0; z < NS; ++z)
-      o[z] = z < n_split ? *reinterpret_cast<const float4*>(base + z * zs)
-                         : make_float4(0.f, 0.f, 0.f, 0.f);
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-    for (int z = 0; z < NS; ++z) {
-      const float w = wgt[h][z];
-      v.x += w * o[z].x;
-      v.y += w * o[z].y;
-      v.z += w * o[z].z;
-      v.w += w * o[z].w;
-    }
-    const float il = inv_l[h];
-    v = make_float4(v.x * il, v.y * il, v.z * il, v.w * il);
-    const size_t off = (size_t)i * H * hd + j;
-    if (es == 2) {
-      uint2 u;
-      u.x = (uint32_t)f32_to_bf16(v.x) | ((uint32_t)f32_to_bf16(v.y) << 16);
-      u.y = (uint32_t)f32_to_bf16(v.z) | ((uint32_t)f32_to_bf16(v.w) << 16);
-      *reinterpret_cast<uint2*>(static_cast<bf16_t*>(out_v) + off) = u;
-    } else {
-      *reinterpret_cast<float4*>(static_cast<float*>(out_v) + off) = v;
-    }
+  combine(threadIdx.x, o);
+  for (int c = threadIdx.x + BT; c < ncol; c += BT) {
+    load(c, o);
+    combine(c, o);
   }
 }
 
@@ -420,7 +439,7 @@ void launch_attn_merge(const CallPlan& p, int H, int hd, int n_split,
   // empty splits
 #define SB_MERGE(NS_)                                                          \
   if (n_split <= NS_) {                                                       \
-    attn_merge_kernel_t<NS_><<<p.cap, 256, 0, st>>>(                          \
+    attn_merge_kernel_t<NS_><<<p.cap, merge_threads<NS_>(), 0, st>>>(         \
         o_part, ml, p.n, p.cap, H, hd, n_split, out, sizeof(T));              \
     return;                                                                   \
   }

@@ -93,5 +93,21 @@ def test_lossless_loop_bf16(small):
         out += [int(toks[p]) for p in path] + [int(rt.aout["bonus"][0])]
     ref = specdec.greedy_decode(tgt, prompt, n_new)
     if out[:n_new] != ref:
+        # allowed only where the oracle's own choice is a near-tie: the
+        # oracle's logits for that position (after the common prefix) must
+        # rate the device's token within 2e-2 relative of its best
         j = next(i for i in range(n_new) if out[i] != ref[i])
-        pytest.skip(f"streams part at token {j} (bf16 near-tie)")
+        toks = [int(t) for t in prompt] + ref[:j]
+        n = len(toks)
+        idx = np.arange(n)
+        z, _ = tgt.forward(toks, idx, idx, [list(range(r + 1)) for r in idx],
+                           tgt.new_prefix(), tgt.new_segment(n))
+        zl = z[-1]
+        assert int(np.argmax(zl)) == ref[j]
+        gap = zl[ref[j]] - zl[out[j]]
+        print(f"streams part at token {j}: oracle margin {gap:.3e} "
+              f"(max |z| {np.abs(zl).max():.3f})", flush=True)
+        assert gap <= 2e-2 * np.abs(zl).max(), (j, gap)
+        # the device stream up to and including the tie is the target's
+        # greedy stream under its own (equally valid) choice at the tie
+        assert out[:j] == ref[:j]
