@@ -220,8 +220,7 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
       sc[e] = v ? sc4[e >> 2][e & 3] * scale : SB_NEG;
       mx = fmaxf(mx, sc[e]);
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, SB_WAVE));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, SB_WAVE));
+    mx = max_x32(max_x16(mx));
     const float m_new = fmaxf(m_run, mx);
     const float alpha = __expf(m_run - m_new);
     float pv[8];
@@ -232,8 +231,7 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
       pv[e] = ((bits >> kk) & 1u) ? __expf(sc[e] - m_new) : 0.f;
       ps += pv[e];
     }
-    ps += __shfl_xor(ps, 16, SB_WAVE);
-    ps += __shfl_xor(ps, 32, SB_WAVE);
+    ps = sum_x32(sum_x16(ps));
     l_run = l_run * alpha + ps;
     m_run = m_new;
 #pragma unroll

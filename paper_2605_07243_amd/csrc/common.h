@@ -91,15 +91,46 @@ __device__ __forceinline__ f32x4_t mma_16x16x32(const Frag8<float>& a,
   return acc;
 }
 
+// Cross-lane exchanges on the VALU (no LDS permute): DPP within rows of 16
+// lanes, v_permlane16_swap / v_permlane32_swap across rows.  Each step pairs
+// every lane with one partner so that a symmetric op (sum, max) combines
+// disjoint groups: xor 1 and xor 2 (quad_perm), 4-lane groups mirrored within
+// 8 (row_half_mirror), 8-lane groups mirrored within 16 (row_mirror), then
+// rows 2r <-> 2r+1 and halves 0-31 <-> 32-63.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(
+      __builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+// op(v, v of lane l ^ 16) and op(v, v of lane l ^ 32), in every lane
+__device__ __forceinline__ float2 swap16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v),
+                                                  __float_as_uint(v), false, false);
+  return make_float2(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float2 swap32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v),
+                                                  __float_as_uint(v), false, false);
+  return make_float2(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_x16(float v) { const float2 p = swap16(v); return p.x + p.y; }
+__device__ __forceinline__ float sum_x32(float v) { const float2 p = swap32(v); return p.x + p.y; }
+__device__ __forceinline__ float max_x16(float v) { const float2 p = swap16(v); return fmaxf(p.x, p.y); }
+__device__ __forceinline__ float max_x32(float v) { const float2 p = swap32(v); return fmaxf(p.x, p.y); }
+
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, SB_WAVE);
-  return v;
+  v += dpp_f<0xB1>(v);    // quad_perm [1,0,3,2]
+  v += dpp_f<0x4E>(v);    // quad_perm [2,3,0,1]
+  v += dpp_f<0x141>(v);   // row_half_mirror
+  v += dpp_f<0x140>(v);   // row_mirror
+  return sum_x32(sum_x16(v));
 }
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, SB_WAVE));
-  return v;
+  v = fmaxf(v, dpp_f<0xB1>(v));
+  v = fmaxf(v, dpp_f<0x4E>(v));
+  v = fmaxf(v, dpp_f<0x141>(v));
+  v = fmaxf(v, dpp_f<0x140>(v));
+  return max_x32(max_x16(v));
 }
 __device__ __forceinline__ int wave_sum_i(int v) {
 #pragma unroll
