@@ -22,7 +22,11 @@
  *   and bfloat16 (uint16_t bits, round-to-nearest-even) when SB_BF16.
  *   Accumulation, norms, softmax, residual stream, logits, h^(L) and all
  *   outputs typed float are float32.
- * - Matrices are row-major [out_features][in_features] (y = W x).
+ * - Matrices are row-major [out_features][in_features] (y = W x), except
+ *   that with SB_BF16 the projection matrices passed to sb_bind (w_qkv, w_o,
+ *   w_gate_up, w_down, w_shift, w_cond, w_fuse and both lm_head) are in the
+ *   fragment-packed layout written by sb_pack_weight.  embed and pos_query
+ *   stay row-major.
  * - Calls are asynchronous: they enqueue work on `stream` (a hipStream_t;
  *   NULL = the default stream) and return.  Outputs are valid once the
  *   stream has reached that point.  No call synchronises with the host.
@@ -208,10 +212,34 @@ void sb_destroy(sb_ctx* ctx);
 const char* sb_last_error(const sb_ctx* ctx);
 
 /* Attach weights and workspace.  Tables are copied (host arrays may be
- * freed); the device memory they point to must outlive the context. */
+ * freed); the device memory they point to must outlive the context.
+ * SB_BF16: the projection matrices must have been packed by sb_pack_weight
+ * (w_gate_up with gate_up = 1, the others with 0). */
 int sb_bind(sb_ctx* ctx, const sb_target_weights* target,
             const sb_drafter_weights* drafter, void* workspace,
             size_t workspace_bytes);
+
+/* Weight layout conversion (setup, not the hot path).  The projections
+ * are the dense contractions of the drafter and the target (Sec. 3.1, Eq.
+ * 1-3); their bf16 weights are stored in the order the MFMA kernels consume
+ * them, so that every weight load of a wavefront is 1 KiB contiguous.
+ *
+ * src: device, row-major elem [rows][cols] (for gate_up: gate rows
+ * 0..rows/2-1, then up rows).  dst: device, rows * cols elem, must not
+ * overlap src; the caller owns both.
+ *   SB_F32:  dst is a plain copy (f32 weights stay row-major).
+ *   SB_BF16: needs rows % 32 == 0 and cols % 64 == 0 (src, dst 16-byte
+ *     aligned).  Logical row r' of block rb = r' / 32 is source row r' when
+ *     gate_up == 0; with gate_up != 0, logical row 32 rb + j is gate row
+ *     16 rb + j (j < 16) or up row rows/2 + 16 rb + j - 16.  Element
+ *       dst[((rb * (cols / 64) + kb) * 4 + i) * 512 + l * 8 + e]
+ *         = logical[32 rb + l % 32][64 kb + 32 (l / 32) + 8 i + e]
+ *     for l = 0..63, i = 0..3, e = 0..7.
+ * Enqueued on `stream`; errors: SB_EINVAL (NULL / misaligned / overlapping
+ * pointers, rows or cols < 1), SB_ESHAPE (bf16 sizes), SB_EDTYPE, SB_EHIP;
+ * the message is in sb_last_error(NULL). */
+int sb_pack_weight(const void* src, void* dst, int32_t rows, int32_t cols,
+                   int32_t dtype, int32_t gate_up, void* stream);
 
 /* Prefill (setup, not the hot path): causal target forward over each prompt
  * x_0..x_{n_s-1}, writing target K/V entries 0..n_s-1, the root x_{n_s}

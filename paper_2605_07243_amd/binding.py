@@ -97,7 +97,7 @@ PROF_CLASSES = ("gemm", "tree_attn", "vocab")
 EXPORTS = ["sb_row_capacity", "sb_workspace_bytes", "sb_create", "sb_destroy",
            "sb_last_error", "sb_bind", "sb_prefill", "sb_draft_block_expand",
            "sb_tree_verify", "sb_accept", "sb_commit", "sb_set_length_bound",
-           "sb_profile", "sb_profile_read"]
+           "sb_profile", "sb_profile_read", "sb_pack_weight"]
 
 _lib = None
 
@@ -126,6 +126,8 @@ def load(path: str = LIB_PATH):
     lib.sb_bind.argtypes = [vp, P(TargetWeights), P(DrafterWeights), vp,
                             C.c_size_t]
     lib.sb_bind.restype = C.c_int
+    lib.sb_pack_weight.argtypes = [vp, vp, i32, i32, i32, i32, vp]
+    lib.sb_pack_weight.restype = C.c_int
     lib.sb_prefill.argtypes = [vp, P(Seqs), vp, i32, P(i32), P(KV), P(KV), vp]
     lib.sb_prefill.restype = C.c_int
     lib.sb_draft_block_expand.argtypes = [vp, i32, i32, P(Seqs), P(KV),

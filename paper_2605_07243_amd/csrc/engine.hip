@@ -37,7 +37,7 @@ struct Carver {
 struct Dims {
   int S, d, H, Hkv, hd, F, V, L, LD, qkv_n, es;
   int K, M, B_max, budget, row_cap, rw, bw, vis_words, R_cap, chunk;
-  int tpages, dpages, n_chunks, ksplit_cap, n_split;
+  int tpages, dpages, n_chunks, n_split;
   size_t part_elems;
 };
 
@@ -68,12 +68,11 @@ Dims derive(const sb_config& c) {
   D.tpages = ceil_div(std::max(D.budget, D.chunk), 16);
   D.dpages = ceil_div(std::max(D.row_cap, D.chunk), 16);
   D.n_chunks = std::max(1, std::min(64, D.V / 2048));
-  D.ksplit_cap = 16;
   D.n_split = 32;
   // partial-sum buffer: the largest ks * N over the projections
   size_t mx = 0;
   auto upd = [&](int N, int Kd) {
-    mx = std::max(mx, (size_t)gemm_ksplit(N, Kd, D.ksplit_cap) * N);
+    mx = std::max(mx, (size_t)gemm_ksplit(N, Kd, D.es) * N);
   };
   upd(D.qkv_n, D.d);
   upd(D.d, D.H * D.hd);
@@ -264,6 +263,20 @@ static int validate_cfg(const sb_config* c, std::string& msg) {
     msg = "vocab and the QKV width must be multiples of 16";
     return SB_ESHAPE;
   }
+  {
+    const int es = c->dtype == SB_BF16 ? 2 : 4;
+    const int d = t.d_model, F = t.d_ff, hq = t.n_heads * t.head_dim;
+    const int qkv = (t.n_heads + 2 * t.n_kv_heads) * t.head_dim;
+    const int shapes[][2] = {{qkv, d},   {d, hq},    {2 * F, d}, {d, F},
+                             {d, 3 * d}, {d, 2 * d}, {t.vocab, d}};
+    for (const auto& nk : shapes)
+      if (!sb::gemm_shape_ok(nk[0], nk[1], es) || (es == 2 && F % 16)) {
+        msg = es == 2 ? "bf16 projections need output widths % 32 == 0 and "
+                        "input widths % 128 == 0 (d_model, d_ff, heads*head_dim)"
+                      : "projection widths must be multiples of 16 / 32";
+        return SB_ESHAPE;
+      }
+  }
   if (!(t.rope_theta > 0.f) || !(t.norm_eps > 0.f)) {
     msg = "rope_theta and norm_eps must be positive";
     return SB_EINVAL;
@@ -357,6 +370,43 @@ static int check_layer(sb_ctx* c, const sb_layer_weights& l, bool drafter) {
     return fail(c, SB_EINVAL, "layer weight pointer NULL or misaligned");
   if (drafter && bad_ptr(l.w_shift, 16))
     return fail(c, SB_EINVAL, "drafter layer needs w_shift");
+  return SB_OK;
+}
+
+int sb_pack_weight(const void* src, void* dst, int32_t rows, int32_t cols,
+                   int32_t dtype, int32_t gate_up, void* stream) {
+  auto err = [](int code, const char* m) {
+    g_create_err = m;
+    return code;
+  };
+  if (dtype != SB_F32 && dtype != SB_BF16)
+    return err(SB_EDTYPE, "sb_pack_weight: dtype must be SB_F32 or SB_BF16");
+  if (rows < 1 || cols < 1)
+    return err(SB_EINVAL, "sb_pack_weight: rows and cols must be >= 1");
+  const size_t bytes = (size_t)rows * cols * (dtype == SB_BF16 ? 2 : 4);
+  if (bad_ptr(src, 16) || bad_ptr(dst, 16))
+    return err(SB_EINVAL, "sb_pack_weight: src/dst NULL or not 16-byte aligned");
+  const uintptr_t a = reinterpret_cast<uintptr_t>(src);
+  const uintptr_t b = reinterpret_cast<uintptr_t>(dst);
+  if (a < b + bytes && b < a + bytes)
+    return err(SB_EINVAL, "sb_pack_weight: src and dst overlap");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (dtype == SB_F32) {
+    if (hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, st) != hipSuccess)
+      return err(SB_EHIP, "sb_pack_weight: hipMemcpyAsync failed");
+    return SB_OK;
+  }
+  if (rows % 32 || cols % 64)
+    return err(SB_ESHAPE, "sb_pack_weight: bf16 needs rows % 32 == 0 and cols % 64 == 0");
+  (void)hipGetLastError();
+  sb::launch_pack_weight(static_cast<const sb::bf16_t*>(src),
+                         static_cast<sb::bf16_t*>(dst), rows, cols, gate_up != 0,
+                         st);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    g_create_err = std::string("sb_pack_weight: ") + hipGetErrorString(e);
+    return SB_EHIP;
+  }
   return SB_OK;
 }
 
@@ -456,27 +506,27 @@ int gemm(sb_ctx* c, const void* X, int ldx, const void* W, int N, int K,
                             (size_t)c->D.R_cap * N, n, m_cap, ks, st);
 }
 
-// Gate/up projection + SwiGLU into out; fused in the GEMM epilogue where the
-// shape allows, else the GEMM's partials and a separate SwiGLU pass.
+// Gate/up projection + SwiGLU into out: bf16 in the GEMM epilogue (the
+// weight carries the gate/up interleave), f32 through partial sums and a
+// separate SwiGLU pass.
 template <typename T>
 void gate_up_swiglu(sb_ctx* c, const void* X, const void* W, const int* n,
                     int m_cap, T* out, hipStream_t st) {
   const Dims& D = c->D;
   if constexpr (sizeof(T) == 2) {
-    if (gemm_swiglu_fits(D.F, D.d, m_cap)) {
-      const double es = sizeof(T);
-      ProfScope ps(c, st, SB_PROF_GEMM,
-                   2.0 * D.F * D.d * es + (double)m_cap * D.d * es +
-                       (double)m_cap * D.F * es,
-                   2.0 * m_cap * 2 * D.F * D.d);
-      launch_gemm_swiglu(static_cast<const bf16_t*>(X), D.d,
-                         static_cast<const bf16_t*>(W), D.F, D.d, out, n,
-                         m_cap, st);
-      return;
-    }
+    const double es = sizeof(T);
+    ProfScope ps(c, st, SB_PROF_GEMM,
+                 2.0 * D.F * D.d * es + (double)m_cap * D.d * es +
+                     (double)m_cap * D.F * es,
+                 2.0 * m_cap * 2 * D.F * D.d);
+    launch_gemm_swiglu(static_cast<const bf16_t*>(X), D.d,
+                       static_cast<const bf16_t*>(W), D.F, D.d, out, n, m_cap,
+                       st);
+  } else {
+    const int ks = gemm<T>(c, X, D.d, W, 2 * D.F, D.d, n, m_cap, st);
+    launch_swiglu<T>(c->P, ks, (size_t)D.R_cap * 2 * D.F, n, m_cap, D.F, out,
+                     st);
   }
-  const int ks = gemm<T>(c, X, D.d, W, 2 * D.F, D.d, n, m_cap, st);
-  launch_swiglu<T>(c->P, ks, (size_t)D.R_cap * 2 * D.F, n, m_cap, D.F, out, st);
 }
 
 struct Prefix {

@@ -1,24 +1,40 @@
-// Weight-streaming projection GEMM on MFMA (gfx950).
+// Projection GEMMs on MFMA (gfx950).
 //
 //   P[ks][m][n] = sum_{k in K-chunk ks} X[m][k] * W[n][k]
 //
-// X holds the few activation rows of a call (<= 64 per m-chunk), W is a
-// row-major [N][K] weight matrix streamed from HBM once per m-chunk.  MFMA
-// 16x16x32 with weight rows as the A operand (16 features x 32 k) and
-// activation rows as the B operand, so a lane's four results are four
-// consecutive features of one row (one 16-byte store).  K-chunks
-// (gridDim.y) write separate partial sums that the consumer kernel adds,
-// which keeps results independent of scheduling order.
+// X holds the activation rows of a call (their count is read on the device),
+// W is a [N][K] weight matrix.  K-chunks (the split of the contraction
+// across workgroups) write separate partial sums that the consumer kernel
+// adds, which keeps results independent of scheduling order.
 //
-// bf16 path (gemm_stream_kernel): a workgroup of NW waves owns 16 NW
-// features and one K-chunk.  Each wave streams its own 16 weight rows with
-// row-contiguous 16-byte loads (a wave instruction covers 1 KiB of whole row
-// segments, so every HBM line is used by one instruction), one K-stage ahead
-// in registers, and transposes them into MFMA order through a wave-private
-// LDS tile.  The workgroup stages the activation K-slice in LDS once
-// (double buffered) and all its waves read it from there, so activation
-// traffic does not grow with the number of weight rows.  fp32 path
-// (gemm_xwt_kernel): weight fragments load straight into registers.
+// bf16 (gemm_tile_kernel).  Weights are stored fragment-packed (the layout
+// sb_pack_weight writes): 32-row x 64-column blocks of 4 KiB, block
+// (rb, kb) at element offset (rb * K/64 + kb) * 2048, and inside a block
+// four 1 KiB sub-steps i, lane l holding the 8 elements
+//   W[32 rb + l % 32][64 kb + 32 (l / 32) + 8 i + e],  e = 0..7.
+// That is the A operand of v_mfma_f32_32x32x16_bf16 for sub-step i when the
+// contraction index of the 64-column block is permuted so that lane group
+// l / 32 owns 32 consecutive columns; the activation operand is read with
+// the same permutation, so the product is unchanged.  Every weight load of
+// a wave is one contiguous 1 KiB, straight into registers (no LDS pass), a
+// few K-stages ahead of the MFMAs.
+//
+// A workgroup (4 waves) owns 32 MF activation rows and 128 NF weight rows
+// (32 NF per wave).  The activation K-slice is staged once per workgroup in
+// LDS (double buffered, rows padded so the 16-byte MFMA operand reads are
+// conflict-free) and read by all waves; activation rows are therefore the
+// MFMA B operand and a lane's outputs are four consecutive features of one
+// row (one 16-byte store).  Workgroup ids are remapped so that the
+// workgroups resident on one XCD (ids congruent mod 8) take consecutive
+// tiles: the activation row tiles of one weight tile run on the same XCD
+// and share its weight lines in that XCD's L2.
+//
+// The SwiGLU variant reads a gate/up weight packed with 16 gate rows and the
+// matching 16 up rows per 32-row block: a lane then holds gate and up of the
+// same features and writes act = silu(gate) * up directly.
+//
+// f32 (gemm_xwt_kernel): row-major weights, fragments load straight into
+// registers and eight v_mfma_f32_16x16x4_f32 per 32-wide step.
 #include <algorithm>
 
 #include "common.h"
@@ -26,147 +42,199 @@
 
 namespace sb {
 
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ uint4 load_stream16(const void* p) {
-  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
-  return make_uint4(v[0], v[1], v[2], v[3]);
+// acc[32x32] += A[32 x 16] * B[16 x 32]; lane l holds row l % 32 of A and
+// column l % 32 of B, each with 8 contraction indices of lane group l / 32.
+// Output register r of lane l: acc[8 (r / 4) + 4 (l / 32) + r % 4][l % 32].
+__device__ __forceinline__ f32x16_t mma_32x32x16(u32x4_t a, u32x4_t b,
+                                                 f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+      __builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c, 0,
+      0, 0);
 }
 
-// SWIGLU: the weight is [gate; up] ([2F][K]) and the workgroup owns gate
-// features j0 .. j0 + 8 NW - 1 (first NW/2 waves) and the matching up
-// features (last NW/2 waves); with one K-chunk the epilogue writes
-// act[m][j] = silu(gate) * up as bf16 instead of partial sums.
-template <int MT, int NW, int KT, bool SWIGLU>
-__global__ __launch_bounds__(NW * 64) void gemm_stream_kernel(
+__device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
+
+// MF: 32-row activation tiles per workgroup; NF: 32-row weight fragments
+// per wave; PF: K-stages (64 columns each) of weights in flight per wave.
+template <int MF, int NF, int PF, bool SWIGLU>
+__global__ __launch_bounds__(256) void gemm_tile_kernel(
     const bf16_t* __restrict__ X, int ldx, const bf16_t* __restrict__ W,
     int K, float* __restrict__ P, int N, size_t part_stride,
-    const int* __restrict__ m_count, int k_chunk, bf16_t* __restrict__ act,
-    int F) {
-  constexpr int LD = KT + 8;                        // padded LDS row
-  constexpr int RPI = 1024 / (KT * 2);              // rows per wave load
-  constexpr int NI = 16 / RPI;                      // loads per stage
-  constexpr int XCH = MT * 16 * KT / 8;             // 16-byte X chunks
-  constexpr int XPT = (XCH + NW * 64 - 1) / (NW * 64);
-  __shared__ __attribute__((aligned(16))) bf16_t wl[NW][16][LD];
-  __shared__ __attribute__((aligned(16))) bf16_t xs[2][MT * 16][LD];
-  const int m_base = blockIdx.z * (MT * 16);
-  const int M = min(*m_count - m_base, MT * 16);
-  if (M <= 0) return;
+    const int* __restrict__ m_count, int k_chunk, int n_mt, int n_nt,
+    bf16_t* __restrict__ act, int F) {
+  static_assert(PF == 2 || PF == 4, "weight ring depth");
+  constexpr int BM = 32 * MF;
+  constexpr int LD = 64 + 8;
+  __shared__ __attribute__((aligned(16))) bf16_t xs[2][BM][LD];
+  const int total = gridDim.x;
+  int b = blockIdx.x;
+  if ((total & 7) == 0) b = (b & 7) * (total >> 3) + (b >> 3);
+  const int mt = b % n_mt;
+  const int rest = b / n_mt;
+  const int nt = rest % n_nt;
+  const int kc = rest / n_nt;
+  const int M = *m_count;
+  const int m_base = mt * BM;
+  if (m_base >= M) return;  // whole workgroup
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int r = lane & 15, g = lane >> 4;
-  int n0 = blockIdx.x * 16 * NW + wave * 16;
-  if constexpr (SWIGLU) {
-    constexpr int HW = NW / 2;
-    n0 = blockIdx.x * 16 * HW + (wave % HW) * 16 + (wave >= HW ? F : 0);
+  const int lr = lane & 31, h = lane >> 5;
+  const int nb = nt * (128 * NF) + wave * (32 * NF);  // first weight row
+  const bool wave_on = nb < N;                         // N % 32 == 0 tails
+  const int kc0 = kc * k_chunk;
+  const int nstage = k_chunk / 64;
+  const int kblocks = K / 64;
+  const bf16_t* wp[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    const int rb = min((nb >> 5) + f, N / 32 - 1);
+    wp[f] = W + ((size_t)rb * kblocks + kc0 / 64) * 2048 + lane * 8;
   }
-  const int kc0 = blockIdx.y * k_chunk;
-  const int kc1 = min(K, kc0 + k_chunk);
-  const int nstage = (kc1 - kc0) / KT;
-  const int lrow = lane / (KT / 8), lcol = (lane % (KT / 8)) * 8;
-  const bf16_t* wsrc = W + (size_t)(n0 + lrow) * K + kc0 + lcol;
-  const bf16_t* xbase = X + (size_t)m_base * ldx + kc0;
-  f32x4_t acc[MT];
+  // activation chunks of this thread: c = tid + 256 q is row c / 8,
+  // 16-byte column chunk c % 8 of the stage; rows >= M repeat row M - 1
+  // (their outputs are not stored)
+  const bf16_t* xp[MF];
 #pragma unroll
-  for (int t = 0; t < MT; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  uint4 stg[NI];
-  uint4 xr[XPT];
+  for (int q = 0; q < MF; ++q) {
+    const int c = tid + 256 * q;
+    const int row = min(m_base + c / 8, M - 1);
+    xp[q] = X + (size_t)row * ldx + kc0 + 8 * (c % 8);
+  }
+  u32x4_t wq[PF][NF][4];
+  u32x4_t xq[2][MF];
+  f32x16_t acc[MF][NF];
 #pragma unroll
-  for (int i = 0; i < NI; ++i) stg[i] = load_stream16(wsrc + (size_t)(i * RPI) * K);
-  auto xfetch = [&](int st) {
+  for (int t = 0; t < MF; ++t)
 #pragma unroll
-    for (int q = 0; q < XPT; ++q) {
-      const int c = tid + q * NW * 64;
-      const int row = c / (KT / 8), col = (c % (KT / 8)) * 8;
-      xr[q] = (c < XCH && row < M)
-                  ? *reinterpret_cast<const uint4*>(xbase + (size_t)row * ldx +
-                                                    st * KT + col)
-                  : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto xstore = [&](int buf) {
+    for (int f = 0; f < NF; ++f)
 #pragma unroll
-    for (int q = 0; q < XPT; ++q) {
-      const int c = tid + q * NW * 64;
-      const int row = c / (KT / 8), col = (c % (KT / 8)) * 8;
-      if (c < XCH) *reinterpret_cast<uint4*>(&xs[buf][row][col]) = xr[q];
-    }
-  };
-  xfetch(0);
-  xstore(0);
+      for (int r = 0; r < 16; ++r) acc[t][f][r] = 0.f;
+
+  // Stage s: weights in wq[s % PF], activations in LDS buffer s & 1.  In
+  // iteration s the activations of stage s + 2 are fetched into registers
+  // (slot s & 1) before the MFMAs and the weights of stage s + PF after
+  // them; the activations of stage s + 1 go to LDS at the end.  Stage
+  // indices past the chunk re-read its last stage (results unused) so that
+  // every iteration issues the same loads.
+#define SB_SCHED __builtin_amdgcn_sched_barrier(0);
+#define SB_ISSUE_W(p, s_)                                                     \
+  {                                                                           \
+    const size_t so = (size_t)min((s_), nstage - 1) * 2048;                   \
+    _Pragma("unroll") for (int f = 0; f < NF; ++f)                            \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i) wq[p][f][i] =               \
+        *reinterpret_cast<const u32x4_t*>(wp[f] + so + 512 * i);              \
+  }
+#define SB_ISSUE_X(slot, s_)                                                  \
+  {                                                                           \
+    const size_t so = (size_t)min((s_), nstage - 1) * 64;                     \
+    _Pragma("unroll") for (int q = 0; q < MF; ++q) xq[slot][q] =              \
+        *reinterpret_cast<const u32x4_t*>(xp[q] + so);                        \
+  }
+#define SB_STORE_X(slot, buf)                                                 \
+  {                                                                           \
+    _Pragma("unroll") for (int q = 0; q < MF; ++q) {                          \
+      const int c = tid + 256 * q;                                            \
+      *reinterpret_cast<u32x4_t*>(&xs[buf][c / 8][8 * (c % 8)]) = xq[slot][q]; \
+    }                                                                         \
+  }
+#define SB_READ_X(dst, buf, i)                                                \
+  _Pragma("unroll") for (int t = 0; t < MF; ++t) dst[t] =                     \
+      *reinterpret_cast<const u32x4_t*>(&xs[buf][32 * t + lr][32 * h + 8 * (i)]);
+#define SB_MMA(p, i, src)                                                     \
+  _Pragma("unroll") for (int t = 0; t < MF; ++t)                              \
+  _Pragma("unroll") for (int f = 0; f < NF; ++f)                              \
+    acc[t][f] = mma_32x32x16(wq[p][f][i], src[t], acc[t][f]);
+  // the activation operands of sub-step i + 1 are read from LDS while the
+  // MFMAs of sub-step i run
+#define SB_STAGE(p)                                                           \
+  {                                                                           \
+    const int s = s0 + (p);                                                   \
+    u32x4_t xa[MF], xb[MF];                                                   \
+    SB_READ_X(xa, (p) & 1, 0)                                                 \
+    SB_ISSUE_X((p) & 1, s + 2)                                                \
+    SB_READ_X(xb, (p) & 1, 1)                                                 \
+    SB_SCHED SB_MMA(p, 0, xa) SB_SCHED                                        \
+    SB_READ_X(xa, (p) & 1, 2)                                                 \
+    SB_SCHED SB_MMA(p, 1, xb) SB_SCHED                                        \
+    SB_READ_X(xb, (p) & 1, 3)                                                 \
+    SB_SCHED SB_MMA(p, 2, xa) SB_SCHED                                        \
+    SB_MMA(p, 3, xb)                                                          \
+    SB_ISSUE_W(p, s + PF)                                                     \
+    SB_STORE_X(((p) + 1) & 1, ((p) + 1) & 1)                                  \
+    __syncthreads();                                                          \
+  }
+  SB_ISSUE_X(0, 0)
+  SB_ISSUE_W(0, 0)
+  SB_ISSUE_X(1, 1)
+  SB_ISSUE_W(1, 1)
+  if constexpr (PF == 4) {
+    SB_ISSUE_W(2, 2)
+    SB_ISSUE_W(3, 3)
+  }
+  SB_STORE_X(0, 0)
   __syncthreads();
-  for (int st = 0; st < nstage; ++st) {
-    const int buf = st & 1;
-    // this stage's weight rows into the wave's LDS tile, next stage's loads
-    // in flight during the MFMAs
-#pragma unroll
-    for (int i = 0; i < NI; ++i)
-      *reinterpret_cast<uint4*>(&wl[wave][i * RPI + lrow][lcol]) = stg[i];
-    if (st + 1 < nstage) {
-#pragma unroll
-      for (int i = 0; i < NI; ++i)
-        stg[i] = load_stream16(wsrc + (size_t)(i * RPI) * K + (size_t)(st + 1) * KT);
-      xfetch(st + 1);
+  for (int s0 = 0; s0 < nstage; s0 += PF) {
+    SB_STAGE(0)
+    SB_STAGE(1)
+    if constexpr (PF == 4) {
+      SB_STAGE(2)
+      SB_STAGE(3)
     }
-#pragma unroll
-    for (int j = 0; j < KT / 32; ++j) {
-      Frag8<bf16_t> wf;
-      wf.v = *reinterpret_cast<const uint4*>(&wl[wave][r][j * 32 + g * 8]);
-#pragma unroll
-      for (int t = 0; t < MT; ++t) {
-        Frag8<bf16_t> xf;
-        xf.v = *reinterpret_cast<const uint4*>(&xs[buf][t * 16 + r][j * 32 + g * 8]);
-        acc[t] = mma_16x16x32(wf, xf, acc[t]);
-      }
-    }
-    if (st + 1 < nstage) xstore(buf ^ 1);
-    __syncthreads();
   }
+#undef SB_STAGE
+#undef SB_MMA
+#undef SB_READ_X
+#undef SB_STORE_X
+#undef SB_ISSUE_X
+#undef SB_ISSUE_W
+#undef SB_SCHED
+  if (!wave_on) return;
   if constexpr (SWIGLU) {
-    // up waves hand their sums to the gate waves through LDS (the loop
-    // ended with a barrier, so the X tiles are free)
-    constexpr int HW = NW / 2;
-    f32x4_t* ex = reinterpret_cast<f32x4_t*>(&xs[0][0][0]);
-    static_assert(sizeof(xs) >= HW * MT * 64 * sizeof(f32x4_t), "LDS");
-    if (wave >= HW) {
+    // fragment f covers gate/up features 16 (nb / 32 + f) .. + 15; lane
+    // registers 0-7 hold gate rows 8 q + 4 h + e, registers 8-15 the up rows
+    // of the same features
 #pragma unroll
-      for (int t = 0; t < MT; ++t) ex[((wave - HW) * MT + t) * 64 + lane] = acc[t];
-    }
-    __syncthreads();
-    if (wave < HW) {
+    for (int t = 0; t < MF; ++t) {
+      const int m = m_base + 32 * t + lr;
+      if (m >= M) continue;
 #pragma unroll
-      for (int t = 0; t < MT; ++t) {
-        const int m = t * 16 + r;
-        const f32x4_t u = ex[(wave * MT + t) * 64 + lane];
-        float o[4];
+      for (int f = 0; f < NF; ++f) {
+        const int j0 = 16 * ((nb >> 5) + f);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float gt = acc[t][e];
-          o[e] = gt / (1.0f + expf(-gt)) * u[e];
-        }
-        if (m < M) {
+        for (int q = 0; q < 2; ++q) {
+          float o[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            o[e] = silu(acc[t][f][4 * q + e]) * acc[t][f][8 + 4 * q + e];
           uint2 pk;
           pk.x = (uint32_t)f32_to_bf16(o[0]) | ((uint32_t)f32_to_bf16(o[1]) << 16);
           pk.y = (uint32_t)f32_to_bf16(o[2]) | ((uint32_t)f32_to_bf16(o[3]) << 16);
-          *reinterpret_cast<uint2*>(act + (size_t)(m_base + m) * F + n0 + 4 * g) = pk;
+          *reinterpret_cast<uint2*>(act + (size_t)m * F + j0 + 8 * q + 4 * h) = pk;
         }
       }
     }
     return;
   }
-  float* out = P + (size_t)blockIdx.y * part_stride;
+  float* out = P + (size_t)kc * part_stride;
 #pragma unroll
-  for (int t = 0; t < MT; ++t) {
-    const int m = t * 16 + r;
-    if (m < M)
-      *reinterpret_cast<float4*>(out + (size_t)(m_base + m) * N + n0 + 4 * g) =
-          make_float4(acc[t][0], acc[t][1], acc[t][2], acc[t][3]);
+  for (int t = 0; t < MF; ++t) {
+    const int m = m_base + 32 * t + lr;
+    if (m >= M) continue;
+#pragma unroll
+    for (int f = 0; f < NF; ++f)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<float4*>(out + (size_t)m * N + nb + 32 * f + 8 * q + 4 * h) =
+            make_float4(acc[t][f][4 * q], acc[t][f][4 * q + 1],
+                        acc[t][f][4 * q + 2], acc[t][f][4 * q + 3]);
   }
 }
 
-template <typename T, int MT>
+template <int MT>
 __global__ __launch_bounds__(256) void gemm_xwt_kernel(
-    const T* __restrict__ X, int ldx, const T* __restrict__ W, int K,
+    const float* __restrict__ X, int ldx, const float* __restrict__ W, int K,
     float* __restrict__ P, int N, size_t part_stride,
     const int* __restrict__ m_count, int k_chunk) {
   const int m_base = blockIdx.z * (MT * 16);
@@ -182,8 +250,8 @@ __global__ __launch_bounds__(256) void gemm_xwt_kernel(
   const int s0 = wave * per;
   const int s1 = min(nsteps, s0 + per);
 
-  const T* wp = W + (size_t)(n0 + r) * K + kc0 + g * 8;
-  const T* xp[MT];
+  const float* wp = W + (size_t)(n0 + r) * K + kc0 + g * 8;
+  const float* xp[MT];
   bool xv[MT];
 #pragma unroll
   for (int t = 0; t < MT; ++t) {
@@ -197,8 +265,8 @@ __global__ __launch_bounds__(256) void gemm_xwt_kernel(
 
   constexpr int U = 4;
   for (int s = s0; s < s1; s += U) {
-    Frag8<T> wf[U];
-    Frag8<T> xf[U][MT];
+    Frag8<float> wf[U];
+    Frag8<float> xf[U][MT];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       if (s + u < s1) {
@@ -241,114 +309,134 @@ __global__ __launch_bounds__(256) void gemm_xwt_kernel(
   }
 }
 
+// Packs row-major src [rows][cols] into the fragment layout, one 16-byte
+// chunk per thread.  gate_up: src is [gate; up] ([2F][cols], F = rows / 2)
+// and packed row 32 rb + j is gate row 16 rb + j (j < 16) or up row
+// 16 rb + j - 16.
+__global__ void pack_kernel(const bf16_t* __restrict__ src,
+                            bf16_t* __restrict__ dst, int rows, int cols,
+                            bool gate_up, size_t chunks) {
+  const size_t c = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= chunks) return;
+  const int kblocks = cols / 64;
+  const size_t blk = c >> 8;
+  const int i = (int)((c >> 6) & 3), l = (int)(c & 63);
+  const int rb = (int)(blk / kblocks), kb = (int)(blk % kblocks);
+  const int j = l & 31;
+  int row = 32 * rb + j;
+  if (gate_up) row = j < 16 ? 16 * rb + j : rows / 2 + 16 * rb + (j - 16);
+  const int col = 64 * kb + 32 * (l >> 5) + 8 * i;
+  *reinterpret_cast<uint4*>(dst + c * 8) =
+      *reinterpret_cast<const uint4*>(src + (size_t)row * cols + col);
+}
+
+namespace {
+
+constexpr int kTargetWorkgroups = 256;  // one per CU
+
+// K must be a multiple of 64 * pf * ks (whole weight rings per chunk).
+int pick_split(int tiles, int K, int pf) {
+  int ks = 1;
+  while (ks < 16 && tiles * ks * 2 <= kTargetWorkgroups &&
+         K % (64 * pf * ks * 2) == 0)
+    ks *= 2;
+  return ks;
+}
+
+}  // namespace
+
+bool gemm_shape_ok(int N, int K, int elem_bytes) {
+  if (elem_bytes == 4) return N % 16 == 0 && K % 32 == 0;
+  return N % 32 == 0 && K % 128 == 0;
+}
+
 GemmPlan gemm_plan(int N, int K, int m_cap, int elem_bytes) {
   GemmPlan g{};
-  g.mt = m_cap <= 16 ? 1 : (m_cap <= 32 ? 2 : 4);
-  if (elem_bytes == 2 && N % 64 == 0 && K % 128 == 0) {
-    g.stream = true;
-    g.kt = (g.mt == 4 || K % 256 != 0) ? 128 : 256;
-    g.nw = (g.mt == 4 && N >= 65536 && N % 128 == 0) ? 8 : 4;
-    const int tiles = N / (16 * g.nw);
-    g.ks = 1;
-    // enough workgroups to fill the chip; each K-chunk a whole number of
-    // stages and at least four of them
-    while (tiles * g.ks < 400 && g.ks < 16 && K % (g.ks * 2 * g.kt) == 0 &&
-           K / (g.ks * 2) >= 4 * g.kt)
-      g.ks *= 2;
-  } else {
-    g.stream = false;
+  if (elem_bytes == 4) {
+    g.mf = m_cap <= 16 ? 1 : (m_cap <= 32 ? 2 : 4);  // 16-row tiles
     const int tiles = N / 16;
     g.ks = 1;
     while (tiles * g.ks < 1024 && K / (32 * (g.ks * 2)) >= 32 && g.ks < 16)
       g.ks *= 2;
+    return g;
   }
+  g.mf = m_cap <= 32 ? 1 : m_cap <= 64 ? 2 : m_cap < 512 ? 4 : 8;
+  g.nf = (g.mf == 8 || (g.mf == 4 && m_cap > 128)) && N % 64 == 0 ? 2 : 1;
+  g.pf = (g.mf == 4 && (K / 64) % 4 == 0) ? 4 : 2;
+  const int n_mt = (m_cap + 32 * g.mf - 1) / (32 * g.mf);
+  const int n_nt = (N + 128 * g.nf - 1) / (128 * g.nf);
+  g.ks = pick_split(n_mt * n_nt, K, g.pf);
   return g;
 }
 
-int gemm_ksplit(int N, int K, int ksplit_cap) {
-  (void)ksplit_cap;
-  int mx = 1;
-  for (int mc : {16, 32, 64}) {
-    mx = std::max(mx, gemm_plan(N, K, mc, 2).ks);
-    mx = std::max(mx, gemm_plan(N, K, mc, 4).ks);
-  }
-  return mx;
+int gemm_ksplit(int N, int K, int elem_bytes) {
+  // fewest row tiles -> most K-chunks
+  return gemm_plan(N, K, 1, elem_bytes).ks;
 }
+
+namespace {
+
+template <bool SWIGLU>
+void launch_tile(const GemmPlan& g, const bf16_t* X, int ldx, const bf16_t* W,
+                 int N, int K, float* P, size_t part_stride,
+                 const int* m_count, int m_cap, int ks, bf16_t* act, int F,
+                 hipStream_t st) {
+  const int n_mt = (m_cap + 32 * g.mf - 1) / (32 * g.mf);
+  const int n_nt = (N + 128 * g.nf - 1) / (128 * g.nf);
+  const int k_chunk = K / ks;
+  const dim3 grid(n_mt * n_nt * ks);
+#define SB_LAUNCH(MF_, NF_, PF_)                                              \
+  if (g.mf == MF_ && g.nf == NF_ && g.pf == PF_) {                            \
+    gemm_tile_kernel<MF_, NF_, PF_, SWIGLU><<<grid, 256, 0, st>>>(            \
+        X, ldx, W, K, P, N, part_stride, m_count, k_chunk, n_mt, n_nt, act,   \
+        F);                                                                   \
+    return;                                                                   \
+  }
+  SB_LAUNCH(1, 1, 2)
+  SB_LAUNCH(2, 1, 2)
+  SB_LAUNCH(4, 1, 2)
+  SB_LAUNCH(4, 1, 4)
+  SB_LAUNCH(4, 2, 2)
+  SB_LAUNCH(4, 2, 4)
+  SB_LAUNCH(8, 1, 2)
+  SB_LAUNCH(8, 2, 2)
+#undef SB_LAUNCH
+}
+
+}  // namespace
 
 template <typename T>
 int launch_gemm_xwt(const T* X, int ldx, const T* W, int N, int K, float* P,
                     size_t part_stride, const int* m_count, int m_cap,
                     int ksplit, hipStream_t st) {
   const GemmPlan g = gemm_plan(N, K, m_cap, sizeof(T));
-  const int ks_req = ksplit > 0 ? std::min(ksplit, g.ks) : g.ks;
-  const int mz = (m_cap + 63) / 64;
   if constexpr (sizeof(T) == 2) {
-    if (g.stream) {
-      const int ks = ks_req;
-      const int k_chunk = K / ks;
-      const dim3 grid(N / (16 * g.nw), ks, g.mt == 4 ? mz : 1);
-#define SB_LAUNCH(MT_, NW_, KT_)                                              \
-  if (g.mt == MT_ && g.nw == NW_ && g.kt == KT_) {                            \
-    gemm_stream_kernel<MT_, NW_, KT_, false><<<grid, NW_ * 64, 0, st>>>(      \
-        X, ldx, W, K, P, N, part_stride, m_count, k_chunk, nullptr, 0);       \
-    return ks;                                                                \
-  }
-      SB_LAUNCH(1, 4, 256)
-      SB_LAUNCH(1, 4, 128)
-      SB_LAUNCH(2, 4, 256)
-      SB_LAUNCH(2, 4, 128)
-      SB_LAUNCH(4, 4, 128)
-      SB_LAUNCH(4, 8, 128)
-#undef SB_LAUNCH
-    }
-  }
-  const int steps = K / 32;
-  const int per = (steps + ks_req - 1) / ks_req;
-  const int k_chunk = per * 32;
-  const int ks = (K + k_chunk - 1) / k_chunk;
-  dim3 block(256);
-  if (m_cap <= 16) {
-    dim3 grid(N / 16, ks, 1);
-    gemm_xwt_kernel<T, 1><<<grid, block, 0, st>>>(X, ldx, W, K, P, N,
-                                                  part_stride, m_count, k_chunk);
-  } else if (m_cap <= 32) {
-    dim3 grid(N / 16, ks, 1);
-    gemm_xwt_kernel<T, 2><<<grid, block, 0, st>>>(X, ldx, W, K, P, N,
-                                                  part_stride, m_count, k_chunk);
+    int ks = g.ks;
+    if (ksplit > 0)
+      while (ks > ksplit) ks /= 2;
+    launch_tile<false>(g, X, ldx, W, N, K, P, part_stride, m_count, m_cap, ks,
+                       nullptr, 0, st);
+    return ks;
   } else {
-    dim3 grid(N / 16, ks, mz);
-    gemm_xwt_kernel<T, 4><<<grid, block, 0, st>>>(X, ldx, W, K, P, N,
-                                                  part_stride, m_count, k_chunk);
+    const int ks_req = ksplit > 0 ? std::min(ksplit, g.ks) : g.ks;
+    const int steps = K / 32;
+    const int per = (steps + ks_req - 1) / ks_req;
+    const int k_chunk = per * 32;
+    const int ks = (K + k_chunk - 1) / k_chunk;
+    const int mz = (m_cap + 63) / 64;
+    const dim3 block(256);
+    if (m_cap <= 16) {
+      gemm_xwt_kernel<1><<<dim3(N / 16, ks, 1), block, 0, st>>>(
+          X, ldx, W, K, P, N, part_stride, m_count, k_chunk);
+    } else if (m_cap <= 32) {
+      gemm_xwt_kernel<2><<<dim3(N / 16, ks, 1), block, 0, st>>>(
+          X, ldx, W, K, P, N, part_stride, m_count, k_chunk);
+    } else {
+      gemm_xwt_kernel<4><<<dim3(N / 16, ks, mz), block, 0, st>>>(
+          X, ldx, W, K, P, N, part_stride, m_count, k_chunk);
+    }
+    return ks;
   }
-  return ks;
-}
-
-bool gemm_swiglu_fits(int F, int K, int m_cap) {
-  const GemmPlan g = gemm_plan(2 * F, K, m_cap, 2);
-  return g.stream && g.ks == 1 && F % (8 * g.nw) == 0;
-}
-
-bool launch_gemm_swiglu(const bf16_t* X, int ldx, const bf16_t* W, int F,
-                        int K, bf16_t* act, const int* m_count, int m_cap,
-                        hipStream_t st) {
-  if (!gemm_swiglu_fits(F, K, m_cap)) return false;
-  const GemmPlan g = gemm_plan(2 * F, K, m_cap, 2);
-  const int mz = (m_cap + 63) / 64;
-  const dim3 grid(F / (8 * g.nw), 1, g.mt == 4 ? mz : 1);
-#define SB_LAUNCH_SW(MT_, NW_, KT_)                                           \
-  if (g.mt == MT_ && g.nw == NW_ && g.kt == KT_) {                            \
-    gemm_stream_kernel<MT_, NW_, KT_, true><<<grid, NW_ * 64, 0, st>>>(       \
-        X, ldx, W, K, nullptr, 2 * F, 0, m_count, K, act, F);                 \
-    return true;                                                              \
-  }
-  SB_LAUNCH_SW(1, 4, 256)
-  SB_LAUNCH_SW(1, 4, 128)
-  SB_LAUNCH_SW(2, 4, 256)
-  SB_LAUNCH_SW(2, 4, 128)
-  SB_LAUNCH_SW(4, 4, 128)
-  SB_LAUNCH_SW(4, 8, 128)
-#undef SB_LAUNCH_SW
-  return false;
 }
 
 template int launch_gemm_xwt<float>(const float*, int, const float*, int, int,
@@ -357,5 +445,23 @@ template int launch_gemm_xwt<float>(const float*, int, const float*, int, int,
 template int launch_gemm_xwt<bf16_t>(const bf16_t*, int, const bf16_t*, int,
                                      int, float*, size_t, const int*, int, int,
                                      hipStream_t);
+
+void launch_gemm_swiglu(const bf16_t* X, int ldx, const bf16_t* W, int F,
+                        int K, bf16_t* act, const int* m_count, int m_cap,
+                        hipStream_t st) {
+  const GemmPlan g = gemm_plan(2 * F, K, m_cap, 2);
+  launch_tile<true>(g, X, ldx, W, 2 * F, K, nullptr, 0, m_count, m_cap, 1,
+                    act, F, st);
+}
+
+int launch_pack_weight(const bf16_t* src, bf16_t* dst, int rows, int cols,
+                       bool gate_up, hipStream_t st) {
+  const size_t chunks = (size_t)rows * cols / 8;
+  if (chunks == 0) return 0;
+  const size_t blocks = (chunks + 255) / 256;
+  pack_kernel<<<dim3((unsigned)blocks), 256, 0, st>>>(src, dst, rows, cols,
+                                                      gate_up, chunks);
+  return 0;
+}
 
 }  // namespace sb

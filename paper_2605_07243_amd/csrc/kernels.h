@@ -47,27 +47,34 @@ struct KVView {
   int seg_pages;            // pages per sequence in the segment pool
 };
 
+// Projection GEMM plan.  bf16: 32-row activation tiles per workgroup (mf),
+// 32-row weight fragments per wave (nf), weight stages in flight (pf);
+// f32: mf 16-row tiles.  ks: K-chunks (partial sums).
 struct GemmPlan {
-  bool stream;   // bf16 LDS-streamed kernel
-  int mt, nw, kt, ks;
+  int mf, nf, pf, ks;
 };
+// Shapes the GEMMs take: bf16 N % 32 == 0 and K % 128 == 0 (fragment-packed
+// weights); f32 N % 16 == 0 and K % 32 == 0.
+bool gemm_shape_ok(int N, int K, int elem_bytes);
 GemmPlan gemm_plan(int N, int K, int m_cap, int elem_bytes);
 // Largest K-split any call of this shape may use (partial-buffer sizing).
-int gemm_ksplit(int N, int K, int ksplit_cap);
-// ksplit <= 0: the plan's split; otherwise at most ksplit K-chunks.
-// Returns the number of K-chunks written.
+int gemm_ksplit(int N, int K, int elem_bytes);
+// P[ks][m][n] = X[m] . W[n] over K-chunk ks for the first *m_count rows.
+// bf16 W is fragment-packed, f32 W row-major.  ksplit <= 0: the plan's
+// split; otherwise at most ksplit K-chunks.  Returns the K-chunks written.
 template <typename T>
 int launch_gemm_xwt(const T* X, int ldx, const T* W, int N, int K, float* P,
                     size_t part_stride, const int* m_count, int m_cap,
                     int ksplit, hipStream_t st);
-// Gate/up projection with SwiGLU fused into the epilogue (bf16, weight
-// [gate; up] of [2F][K], one K-chunk): act[m][j] = silu(gate) * up for the
-// first *m_count rows.  Returns false when the shape does not take this
-// path; the caller then runs launch_gemm_xwt and launch_swiglu.
-bool gemm_swiglu_fits(int F, int K, int m_cap);
-bool launch_gemm_swiglu(const bf16_t* X, int ldx, const bf16_t* W, int F,
+// Gate/up projection with SwiGLU in the epilogue (bf16; W packed with the
+// gate_up interleave, [2F][K] logical): act[m][j] = silu(gate_j) * up_j for
+// the first *m_count rows, act row stride F.
+void launch_gemm_swiglu(const bf16_t* X, int ldx, const bf16_t* W, int F,
                         int K, bf16_t* act, const int* m_count, int m_cap,
                         hipStream_t st);
+// Row-major bf16 [rows][cols] -> fragment-packed (rows % 32, cols % 64).
+int launch_pack_weight(const bf16_t* src, bf16_t* dst, int rows, int cols,
+                       bool gate_up, hipStream_t st);
 
 template <typename T>
 void launch_embed(const CallPlan& p, const T* embed, int d, float* x,

@@ -4,7 +4,8 @@ PyTorch is used for device memory and the stream only; every step of the
 hot path runs in the library's HIP kernels (there is no fallback).  This
 module allocates the caches, tree and output buffers the C ABI describes,
 packs weights into the library's layout ([Wq; Wk; Wv] and [Wg; Wu] row
-concatenations) and marshals arguments.
+concatenations, bf16 projections fragment-packed by sb_pack_weight) and
+marshals arguments.
 """
 from __future__ import annotations
 
@@ -105,6 +106,18 @@ class Runtime:
                               dev)
             return t.float() if fp32 else t
 
+        def pack(t, gate_up=False):
+            """Projection matrix in the library's layout (bf16: fragment
+            packed by sb_pack_weight; f32: unchanged)."""
+            if self.et != torch.bfloat16:
+                return t
+            out = torch.empty_like(t)
+            B.check(self.lib, None, self.lib.sb_pack_weight(
+                _ptr(t), _ptr(out), t.shape[0], t.shape[1], B.SB_BF16,
+                int(gate_up), C.c_void_p(
+                    torch.cuda.current_stream(dev).cuda_stream)))
+            return out
+
         def layer(prefix, drafter):
             qkv = torch.cat([get(prefix + "wq", (s.q_dim, d)),
                              get(prefix + "wk", (s.kv_dim, d)),
@@ -112,11 +125,13 @@ class Runtime:
             gu = torch.cat([get(prefix + "wg", (F, d)),
                             get(prefix + "wu", (F, d))]).contiguous()
             t = dict(attn_norm=get(prefix + "attn_norm", (d,), "ones"),
-                     w_qkv=qkv, w_o=get(prefix + "wo", (d, s.q_dim)),
+                     w_qkv=pack(qkv), w_o=pack(get(prefix + "wo", (d, s.q_dim))),
                      mlp_norm=get(prefix + "mlp_norm", (d,), "ones"),
-                     w_gate_up=gu, w_down=get(prefix + "wd", (d, F)),
-                     w_shift=get(prefix + "w_shift", (d, 2 * d))
+                     w_gate_up=pack(gu, True),
+                     w_down=pack(get(prefix + "wd", (d, F))),
+                     w_shift=pack(get(prefix + "w_shift", (d, 2 * d)))
                      if drafter else None)
+            del qkv, gu
             keep.append(t)
             return B.LayerWeights(*[_ptr(t[k]) for k in
                                     ("attn_norm", "w_qkv", "w_o", "mlp_norm",
@@ -126,17 +141,17 @@ class Runtime:
                                              for i in range(s.n_layers)])
         embed = get("embed", (s.vocab, d))
         tfin = get("final_norm", (d,), "ones")
-        tlm = get("lm_head", (s.vocab, d))
+        tlm = pack(get("lm_head", (s.vocab, d)))
         dl = (B.LayerWeights * w.drafter_layers)(
             *[layer(f"d.layers.{i}.", True) for i in range(w.drafter_layers)])
-        dt = dict(w_cond=get("d.w_cond", (d, 3 * d)),
+        dt = dict(w_cond=pack(get("d.w_cond", (d, 3 * d))),
                   norm_c=get("d.norm_c", (d,), "ones"),
                   norm_e=get("d.norm_e", (d,), "ones"),
                   norm_q=get("d.norm_q", (d,), "ones"),
                   pos_query=get("d.pos_query", (w.K, d)),
-                  w_fuse=get("d.w_fuse", (d, 3 * d)),
+                  w_fuse=pack(get("d.w_fuse", (d, 3 * d))),
                   final_norm=get("d.final_norm", (d,), "ones"),
-                  lm_head=get("d.lm_head", (s.vocab, d)),
+                  lm_head=pack(get("d.lm_head", (s.vocab, d))),
                   rank_w=get("d.rank_w", (4, d + 15), fp32=True),
                   rank_b=get("d.rank_b", (4,), "zeros"))
         self._keep = (keep, embed, tfin, tlm, dt, tl, dl)

@@ -68,6 +68,10 @@ def cfg(**kw):
     (dict(max_pages=16385), B.SB_EINVAL),
     (dict(tap_layers=(C.c_int32 * 3)(0, 1, 2)), B.SB_ESHAPE),
     (dict(t_rope_theta=0.0), B.SB_EINVAL),
+    # bf16 projections: input widths % 128, output widths % 32
+    (dict(dtype=B.SB_BF16, t_d_ff=1056), B.SB_ESHAPE),
+    (dict(dtype=B.SB_BF16, t_d_model=288), B.SB_ESHAPE),
+    (dict(dtype=B.SB_BF16, t_vocab=1040), B.SB_ESHAPE),
 ])
 def test_create_rejects_bad_configs(lib, kw, code):
     c = cfg(**kw)
@@ -189,3 +193,29 @@ def test_verify_accept_commit_validation(bound):
     assert lib.sb_prefill(ctx, C.byref(seqs), f.at(), 400, lens, C.byref(tkv),
                           C.byref(dkv), None) == B.SB_EBUDGET
     assert lib.sb_set_length_bound(ctx, -1) == B.SB_EINVAL
+
+
+def test_create_accepts_bf16_shapes(lib):
+    c = cfg(dtype=B.SB_BF16)
+    ctx = C.c_void_p()
+    assert lib.sb_create(C.byref(c), C.byref(ctx)) == B.SB_OK
+    lib.sb_destroy(ctx)
+
+
+@pytest.mark.parametrize("args,code", [
+    # src, dst, rows, cols, dtype, gate_up (fake, never dereferenced: every
+    # case fails validation before anything is enqueued)
+    ((0x10000, 0x90000, 64, 128, 7, 0), B.SB_EDTYPE),
+    ((0x10000, 0x90000, 0, 128, B.SB_BF16, 0), B.SB_EINVAL),
+    ((0x10000, 0x90000, 64, -1, B.SB_BF16, 0), B.SB_EINVAL),
+    ((0, 0x90000, 64, 128, B.SB_BF16, 0), B.SB_EINVAL),
+    ((0x10008, 0x90000, 64, 128, B.SB_BF16, 0), B.SB_EINVAL),
+    ((0x10000, 0x12000, 64, 128, B.SB_BF16, 0), B.SB_EINVAL),   # overlap
+    ((0x10000, 0x90000, 48, 128, B.SB_BF16, 0), B.SB_ESHAPE),
+    ((0x10000, 0x90000, 64, 96, B.SB_BF16, 1), B.SB_ESHAPE),
+])
+def test_pack_weight_validation(lib, args, code):
+    src, dst, rows, cols, dtype, gate_up = args
+    assert lib.sb_pack_weight(C.c_void_p(src), C.c_void_p(dst), rows, cols,
+                              dtype, gate_up, None) == code
+    assert lib.sb_last_error(None)
