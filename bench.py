@@ -11,8 +11,9 @@ sb_accept and sb_commit, with inputs resident in HBM.
 Prints one JSON line: value = committed (accepted + bonus) tokens per second
 over the timed steps; block-expansion steps/s and tree-attention HBM GB/s
 from HIP events on the library's stream; the roofline of the dominant
-kernel (the weight-streaming projection GEMM); and the CPU oracle timed on a
-bounded sample of the same workload.
+kernel (the projection GEMMs: HBM-bound with few rows per call, MFMA-bound
+with many, decided by arithmetic intensity against the ridge point); and the
+CPU oracle timed on a bounded sample of the same workload.
 """
 import argparse
 import json
@@ -24,6 +25,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0   # dense bf16 MFMA, MI355X
 METRIC = ("block-expansion steps/s + tree-attn HBM GB/s; accepted tokens/s "
           "(8B-shape)")
 
@@ -32,20 +34,40 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def attn_bytes(w, T_avg, n_nodes, rows_block, es):
+def attn_bytes(w, T_total, n_nodes, rows_block, es):
     """Algorithmic bytes of the tree-attention launches of one iteration:
-    every prefix K/V entry and every segment entry read once per layer, Q
-    read and O written once per row."""
+    every committed prefix K/V entry of every sequence (T_total entries over
+    the batch) and every segment entry read once per layer, Q read and O
+    written once per row."""
     s = w.target
     kv_entry = 2 * s.n_kv_heads * s.head_dim * es
     q_row = s.n_heads * s.head_dim * es * 2
-    verify = s.n_layers * (T_avg * kv_entry + n_nodes * kv_entry
+    verify = s.n_layers * (T_total * kv_entry + n_nodes * kv_entry
                            + n_nodes * q_row)
     draft = 0.0
     for rows in rows_block:
-        draft += w.drafter_layers * (T_avg * kv_entry + rows * kv_entry
+        draft += w.drafter_layers * (T_total * kv_entry + rows * kv_entry
                                      + rows * q_row)
     return verify + draft
+
+
+def gemm_flops(w, verify_rows, rows_block, n_seqs):
+    """Algorithmic flops (2 per multiply-add) of the projection GEMMs over
+    the actual rows: verify rows through every target layer and the LM
+    head; each block's drafter rows through W_fuse, the drafter layers (with
+    the shift) and the LM head; block 1 also the condition projection."""
+    s = w.target
+    d, F = s.d_model, s.d_ff
+    layer = (s.n_heads + 2 * s.n_kv_heads) * s.head_dim * d \
+        + d * s.n_heads * s.head_dim + 2 * F * d + d * F
+    lm = s.vocab * d
+    fl = 2.0 * verify_rows * (s.n_layers * layer + lm)
+    for i, rows in enumerate(rows_block):
+        fl += 2.0 * rows * (3 * d * d + w.drafter_layers * (layer + 2 * d * d)
+                            + lm)
+        if i % w.M == 0:
+            fl += 2.0 * n_seqs * 3 * d * d
+    return fl
 
 
 def gemm_traffic(workload):
@@ -241,11 +263,13 @@ def main():
     # second pass over the same work with per-kernel HIP events
     Tp0 = rt.T.clone()
     rows_block = []
+    verify_rows = 0
     rt.profile(True)
     for i in range(args.steps):
         for m in range(1, w.M + 1):
             rt.expand(m)
             rows_block.append(int(rt.dout["n_call"][0]))
+        verify_rows += int(rt.tree["n_nodes"].sum())
         rt.verify()
         rt.accept()
         rt.commit()
@@ -253,16 +277,21 @@ def main():
     rt.profile(False)
     prof = rt.profile_read()
     Tp1 = rt.T.clone()
-    T_avg = float((Tp0.sum() + Tp1.sum()) / 2 / rt.S)
+    T_total = float((Tp0.sum() + Tp1.sum()) / 2)
     n_nodes = int(rt.tree["n_nodes"].sum())
     gemm = prof["gemm"]
     gemm_gbps = gemm["bytes"] / (gemm["ms"] * 1e-3) / 1e9
-    ab = sum(attn_bytes(w, T_avg, n_nodes, rows_block[i * w.M:(i + 1) * w.M],
+    flops = gemm_flops(w, verify_rows, rows_block, rt.S)
+    gemm_tflops = flops / (gemm["ms"] * 1e-3) / 1e12
+    # bound by arithmetic intensity against the ridge point of the chip
+    ridge = MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBPS * 1e9)
+    mfma_bound = flops / gemm["bytes"] > ridge
+    ab = sum(attn_bytes(w, T_total, n_nodes, rows_block[i * w.M:(i + 1) * w.M],
                         es) for i in range(args.steps))
     attn = prof["tree_attn"]
     attn_gbps = ab / (attn["ms"] * 1e-3) / 1e9
     log(f"gemm {gemm['launches']} launches {gemm['ms']:.2f} ms "
-        f"{gemm_gbps:.0f} GB/s; tree-attn {attn['launches']} launches "
+        f"{gemm_gbps:.0f} GB/s {gemm_tflops:.0f} TFLOP/s; tree-attn {attn['launches']} launches "
         f"{attn['ms']:.2f} ms {attn_gbps:.0f} GB/s; vocab "
         f"{prof['vocab']['ms']:.2f} ms")
 
@@ -304,13 +333,23 @@ def main():
         # with the paper's mean accepted length (Llama-3.1-8B, T = 0)
         "projected_tokens_per_s_at_paper_tau_4.41": round(
             args.steps * rt.S * 4.41 / dt, 1),
-        "roofline": {"kernel": "gemm_stream_kernel (all projection GEMMs)",
-                     "bound": "hbm", "achieved": round(gemm_gbps, 1),
-                     "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(gemm_gbps / HBM_PEAK_GBPS, 4),
+        "roofline": {"kernel": "gemm_tile_kernel (all projection GEMMs)",
+                     "bound": "mfma" if mfma_bound else "hbm",
+                     "achieved": round(gemm_tflops if mfma_bound
+                                       else gemm_gbps, 1),
+                     "peak": (MFMA_BF16_PEAK_TFLOPS if mfma_bound
+                              else HBM_PEAK_GBPS),
+                     "unit": "TFLOP/s" if mfma_bound else "GB/s",
+                     "frac": round(gemm_tflops / MFMA_BF16_PEAK_TFLOPS
+                                   if mfma_bound
+                                   else gemm_gbps / HBM_PEAK_GBPS, 4),
                      "traffic": traffic,
                      "algorithmic_bytes_per_launch": round(
                          gemm["bytes"] / max(gemm["launches"], 1)),
+                     "algorithmic_flops_per_launch": round(
+                         flops / max(gemm["launches"], 1)),
+                     "hbm_gbps": round(gemm_gbps, 1),
+                     "mfma_tflops": round(gemm_tflops, 1),
                      "launches_per_step": gemm["launches"] // args.steps,
                      "avg_launch_us": round(gemm["ms"] * 1e3 /
                                             max(gemm["launches"], 1), 2)},

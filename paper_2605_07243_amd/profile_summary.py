@@ -10,7 +10,9 @@ each step (``--step-marker``).  With a kernel trace, every kernel family gets
 its dispatches per step, total and mean duration, so the mean duration of a
 kernel can be compared with the HIP-event timing bench.py reports.  With a
 counter collection (``--pmc``), every family gets the mean value of each
-counter per dispatch; the calibration copy (bench.py --calib-mib, an
+counter per dispatch (and, given SQ_VALU_MFMA_BUSY_CYCLES and
+GRBM_GUI_ACTIVE, the fraction of SIMD cycles its MFMAs kept busy); the
+calibration copy (bench.py --calib-mib, an
 elementwise kernel that reads and writes B bytes) gives the factor by which
 the counter over- or under-states bytes moved.
 """
@@ -98,6 +100,17 @@ def main_pmc(a):
         table[name] = {"dispatches_per_step": n / k, **means}
         out.append(f"| `{name}` | {n / k:.1f} | " +
                    " | ".join(f"{means[c]:.0f}" for c in counters) + " |")
+    # MFMA utilisation: SQ_VALU_MFMA_BUSY_CYCLES is summed over every SIMD
+    # (256 CUs x 4), GRBM_GUI_ACTIVE over the 8 XCDs (each counts the
+    # dispatch's active cycles)
+    if "SQ_VALU_MFMA_BUSY_CYCLES" in counters and "GRBM_GUI_ACTIVE" in counters:
+        out += ["", "| kernel | MFMA busy (% of SIMD cycles) |", "|---|---:|"]
+        for name, row in table.items():
+            act = row["GRBM_GUI_ACTIVE"] / 8.0
+            if act > 0 and row["SQ_VALU_MFMA_BUSY_CYCLES"] > 0:
+                util = row["SQ_VALU_MFMA_BUSY_CYCLES"] / (act * 1024.0)
+                row["mfma_busy_frac"] = util
+                out.append(f"| `{name}` | {100 * util:.1f} |")
     print("\n".join(out))
     if a.json:
         with open(a.json, "w") as f:
