@@ -5,9 +5,10 @@
 // ancestors-or-self for verification, on-path rows of earlier blocks plus
 // its own block's rows <= k for the drafter, a causal chain for prefill).
 //
-// One wave owns 16 query vectors of one KV head (grouped-query attention:
-// the G = H / Hkv query heads of a row share the KV head, so the 16 vectors
-// are consecutive (row, head) pairs) and one split of the prefix.  Per tile
+// A q-tile is 16 query vectors of one KV head (grouped-query attention: the
+// G = H / Hkv query heads of a row share the KV head, so the 16 vectors are
+// consecutive (row, head) pairs); a wave owns one to four q-tiles and one
+// split of the prefix.  Per tile
 // of 32 keys it computes S^T = K Q^T with the keys as MFMA rows and the
 // queries as columns, which leaves each lane holding the 8 scores of one
 // query - exactly the B operand of O^T += V^T P^T - so the online softmax
@@ -42,13 +43,16 @@ __device__ __forceinline__ uint4 keep_slots(uint4 v, int first, int nvalid) {
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-// One workgroup = NQ waves = NQ q-tiles of 16 query vectors of one KV head,
-// one split of the prefix (the last split also takes the segment).  K and V
-// tiles of 32 keys are staged once per workgroup in LDS (double buffered;
-// global loads run four tiles ahead in registers) and read by every wave.
-// With several splits each workgroup writes (O, m, l) partials that
-// attn_merge combines; with one split the kernel writes the output.
-template <typename T, int HD, int NQ>
+// One workgroup = NQ waves x QT q-tiles of 16 query vectors of one KV head
+// (q-tile j of wave w is tile group * NQ * QT + j * NQ + w) and one split of
+// the prefix (the last split also takes the segment).  K and V tiles of 32
+// keys are staged once per workgroup in LDS (double buffered; global loads
+// run four tiles ahead in registers) and read by every wave; a wave reuses
+// every K and V operand it reads for its QT q-tiles, so a split's K/V is
+// read once for up to 16 NQ QT query vectors.  With several splits each
+// workgroup writes (O, m, l) partials that attn_merge combines; with one
+// split the kernel writes the output.
+template <typename T, int HD, int NQ, int QT>
 __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
     const T* __restrict__ q, CallPlan p, KVView kv, int H, int Hkv,
     int split_tokens, float scale, float* __restrict__ o_part,
@@ -62,6 +66,7 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
   constexpr int VCR = 16 * ES / 16;                 // chunks per V page row
   constexpr int NT = NQ * 64;
   constexpr int PER = (KCH + VCH + NT - 1) / NT;
+  constexpr int QPW = NQ * QT;                      // q-tiles per workgroup
   __shared__ __attribute__((aligned(16))) T ksh[2][32][LDK];
   __shared__ __attribute__((aligned(16))) T vsh[2][HD][LDV];
   const int s = blockIdx.y / Hkv, kh = blockIdx.y % Hkv;
@@ -69,27 +74,36 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
   const int row0 = p.seq_off[s];
   const int nq = (p.seq_off[s + 1] - row0) * G;
   const int qg = blockIdx.x;
-  if (qg * NQ * 16 >= nq) return;                   // uniform for the group
+  if (qg * QPW * 16 >= nq) return;                  // uniform for the group
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int r = lane & 15, g = lane >> 4;
-  const int qv = (qg * NQ + wave) * 16 + r;
-  const bool qvalid = qv < nq;
-  const bool wave_live = (qg * NQ + wave) * 16 < nq;
-  const int qrow = row0 + (qvalid ? qv / G : 0);
-  const int qh = kh * G + (qvalid ? qv % G : 0);
-
-  Frag8<T> qf[HD / 32];
+  bool qvalid[QT], live[QT];
+  int qrow[QT], qh[QT];
+  Frag8<T> qf[QT][HD / 32];
+  float m_run[QT], l_run[QT];
+  f32x4_t acc[QT][HD / 16];
 #pragma unroll
-  for (int c = 0; c < HD / 32; ++c) {
-    qf[c].load(q + ((size_t)qrow * H + qh) * HD + c * 32 + g * 8);
-    if (!qvalid) qf[c].zero();
+  for (int j = 0; j < QT; ++j) {
+    const int tile = qg * QPW + j * NQ + wave;
+    const int qv = tile * 16 + r;
+    qvalid[j] = qv < nq;
+    live[j] = tile * 16 < nq;
+    qrow[j] = row0 + (qvalid[j] ? qv / G : 0);
+    qh[j] = kh * G + (qvalid[j] ? qv % G : 0);
+#pragma unroll
+    for (int c = 0; c < HD / 32; ++c) {
+      qf[j][c].load(q + ((size_t)qrow[j] * H + qh[j]) * HD + c * 32 + g * 8);
+      if (!qvalid[j]) qf[j][c].zero();
+    }
+    m_run[j] = SB_NEG;
+    l_run[j] = 0.f;
+#pragma unroll
+    for (int c = 0; c < HD / 16; ++c) acc[j][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
-  float m_run = SB_NEG, l_run = 0.f;
-  f32x4_t acc[HD / 16];
+  bool wave_live = false;
 #pragma unroll
-  for (int c = 0; c < HD / 16; ++c) acc[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int j = 0; j < QT; ++j) wave_live |= live[j];
 
-  const size_t page_elems = (size_t)Hkv * 16 * HD;
   const T* kpool = static_cast<const T*>(kv.k);
   const T* vpool = static_cast<const T*>(kv.v);
   const T* skp = static_cast<const T*>(kv.seg_k);
@@ -102,16 +116,8 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
   const int L = last_split ? min(p.seg_len[s], kv.seg_pages * 16) : 0;
   const int n_pre = t1 > t0 ? (t1 - t0 + 31) / 32 : 0;
   const int n_tiles = n_pre + (L + 31) / 32;
-  // this lane's visibility words (segment tile j uses word j) and the
-  // split's page-table entries, read once so that no tile fetch waits on a
-  // dependent global load
-  uint32_t vw[SB_MAX_ANC_WORDS];
-  {
-    const uint32_t* vis = p.vis + (size_t)qrow * p.vis_words;
-#pragma unroll
-    for (int w = 0; w < SB_MAX_ANC_WORDS; ++w)
-      vw[w] = (qvalid && w < p.vis_words && L > 0) ? vis[w] : 0u;
-  }
+  // the split's page-table entries, read once so that no tile fetch waits
+  // on a dependent global load
   constexpr int MAXP = 512;
   __shared__ int pg_sh[MAXP];
   const int pg0 = t0 >> 4;
@@ -120,47 +126,49 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
     pg_sh[j] = min(max(ptab[pg0 + j], 0), kv.n_pages - 1);
   __syncthreads();
 
-  // page base (element offset) of half h of tile i, or -1 when empty
+  // page base (element offset) of half h of tile i, or -1 when empty.  The
+  // launch keeps a split within MAXP pages.
   auto page_base = [&](int i, int h) -> long long {
     if (i < n_pre) {
       const int k = t0 + i * 32 + h * 16;
       if (k >= t1) return -1;
-      const int j = (k >> 4) - pg0;
-      const int pg = j < MAXP ? pg_sh[j]
-                              : min(max(ptab[k >> 4], 0), kv.n_pages - 1);
+      const int pg = pg_sh[min((k >> 4) - pg0, MAXP - 1)];
       return ((long long)pg * Hkv + kh) * 16 * HD;
     }
     const int k = (i - n_pre) * 32 + h * 16;
     if (k >= L || (k >> 4) >= kv.seg_pages) return -1;
     return (((long long)s * kv.seg_pages + (k >> 4)) * Hkv + kh) * 16 * HD;
   };
-  // register ring of DEPTH tiles in flight; slot = tile index mod DEPTH
+  // register ring of DEPTH tiles in flight; slot = tile index mod DEPTH.
+  // Segment tiles also bring the visibility word of every q-tile's row
+  // (segment tile w is word w).  Loads go to clamped addresses and their
+  // values are used raw until the stash / compute of the tile (an empty
+  // half reads page 0: its keys are masked and its V slots zeroed there),
+  // so no load is consumed before its turn and the ring stays in flight.
   constexpr int DEPTH = 4;
   uint4 stg[DEPTH][PER];
-  auto fetch = [&](int i, uint4 (&dst)[PER]) {
+  uint32_t visr[DEPTH][QT];
+  auto fetch = [&](int i, uint4 (&dst)[PER], uint32_t (&vdst)[QT]) {
     const bool seg = i >= n_pre;
     const T* kp = seg ? skp : kpool;
     const T* vp = seg ? svp : vpool;
-    const long long b0 = page_base(i, 0), b1 = page_base(i, 1);
+    const long long b0 = max(page_base(i, 0), 0LL);
+    const long long b1 = max(page_base(i, 1), 0LL);
 #pragma unroll
     for (int e = 0; e < PER; ++e) {
       const int c = tid + e * NT;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (c < KCH) {
-        const int key = c / CPR, part = c % CPR;
-        const long long b = key < 16 ? b0 : b1;
-        if (b >= 0)
-          v = *reinterpret_cast<const uint4*>(kp + b + (key & 15) * HD + part * (16 / ES));
-      } else if (c < KCH + VCH) {
-        const int cc = c - KCH;
-        const int hd = cc / (2 * VCR), rem = cc % (2 * VCR);
-        const int h = rem / VCR, part = rem % VCR;
-        const long long b = h ? b1 : b0;
-        if (b >= 0)
-          v = *reinterpret_cast<const uint4*>(vp + b + hd * 16 + part * (16 / ES));
-      }
-      dst[e] = v;
+      const int ck = min(c, KCH - 1);
+      const int key = ck / CPR, kpart = ck % CPR;
+      const T* ka = kp + (key < 16 ? b0 : b1) + (key & 15) * HD + kpart * (16 / ES);
+      const int cv = min(max(c - KCH, 0), VCH - 1);
+      const int hd = cv / (2 * VCR), rem = cv % (2 * VCR);
+      const int h = rem / VCR, vpart = rem % VCR;
+      const T* va = vp + (h ? b1 : b0) + hd * 16 + vpart * (16 / ES);
+      dst[e] = *reinterpret_cast<const uint4*>(c < KCH ? ka : va);
     }
+    const int wc = min(max(i - n_pre, 0), p.vis_words - 1);
+#pragma unroll
+    for (int j = 0; j < QT; ++j) vdst[j] = p.vis[(size_t)qrow[j] * p.vis_words + wc];
   };
   // valid keys of tile i
   auto n_valid = [&](int i) -> int {
@@ -183,70 +191,68 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
       }
     }
   };
-  auto compute = [&](int i, int buf) {
-    uint32_t bits;
-    if (i < n_pre) {
-      const int nvalid = t1 - (t0 + i * 32);
-      bits = nvalid >= 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
-    } else {
-      const int k0 = (i - n_pre) * 32;
-      const int nvalid = L - k0;
-      bits = nvalid >= 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
-      uint32_t word = 0u;
-#pragma unroll
-      for (int w = 0; w < SB_MAX_ANC_WORDS; ++w)
-        if (w == (k0 >> 5)) word = vw[w];
-      bits &= word;
-    }
+  auto compute = [&](int i, int buf, const uint32_t (&vword)[QT]) {
     if (!wave_live) return;
-    // S^T = K Q^T for the two 16-key halves
-    f32x4_t sc4[2];
+    const bool seg = i >= n_pre;
+    const bool vis_ok = seg && i - n_pre < p.vis_words;
+    const int nvalid = n_valid(i);
+    const uint32_t valid = nvalid >= 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
+    // S^T = K Q^T for the two 16-key halves, every q-tile
+    f32x4_t sc4[QT][2];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      sc4[h] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < QT; ++j)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) sc4[j][h] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int c = 0; c < HD / 32; ++c) {
         Frag8<T> kf;
         kf.load(&ksh[buf][h * 16 + r][c * 32 + g * 8]);
-        sc4[h] = mma_16x16x32(kf, qf[c], sc4[h]);
+#pragma unroll
+        for (int j = 0; j < QT; ++j) sc4[j][h] = mma_16x16x32(kf, qf[j][c], sc4[j][h]);
       }
-    }
-    float sc[8];
-    float mx = SB_NEG;
+    Frag8<T> pf[QT];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int kk = 16 * (e >> 2) + 4 * g + (e & 3);
-      const bool v = (bits >> kk) & 1u;
-      sc[e] = v ? sc4[e >> 2][e & 3] * scale : SB_NEG;
-      mx = fmaxf(mx, sc[e]);
-    }
-    mx = max_x32(max_x16(mx));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = __expf(m_run - m_new);
-    float pv[8];
-    float ps = 0.f;
+    for (int j = 0; j < QT; ++j) {
+      const uint32_t bits =
+          seg ? ((vis_ok && qvalid[j]) ? (valid & vword[j]) : 0u) : valid;
+      float sc[8];
+      float mx = SB_NEG;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int kk = 16 * (e >> 2) + 4 * g + (e & 3);
-      pv[e] = ((bits >> kk) & 1u) ? __expf(sc[e] - m_new) : 0.f;
-      ps += pv[e];
-    }
-    ps = sum_x32(sum_x16(ps));
-    l_run = l_run * alpha + ps;
-    m_run = m_new;
+      for (int e = 0; e < 8; ++e) {
+        const int kk = 16 * (e >> 2) + 4 * g + (e & 3);
+        const bool v = (bits >> kk) & 1u;
+        sc[e] = v ? sc4[j][e >> 2][e & 3] * scale : SB_NEG;
+        mx = fmaxf(mx, sc[e]);
+      }
+      mx = max_x32(max_x16(mx));
+      const float m_new = fmaxf(m_run[j], mx);
+      const float alpha = __expf(m_run[j] - m_new);
+      float pv[8];
+      float ps = 0.f;
 #pragma unroll
-    for (int c = 0; c < HD / 16; ++c) acc[c] *= alpha;
-    Frag8<T> pf;
-    if constexpr (ES == 2) {
-      uint32_t w[4];
+      for (int e = 0; e < 8; ++e) {
+        const int kk = 16 * (e >> 2) + 4 * g + (e & 3);
+        pv[e] = ((bits >> kk) & 1u) ? __expf(sc[e] - m_new) : 0.f;
+        ps += pv[e];
+      }
+      ps = sum_x32(sum_x16(ps));
+      l_run[j] = l_run[j] * alpha + ps;
+      m_run[j] = m_new;
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        w[e] = (uint32_t)f32_to_bf16(pv[2 * e]) |
-               ((uint32_t)f32_to_bf16(pv[2 * e + 1]) << 16);
-      pf.v = make_uint4(w[0], w[1], w[2], w[3]);
-    } else {
-      pf.a = make_float4(pv[0], pv[1], pv[2], pv[3]);
-      pf.b = make_float4(pv[4], pv[5], pv[6], pv[7]);
+      for (int c = 0; c < HD / 16; ++c) acc[j][c] *= alpha;
+      if constexpr (ES == 2) {
+        uint32_t w[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          w[e] = (uint32_t)f32_to_bf16(pv[2 * e]) |
+                 ((uint32_t)f32_to_bf16(pv[2 * e + 1]) << 16);
+        pf[j].v = make_uint4(w[0], w[1], w[2], w[3]);
+      } else {
+        pf[j].a = make_float4(pv[0], pv[1], pv[2], pv[3]);
+        pf[j].b = make_float4(pv[4], pv[5], pv[6], pv[7]);
+      }
     }
 #pragma unroll
     for (int c = 0; c < HD / 16; ++c) {
@@ -260,53 +266,57 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
         vf.a = *reinterpret_cast<const float4*>(vr);
         vf.b = *reinterpret_cast<const float4*>(vr + 16);
       }
-      acc[c] = mma_16x16x32(vf, pf, acc[c]);
+#pragma unroll
+      for (int j = 0; j < QT; ++j) acc[j][c] = mma_16x16x32(vf, pf[j], acc[j][c]);
     }
   };
+  if (n_tiles > 0) {
 #pragma unroll
-  for (int d = 0; d < DEPTH; ++d)
-    if (d < n_tiles) fetch(d, stg[d]);
-  if (n_tiles > 0) stash(0, 0, stg[0]);
-  __syncthreads();
-  // tile i lives in slot i % DEPTH; after it is stashed, the slot is refilled
-  // with tile i + DEPTH
-  for (int i0 = 0; i0 < n_tiles; i0 += DEPTH) {
+    for (int d = 0; d < DEPTH; ++d) fetch(min(d, n_tiles - 1), stg[d], visr[d]);
+    stash(0, 0, stg[0]);
+    __syncthreads();
+    // tile i lives in slot i % DEPTH; after it is stashed the slot is
+    // refilled with tile i + DEPTH (the last tile again past the end); its
+    // visibility words are copied out before the refill
+    for (int i0 = 0; i0 < n_tiles; i0 += DEPTH) {
 #pragma unroll
-    for (int d = 0; d < DEPTH; ++d) {
-      const int i = i0 + d;
-      if (i < n_tiles) {
-        if (i + DEPTH < n_tiles) fetch(i + DEPTH, stg[d]);
-        compute(i, i & 1);
+      for (int d = 0; d < DEPTH; ++d) {
+        const int i = i0 + d;
+        uint32_t vword[QT];
+#pragma unroll
+        for (int j = 0; j < QT; ++j) vword[j] = visr[d][j];
+        fetch(min(i + DEPTH, n_tiles - 1), stg[d], visr[d]);
+        if (i < n_tiles) compute(i, i & 1, vword);
         if (i + 1 < n_tiles) stash(i + 1, (i + 1) & 1, stg[(d + 1) % DEPTH]);
         __syncthreads();
       }
     }
   }
-  (void)page_elems;
 
   const int n_split = gridDim.z;
-  if (n_split == 1) {
-    if (!qvalid) return;
-    const float il = l_run > 0.f ? 1.0f / l_run : 0.f;
-    T* o = out + (size_t)qrow * H * HD + (size_t)qh * HD;
-#pragma unroll
-    for (int c = 0; c < HD / 16; ++c)
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr)
-        o[16 * c + 4 * g + rr] = Elem<T>::from_f32(acc[c][rr] * il);
-    return;
-  }
   const size_t cap = p.cap;
-  if (qvalid) {
-    float* o = o_part + (((size_t)blockIdx.z * cap + qrow) * H + qh) * HD;
+#pragma unroll
+  for (int j = 0; j < QT; ++j) {
+    if (!qvalid[j]) continue;
+    if (n_split == 1) {
+      const float il = l_run[j] > 0.f ? 1.0f / l_run[j] : 0.f;
+      T* o = out + (size_t)qrow[j] * H * HD + (size_t)qh[j] * HD;
+#pragma unroll
+      for (int c = 0; c < HD / 16; ++c)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr)
+          o[16 * c + 4 * g + rr] = Elem<T>::from_f32(acc[j][c][rr] * il);
+      continue;
+    }
+    float* o = o_part + (((size_t)blockIdx.z * cap + qrow[j]) * H + qh[j]) * HD;
 #pragma unroll
     for (int c = 0; c < HD / 16; ++c)
       *reinterpret_cast<float4*>(o + 16 * c + 4 * g) =
-          make_float4(acc[c][0], acc[c][1], acc[c][2], acc[c][3]);
+          make_float4(acc[j][c][0], acc[j][c][1], acc[j][c][2], acc[j][c][3]);
     if (g == 0) {
-      float* mlp = ml + (((size_t)blockIdx.z * cap + qrow) * H + qh) * 2;
-      mlp[0] = m_run;
-      mlp[1] = l_run;
+      float* mlp = ml + (((size_t)blockIdx.z * cap + qrow[j]) * H + qh[j]) * 2;
+      mlp[0] = m_run[j];
+      mlp[1] = l_run[j];
     }
   }
 }
@@ -402,29 +412,53 @@ void launch_attn_merge(const CallPlan& p, int H, int hd, int n_split,
                        const float* o_part, const float* ml, T* out,
                        hipStream_t st);
 
+namespace {
+
+// q-tiles of 16 query vectors per workgroup: NQ waves x QT tiles each.  Two
+// q-tiles per wave (one read of a split's K/V for twice the queries) pay
+// off when there are enough (sequence, KV head) pairs to fill the chip
+// without cutting the prefix into short splits; with few pairs the
+// parallelism has to come from the splits, and one q-tile per wave keeps
+// each split's chain short (measured: 16 sequences x 8 KV heads gain 14%,
+// one sequence loses 8-15%).
+struct AttnShape {
+  int nq, qt, groups;
+};
+AttnShape attn_shape(int rows_per_seq_cap, int G, int seq_heads) {
+  const int qtiles = (rows_per_seq_cap * G + 15) / 16;
+  AttnShape a{};
+  a.nq = qtiles >= 8 ? 8 : (qtiles >= 4 ? 4 : (qtiles >= 2 ? 2 : 1));
+  a.qt = (qtiles > 8 && seq_heads >= 32) ? 2 : 1;  // 8 x 2 fits 256 VGPRs
+  a.groups = (qtiles + a.nq * a.qt - 1) / (a.nq * a.qt);
+  return a;
+}
+
+}  // namespace
+
 template <typename T>
 void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
                       int rows_per_seq_cap, int H, int Hkv, int hd,
                       int n_split, int max_prefix, float* o_part, float* ml,
                       T* out, hipStream_t st) {
-  const int G = H / Hkv;
-  const int qtiles = (rows_per_seq_cap * G + 15) / 16;
-  const int nq = qtiles >= 8 ? 8 : (qtiles >= 4 ? 4 : (qtiles >= 2 ? 2 : 1));
-  const int n_qgroups = (qtiles + nq - 1) / nq;
+  const AttnShape a = attn_shape(rows_per_seq_cap, H / Hkv, p.n_seqs * Hkv);
+  // the caller picks n_split so that a split spans at most 512 pages (the
+  // kernel's page-table stage): max_prefix <= 512 * 16 * n_split
   int split_tokens = (max_prefix + n_split - 1) / n_split;
   split_tokens = ((split_tokens + 31) / 32) * 32;
   if (split_tokens == 0) split_tokens = 32;
-  const dim3 grid(n_qgroups, p.n_seqs * Hkv, n_split);
+  const dim3 grid(a.groups, p.n_seqs * Hkv, n_split);
   const float scale = 1.0f / sqrtf((float)hd);
-#define SB_ATTN(HD_, NQ_)                                                      \
-  if (hd == HD_ && nq == NQ_) {                                               \
-    tree_attn_kernel<T, HD_, NQ_><<<grid, NQ_ * 64, 0, st>>>(                 \
+#define SB_ATTN(HD_, NQ_, QT_)                                                 \
+  if (hd == HD_ && a.nq == NQ_ && a.qt == QT_) {                              \
+    tree_attn_kernel<T, HD_, NQ_, QT_><<<grid, NQ_ * 64, 0, st>>>(            \
         q, p, kv, H, Hkv, split_tokens, scale, o_part, ml, out);              \
     if (n_split > 1) launch_attn_merge<T>(p, H, hd, n_split, o_part, ml, out, st); \
     return;                                                                   \
   }
-  SB_ATTN(128, 8) SB_ATTN(128, 4) SB_ATTN(128, 2) SB_ATTN(128, 1)
-  SB_ATTN(64, 8) SB_ATTN(64, 4) SB_ATTN(64, 2) SB_ATTN(64, 1)
+  SB_ATTN(128, 8, 2) SB_ATTN(128, 8, 1) SB_ATTN(128, 4, 1)
+  SB_ATTN(128, 2, 1) SB_ATTN(128, 1, 1)
+  SB_ATTN(64, 8, 2) SB_ATTN(64, 8, 1) SB_ATTN(64, 4, 1)
+  SB_ATTN(64, 2, 1) SB_ATTN(64, 1, 1)
 #undef SB_ATTN
 }
 
@@ -445,10 +479,8 @@ void launch_attn_merge(const CallPlan& p, int H, int hd, int n_split,
 #undef SB_MERGE
 }
 
-int attn_qgroups(int rows_per_seq_cap, int G) {
-  const int qtiles = (rows_per_seq_cap * G + 15) / 16;
-  const int nq = qtiles >= 8 ? 8 : (qtiles >= 4 ? 4 : (qtiles >= 2 ? 2 : 1));
-  return (qtiles + nq - 1) / nq;
+int attn_qgroups(int rows_per_seq_cap, int G, int seq_heads) {
+  return attn_shape(rows_per_seq_cap, G, seq_heads).groups;
 }
 
 template void launch_tree_attn<float>(const float*, const CallPlan&,
