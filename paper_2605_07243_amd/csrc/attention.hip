@@ -246,8 +246,7 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
         uint32_t w[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          w[e] = (uint32_t)f32_to_bf16(pv[2 * e]) |
-                 ((uint32_t)f32_to_bf16(pv[2 * e + 1]) << 16);
+          w[e] = pack_bf16x2(pv[2 * e], pv[2 * e + 1]);
         pf[j].v = make_uint4(w[0], w[1], w[2], w[3]);
       } else {
         pf[j].a = make_float4(pv[0], pv[1], pv[2], pv[3]);
@@ -368,8 +367,8 @@ __global__ __launch_bounds__(merge_threads<NS>()) void attn_merge_kernel_t(
     const size_t off = (size_t)i * H * hd + j;
     if (es == 2) {
       uint2 u;
-      u.x = (uint32_t)f32_to_bf16(v.x) | ((uint32_t)f32_to_bf16(v.y) << 16);
-      u.y = (uint32_t)f32_to_bf16(v.z) | ((uint32_t)f32_to_bf16(v.w) << 16);
+      u.x = pack_bf16x2(v.x, v.y);
+      u.y = pack_bf16x2(v.z, v.w);
       *reinterpret_cast<uint2*>(static_cast<bf16_t*>(out_v) + off) = u;
     } else {
       *reinterpret_cast<float4*>(static_cast<float*>(out_v) + off) = v;

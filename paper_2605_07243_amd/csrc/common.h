@@ -17,11 +17,18 @@ __device__ __forceinline__ float bf16_to_f32(bf16_t b) {
   return __uint_as_float(((uint32_t)b) << 16);
 }
 
-// float -> bfloat16, round to nearest, ties to even (finite inputs).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// float -> bfloat16, round to nearest, ties to even (v_cvt_pk_bf16_f32;
+// checked bit-exact against the integer rounding on finite inputs, ties
+// included).
 __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
+  return __builtin_bit_cast(bf16_t, (__bf16)f);
+}
+// Two values packed as (lo, hi) bf16 halves of one word.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 // Storage-type traits: elem is float (SB_F32) or bf16_t (SB_BF16).

@@ -108,8 +108,8 @@ __device__ __forceinline__ void store4<float>(float* p, float4 v) {
 template <>
 __device__ __forceinline__ void store4<bf16_t>(bf16_t* p, float4 v) {
   uint2 u;
-  u.x = (uint32_t)f32_to_bf16(v.x) | ((uint32_t)f32_to_bf16(v.y) << 16);
-  u.y = (uint32_t)f32_to_bf16(v.z) | ((uint32_t)f32_to_bf16(v.w) << 16);
+  u.x = pack_bf16x2(v.x, v.y);
+  u.y = pack_bf16x2(v.z, v.w);
   *reinterpret_cast<uint2*>(p) = u;
 }
 

@@ -572,7 +572,7 @@ void layer_body(sb_ctx* c, const sb_layer_weights& lw, int layer,
   const int groups = attn_qgroups(rows_per_seq, D.H / D.Hkv, p.n_seqs * D.Hkv) *
                      p.n_seqs * D.Hkv;
   // enough workgroups for the chip, splits of at least 128 keys (the
-  // kernel keeps four 32-key tiles in flight)
+  // kernel keeps four 32-key tiles in flight; shorter splits measured slower)
   int n_split = std::max(1, ceil_div(512, groups));
   n_split = std::min(n_split, std::max(1, max_prefix / 128));
   // a split spans at most 512 pages of 16 keys

@@ -209,8 +209,8 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(
           for (int e = 0; e < 4; ++e)
             o[e] = silu(acc[t][f][4 * q + e]) * acc[t][f][8 + 4 * q + e];
           uint2 pk;
-          pk.x = (uint32_t)f32_to_bf16(o[0]) | ((uint32_t)f32_to_bf16(o[1]) << 16);
-          pk.y = (uint32_t)f32_to_bf16(o[2]) | ((uint32_t)f32_to_bf16(o[3]) << 16);
+          pk.x = pack_bf16x2(o[0], o[1]);
+          pk.y = pack_bf16x2(o[2], o[3]);
           *reinterpret_cast<uint2*>(act + (size_t)m * F + j0 + 8 * q + 4 * h) = pk;
         }
       }
