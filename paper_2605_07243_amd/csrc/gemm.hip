@@ -112,12 +112,14 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[t][f][r] = 0.f;
 
-  // Stage s: weights in wq[s % PF], activations in LDS buffer s & 1.  In
-  // iteration s the activations of stage s + 2 are fetched into registers
-  // (slot s & 1) before the MFMAs and the weights of stage s + PF after
-  // them; the activations of stage s + 1 go to LDS at the end.  Stage
-  // indices past the chunk re-read its last stage (results unused) so that
-  // every iteration issues the same loads.
+  // Stage s: weights in wq[s % PF], activations in LDS buffer s & 1.
+  // Iteration s first writes the activations of stage s + 1 (fetched into
+  // registers one iteration earlier) to the other LDS buffer, fetches those
+  // of stage s + 2 into the freed register slot, and then runs the four
+  // MFMA sub-steps; after sub-step i the weight registers of that sub-step
+  // are refilled with stage s + PF.  The barrier at the end finds the LDS
+  // writes long done.  Stage indices past the chunk re-read its last stage
+  // (results unused) so that every iteration issues the same loads.
 #define SB_SCHED __builtin_amdgcn_sched_barrier(0);
 #define SB_ISSUE_W(p, s_)                                                     \
   {                                                                           \
@@ -125,6 +127,12 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(
     _Pragma("unroll") for (int f = 0; f < NF; ++f)                            \
     _Pragma("unroll") for (int i = 0; i < 4; ++i) wq[p][f][i] =               \
         *reinterpret_cast<const u32x4_t*>(wp[f] + so + 512 * i);              \
+  }
+#define SB_ISSUE_WI(p, s_, i)                                                 \
+  {                                                                           \
+    const size_t so = (size_t)min((s_), nstage - 1) * 2048;                   \
+    _Pragma("unroll") for (int f = 0; f < NF; ++f) wq[p][f][i] =              \
+        *reinterpret_cast<const u32x4_t*>(wp[f] + so + 512 * (i));            \
   }
 #define SB_ISSUE_X(slot, s_)                                                  \
   {                                                                           \
@@ -152,17 +160,20 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(
   {                                                                           \
     const int s = s0 + (p);                                                   \
     u32x4_t xa[MF], xb[MF];                                                   \
+    SB_STORE_X(((p) + 1) & 1, ((p) + 1) & 1)                                  \
     SB_READ_X(xa, (p) & 1, 0)                                                 \
     SB_ISSUE_X((p) & 1, s + 2)                                                \
     SB_READ_X(xb, (p) & 1, 1)                                                 \
     SB_SCHED SB_MMA(p, 0, xa) SB_SCHED                                        \
+    SB_ISSUE_WI(p, s + PF, 0)                                                 \
     SB_READ_X(xa, (p) & 1, 2)                                                 \
     SB_SCHED SB_MMA(p, 1, xb) SB_SCHED                                        \
+    SB_ISSUE_WI(p, s + PF, 1)                                                 \
     SB_READ_X(xb, (p) & 1, 3)                                                 \
     SB_SCHED SB_MMA(p, 2, xa) SB_SCHED                                        \
-    SB_MMA(p, 3, xb)                                                          \
-    SB_ISSUE_W(p, s + PF)                                                     \
-    SB_STORE_X(((p) + 1) & 1, ((p) + 1) & 1)                                  \
+    SB_ISSUE_WI(p, s + PF, 2)                                                 \
+    SB_SCHED SB_MMA(p, 3, xb) SB_SCHED                                        \
+    SB_ISSUE_WI(p, s + PF, 3)                                                 \
     __syncthreads();                                                          \
   }
   SB_ISSUE_X(0, 0)
@@ -189,6 +200,7 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(
 #undef SB_STORE_X
 #undef SB_ISSUE_X
 #undef SB_ISSUE_W
+#undef SB_ISSUE_WI
 #undef SB_SCHED
   if (!wave_on) return;
   if constexpr (SWIGLU) {
@@ -360,8 +372,10 @@ GemmPlan gemm_plan(int N, int K, int m_cap, int elem_bytes) {
       g.ks *= 2;
     return g;
   }
-  g.mf = m_cap <= 32 ? 1 : m_cap <= 64 ? 2 : m_cap < 512 ? 4 : 8;
-  g.nf = (g.mf == 8 || (g.mf == 4 && m_cap > 128)) && N % 64 == 0 ? 2 : 1;
+  // 128-row tiles with 64 weight rows per wave measured fastest from 129 to
+  // 1024 rows (256-row tiles need twice the accumulators for no gain)
+  g.mf = m_cap <= 32 ? 1 : m_cap <= 64 ? 2 : 4;
+  g.nf = g.mf == 4 && m_cap > 128 && N % 64 == 0 ? 2 : 1;
   g.pf = (g.mf == 4 && (K / 64) % 4 == 0) ? 4 : 2;
   const int n_mt = (m_cap + 32 * g.mf - 1) / (32 * g.mf);
   const int n_nt = (N + 128 * g.nf - 1) / (128 * g.nf);
@@ -398,8 +412,6 @@ void launch_tile(const GemmPlan& g, const bf16_t* X, int ldx, const bf16_t* W,
   SB_LAUNCH(4, 1, 4)
   SB_LAUNCH(4, 2, 2)
   SB_LAUNCH(4, 2, 4)
-  SB_LAUNCH(8, 1, 2)
-  SB_LAUNCH(8, 2, 2)
 #undef SB_LAUNCH
 }
 
