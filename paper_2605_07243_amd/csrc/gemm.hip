@@ -362,6 +362,16 @@ bool gemm_shape_ok(int N, int K, int elem_bytes) {
   return N % 32 == 0 && K % 128 == 0;
 }
 
+namespace {
+
+// fraction of the last round of workgroups that is busy
+double round_fill(int wgs) {
+  const int rounds = (wgs + kTargetWorkgroups - 1) / kTargetWorkgroups;
+  return (double)wgs / ((double)rounds * kTargetWorkgroups);
+}
+
+}  // namespace
+
 GemmPlan gemm_plan(int N, int K, int m_cap, int elem_bytes) {
   GemmPlan g{};
   if (elem_bytes == 4) {
@@ -372,12 +382,22 @@ GemmPlan gemm_plan(int N, int K, int m_cap, int elem_bytes) {
       g.ks *= 2;
     return g;
   }
-  // 128-row tiles with 64 weight rows per wave measured fastest from 129 to
-  // 1024 rows (256-row tiles need twice the accumulators for no gain)
+  // 128-row tiles above 64 rows (256-row tiles measured no faster at 1024
+  // rows); 64 weight rows per wave above 128 rows, 128 per wave when the
+  // weight tiles alone fill the chip at least as evenly (fewer activation
+  // LDS reads per MFMA: +13% on the 28672- and 128256-wide projections at
+  // 1024 rows).  Four weight stages in flight only for the 32-row-per-wave
+  // shapes (measured best there, no gain with more rows per wave).
   g.mf = m_cap <= 32 ? 1 : m_cap <= 64 ? 2 : 4;
-  g.nf = g.mf == 4 && m_cap > 128 && N % 64 == 0 ? 2 : 1;
-  g.pf = (g.mf == 4 && (K / 64) % 4 == 0) ? 4 : 2;
   const int n_mt = (m_cap + 32 * g.mf - 1) / (32 * g.mf);
+  g.nf = 1;
+  if (g.mf == 4 && m_cap > 128 && N % 64 == 0) {
+    g.nf = 2;
+    const int t2 = n_mt * ((N + 255) / 256), t4 = n_mt * ((N + 511) / 512);
+    if (N % 128 == 0 && t4 >= kTargetWorkgroups && round_fill(t4) >= round_fill(t2))
+      g.nf = 4;
+  }
+  g.pf = (g.mf == 4 && g.nf == 1 && (K / 64) % 4 == 0) ? 4 : 2;
   const int n_nt = (N + 128 * g.nf - 1) / (128 * g.nf);
   g.ks = pick_split(n_mt * n_nt, K, g.pf);
   return g;
@@ -411,7 +431,7 @@ void launch_tile(const GemmPlan& g, const bf16_t* X, int ldx, const bf16_t* W,
   SB_LAUNCH(4, 1, 2)
   SB_LAUNCH(4, 1, 4)
   SB_LAUNCH(4, 2, 2)
-  SB_LAUNCH(4, 2, 4)
+  SB_LAUNCH(4, 4, 2)
 #undef SB_LAUNCH
 }
 
