@@ -321,6 +321,315 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
 }
 
 
+// bf16 tree attention on 32x32x16 MFMAs.  A wave owns 32 query vectors of
+// one KV head (lane l: query l % 32; the two lane halves split the
+// contraction), a workgroup NW waves, one split of the prefix; keys come in
+// tiles of 64 (four 16-key pages).  Per tile a wave computes
+// S^T = K Q^T for two 32-key blocks (8 MFMAs each over head_dim 128), so a
+// lane holds 16 scores of its query per block and the softmax reductions
+// are in-lane plus one swap with lane l ^ 32.  The scores of key-block b,
+// converted to bf16, are directly the B operand of O^T += V^T P^T when V^T
+// is read from LDS with the same key permutation (keys 4h..4h+3 and
+// 8+4h..8+4h+3 of each 16-key step for lane half h), so P never leaves
+// registers.  K [64][HD] and V^T [HD][64] tiles are staged once per
+// workgroup in LDS (double buffered, padded rows: conflict-free 16-byte K
+// reads and 8-byte V^T reads), global loads run DEPTH tiles ahead.
+typedef float attn_f32x16_t __attribute__((ext_vector_type(16)));
+typedef unsigned int attn_u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ attn_f32x16_t mma32_attn(attn_u32x4_t a, attn_u32x4_t b,
+                                                   attn_f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+      __builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c, 0,
+      0, 0);
+}
+
+template <int HD, int NW>
+__global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
+    const bf16_t* __restrict__ q, CallPlan p, KVView kv, int H, int Hkv,
+    int split_tokens, float scale, float* __restrict__ o_part,
+    float* __restrict__ ml, bf16_t* __restrict__ out) {
+  constexpr int KT = 64;                    // keys per tile
+  constexpr int LDK = HD + 8;               // K row: 16 B mod 256 B
+  constexpr int LDV = KT + 4;               // V^T row: 136 B, 8-byte reads
+  constexpr int NT = NW * 64;
+  constexpr int KCH = KT * HD / 8;          // 16-byte chunks of a K tile
+  constexpr int CH = 2 * KCH;               // K + V chunks per tile
+  constexpr int PER = (CH + NT - 1) / NT;
+  constexpr int HB = HD / 32;               // head_dim blocks of 32
+  constexpr int QK = HD / 16;               // contraction steps of S^T
+  constexpr int DEPTH = NW >= 8 ? 2 : 3;     // staging registers: 16 PER each
+  __shared__ __attribute__((aligned(16))) bf16_t ksh[2][KT][LDK];
+  __shared__ __attribute__((aligned(16))) bf16_t vsh[2][HD][LDV];
+  constexpr int MAXP = 512;
+  __shared__ int pg_sh[MAXP];
+  const int s = blockIdx.y / Hkv, kh = blockIdx.y % Hkv;
+  const int G = H / Hkv;
+  const int row0 = p.seq_off[s];
+  const int nq = (p.seq_off[s + 1] - row0) * G;
+  const int qg = blockIdx.x;
+  if (qg * NW * 32 >= nq) return;           // uniform for the group
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int lq = lane & 31, h = lane >> 5;
+  const int qv = (qg * NW + wave) * 32 + lq;
+  const bool qvalid = qv < nq;
+  const bool wave_live = (qg * NW + wave) * 32 < nq;
+  const int qrow = row0 + (qvalid ? qv / G : 0);
+  const int qh = kh * G + (qvalid ? qv % G : 0);
+  attn_u32x4_t qf[QK];
+#pragma unroll
+  for (int j = 0; j < QK; ++j) {
+    qf[j] = *reinterpret_cast<const attn_u32x4_t*>(
+        q + ((size_t)qrow * H + qh) * HD + 16 * j + 8 * h);
+    if (!qvalid) qf[j] = attn_u32x4_t{0u, 0u, 0u, 0u};
+  }
+  float m_run = SB_NEG, l_run = 0.f;
+  attn_f32x16_t acc[HB];
+#pragma unroll
+  for (int b = 0; b < HB; ++b)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[b][r] = 0.f;
+
+  const bf16_t* kpool = static_cast<const bf16_t*>(kv.k);
+  const bf16_t* vpool = static_cast<const bf16_t*>(kv.v);
+  const bf16_t* skp = static_cast<const bf16_t*>(kv.seg_k);
+  const bf16_t* svp = static_cast<const bf16_t*>(kv.seg_v);
+  const int* ptab = kv.page_table + (size_t)s * kv.max_pages;
+  const int Tp = min(p.prefix_len[s], kv.max_pages * 16);
+  const int t0 = blockIdx.z * split_tokens;
+  const int t1 = min(Tp, t0 + split_tokens);
+  const bool last_split = blockIdx.z == gridDim.z - 1;
+  const int L = last_split ? min(p.seg_len[s], kv.seg_pages * 16) : 0;
+  const int n_pre = t1 > t0 ? (t1 - t0 + KT - 1) / KT : 0;
+  const int n_tiles = n_pre + (L + KT - 1) / KT;
+  const int pg0 = t0 >> 4;
+  const int n_pg = t1 > t0 ? ((t1 + 15) >> 4) - pg0 : 0;
+  for (int j = tid; j < n_pg && j < MAXP; j += NT)
+    pg_sh[j] = min(max(ptab[pg0 + j], 0), kv.n_pages - 1);
+  __syncthreads();
+
+  // element offset of page pp (0..3) of tile i in its pool, or -1 (empty;
+  // the launch keeps a split within MAXP pages)
+  auto page_base = [&](int i, int pp) -> long long {
+    if (i < n_pre) {
+      const int k = t0 + i * KT + pp * 16;
+      if (k >= t1) return -1;
+      const int pg = pg_sh[min((k >> 4) - pg0, MAXP - 1)];
+      return ((long long)pg * Hkv + kh) * 16 * HD;
+    }
+    const int k = (i - n_pre) * KT + pp * 16;
+    if (k >= L || (k >> 4) >= kv.seg_pages) return -1;
+    return (((long long)s * kv.seg_pages + (k >> 4)) * Hkv + kh) * 16 * HD;
+  };
+  // Chunk c of a tile (16 bytes): c < KCH is K of page c / KPC, key
+  // (c % KPC) / (HD / 8), elements 8 (c % (HD / 8)); c = KCH + c' is V^T of
+  // page c' / (2 HD), head_dim row (c' % (2 HD)) / 2, slots 8 (c' % 2).
+  // Every thread's chunks sit at the same page and offset in every tile.
+  constexpr int KPC = 16 * HD / 8;          // K chunks per page
+  static_assert(KCH % NT == 0, "a thread's chunks are all K or all V");
+  int c_pg[PER], c_off[PER], c_lds[PER];
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const int c = tid + e * NT;
+    if (e * NT < KCH) {
+      const int krem = c % KPC, key = 16 * (c / KPC) + krem / (HD / 8);
+      c_pg[e] = c / KPC;
+      c_off[e] = (krem / (HD / 8)) * HD + (krem % (HD / 8)) * 8;
+      c_lds[e] = key * LDK + (krem % (HD / 8)) * 8;
+    } else {
+      const int cv = min(c - KCH, KCH - 1);
+      const int vrem = cv % (2 * HD);
+      c_pg[e] = cv / (2 * HD);
+      c_off[e] = (vrem / 2) * 16 + (vrem % 2) * 8;
+      c_lds[e] = (vrem / 2) * LDV + 16 * (cv / (2 * HD)) + 8 * (vrem % 2);
+    }
+  }
+  attn_u32x4_t stg[DEPTH][PER];
+  uint32_t visr[DEPTH][2];
+  auto fetch = [&](int i, attn_u32x4_t (&dst)[PER], uint32_t (&vdst)[2]) {
+    const bool seg = i >= n_pre;
+    const bf16_t* kp = seg ? skp : kpool;
+    const bf16_t* vp = seg ? svp : vpool;
+    long long pb[4];
+#pragma unroll
+    for (int pp = 0; pp < 4; ++pp) pb[pp] = max(page_base(i, pp), 0LL);
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      const long long base = c_pg[e] == 0 ? pb[0] : c_pg[e] == 1 ? pb[1]
+                           : c_pg[e] == 2 ? pb[2] : pb[3];
+      const bf16_t* src = (e * NT < KCH ? kp : vp) + base + c_off[e];
+      dst[e] = *reinterpret_cast<const attn_u32x4_t*>(src);
+    }
+    const int w0 = min(max(2 * (i - n_pre), 0), p.vis_words - 1);
+    const int w1 = min(w0 + 1, p.vis_words - 1);
+    vdst[0] = p.vis[(size_t)qrow * p.vis_words + w0];
+    vdst[1] = p.vis[(size_t)qrow * p.vis_words + w1];
+  };
+  auto n_valid = [&](int i) -> int {
+    return i < n_pre ? min(KT, t1 - (t0 + i * KT)) : min(KT, L - (i - n_pre) * KT);
+  };
+  // V^T slots at or past the tile's valid keys are zeroed (never-written
+  // slots may hold anything; a zero probability would not cancel a NaN)
+  auto stash = [&](int i, int buf, const attn_u32x4_t (&src)[PER]) {
+    const int nv = n_valid(i);
+    bf16_t* kb = &ksh[buf][0][0];
+    bf16_t* vb = &vsh[buf][0][0];
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      if (e * NT < KCH) {
+        *reinterpret_cast<attn_u32x4_t*>(kb + c_lds[e]) = src[e];
+      } else if (tid + e * NT < CH) {
+        uint4 v = make_uint4(src[e][0], src[e][1], src[e][2], src[e][3]);
+        if (nv < KT) v = keep_slots<2>(v, c_lds[e] % LDV, nv);
+        *reinterpret_cast<uint2*>(vb + c_lds[e]) = make_uint2(v.x, v.y);
+        *reinterpret_cast<uint2*>(vb + c_lds[e] + 4) = make_uint2(v.z, v.w);
+      }
+    }
+  };
+  // Scores in log2 units (scale * log2 e folded in).  The reference max
+  // used for the exponentials moves only when a score exceeds it by more
+  // than 8 (then every probability is <= 2^8 and O, l are rescaled once);
+  // O / l is exact either way, and the (O, m, l) partials carry the
+  // reference.
+  const float sl2 = scale * 1.44269504088896341f;
+  constexpr float kMasked = -3.0e38f;
+  auto compute = [&](int i, int buf, const uint32_t (&vw)[2]) {
+    if (!wave_live) return;
+    const bool seg = i >= n_pre;
+    const int nv = n_valid(i);
+    const bool full = !seg && nv == KT;
+    const int w = i - n_pre;
+    attn_f32x16_t sc[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sc[b][r] = 0.f;
+#pragma unroll
+      for (int j = 0; j < QK; ++j) {
+        const attn_u32x4_t kf =
+            *reinterpret_cast<const attn_u32x4_t*>(&ksh[buf][32 * b + lq][16 * j + 8 * h]);
+        sc[b] = mma32_attn(kf, qf[j], sc[b]);
+      }
+    }
+    // lane register r of block b is key 32 b + 8 (r / 4) + 4 h + r % 4
+    float mx = SB_NEG;
+    if (full) {
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          sc[b][r] *= sl2;
+          mx = fmaxf(mx, sc[b][r]);
+        }
+    } else {
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const int nb = min(max(nv - 32 * b, 0), 32);
+        uint32_t m = nb >= 32 ? 0xFFFFFFFFu : ((1u << nb) - 1u);
+        if (seg) m &= (qvalid && 2 * w + b < p.vis_words) ? vw[b] : 0u;
+        m >>= 4 * h;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int k = 8 * (r >> 2) + (r & 3);
+          sc[b][r] = ((m >> k) & 1u) ? sc[b][r] * sl2 : kMasked;
+          mx = fmaxf(mx, sc[b][r]);
+        }
+      }
+    }
+    mx = max_x32(mx);
+    // move the reference (wave-uniform decision) only when needed
+    if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.0f) != 0) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int hb = 0; hb < HB; ++hb) acc[hb] *= alpha;
+      m_run = m_new;
+    }
+    float ps = 0.f;
+    attn_u32x4_t pf[2][2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      float pv[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        // masked scores sit far below any reference (which starts at
+        // -1e30): exp2 underflows to 0
+        pv[r] = __builtin_amdgcn_exp2f(sc[b][r] - m_run);
+        ps += pv[r];
+      }
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+        pf[b][u] = attn_u32x4_t{pack_bf16x2(pv[8 * u], pv[8 * u + 1]),
+                                pack_bf16x2(pv[8 * u + 2], pv[8 * u + 3]),
+                                pack_bf16x2(pv[8 * u + 4], pv[8 * u + 5]),
+                                pack_bf16x2(pv[8 * u + 6], pv[8 * u + 7])};
+    }
+    l_run += sum_x32(ps);
+    // O^T[hd][query] += V^T[hd][keys] P^T[keys][query], 16 keys per step
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int k0 = 32 * b + 16 * u + 4 * h;
+#pragma unroll
+        for (int hb = 0; hb < HB; ++hb) {
+          const bf16_t* vr = &vsh[buf][32 * hb + lq][k0];
+          const uint2 lo = *reinterpret_cast<const uint2*>(vr);
+          const uint2 hi = *reinterpret_cast<const uint2*>(vr + 8);
+          acc[hb] = mma32_attn(attn_u32x4_t{lo.x, lo.y, hi.x, hi.y}, pf[b][u], acc[hb]);
+        }
+      }
+  };
+  if (n_tiles > 0) {
+#pragma unroll
+    for (int d = 0; d < DEPTH; ++d) fetch(min(d, n_tiles - 1), stg[d], visr[d]);
+    stash(0, 0, stg[0]);
+    __syncthreads();
+    for (int i0 = 0; i0 < n_tiles; i0 += DEPTH) {
+#pragma unroll
+      for (int d = 0; d < DEPTH; ++d) {
+        const int i = i0 + d;
+        uint32_t vw[2] = {visr[d][0], visr[d][1]};
+        fetch(min(i + DEPTH, n_tiles - 1), stg[d], visr[d]);
+        if (i < n_tiles) compute(i, i & 1, vw);
+        if (i + 1 < n_tiles) stash(i + 1, (i + 1) & 1, stg[(d + 1) % DEPTH]);
+        __syncthreads();
+      }
+    }
+  }
+  if (!qvalid) return;
+  // lane register r of head_dim block hb is element 32 hb + 8 (r / 4) +
+  // 4 h + r % 4 of this lane's query
+  const int n_split = gridDim.z;
+  if (n_split == 1) {
+    const float il = l_run > 0.f ? 1.0f / l_run : 0.f;
+    bf16_t* o = out + ((size_t)qrow * H + qh) * HD;
+#pragma unroll
+    for (int hb = 0; hb < HB; ++hb)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4)
+        *reinterpret_cast<uint2*>(o + 32 * hb + 8 * g4 + 4 * h) =
+            make_uint2(pack_bf16x2(acc[hb][4 * g4] * il, acc[hb][4 * g4 + 1] * il),
+                       pack_bf16x2(acc[hb][4 * g4 + 2] * il, acc[hb][4 * g4 + 3] * il));
+    return;
+  }
+  float* o = o_part + (((size_t)blockIdx.z * p.cap + qrow) * H + qh) * HD;
+#pragma unroll
+  for (int hb = 0; hb < HB; ++hb)
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4)
+      *reinterpret_cast<float4*>(o + 32 * hb + 8 * g4 + 4 * h) =
+          make_float4(acc[hb][4 * g4], acc[hb][4 * g4 + 1], acc[hb][4 * g4 + 2],
+                      acc[hb][4 * g4 + 3]);
+  if (h == 0) {
+    float* mlp = ml + (((size_t)blockIdx.z * p.cap + qrow) * H + qh) * 2;
+    mlp[0] = m_run * 0.69314718055994531f;   // natural-log units
+    mlp[1] = l_run;
+  }
+}
+
+
 // Combine the splits of every (row, head): out = sum_z w_z O_z / sum_z w_z l_z
 // with w_z = exp(m_z - max m).  A separate launch: the kernel boundary
 // orders the partial writes of every XCD before the reads.  One workgroup
@@ -423,9 +732,18 @@ namespace {
 struct AttnShape {
   int nq, qt, groups;
 };
-AttnShape attn_shape(int rows_per_seq_cap, int G, int seq_heads) {
-  const int qtiles = (rows_per_seq_cap * G + 15) / 16;
+AttnShape attn_shape(int rows_per_seq_cap, int G, int seq_heads, int es) {
   AttnShape a{};
+  if (es == 2) {
+    // bf16: waves of 32 query vectors, 4 or 8 per workgroup (at least four
+    // waves share the tile loads; waves past the queries only load)
+    const int qblocks = (rows_per_seq_cap * G + 31) / 32;
+    a.nq = qblocks > 4 ? 8 : 4;
+    a.qt = 1;
+    a.groups = (qblocks + a.nq - 1) / a.nq;
+    return a;
+  }
+  const int qtiles = (rows_per_seq_cap * G + 15) / 16;
   a.nq = qtiles >= 8 ? 8 : (qtiles >= 4 ? 4 : (qtiles >= 2 ? 2 : 1));
   a.qt = (qtiles > 8 && seq_heads >= 32) ? 2 : 1;  // 8 x 2 fits 256 VGPRs
   a.groups = (qtiles + a.nq * a.qt - 1) / (a.nq * a.qt);
@@ -439,14 +757,26 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
                       int rows_per_seq_cap, int H, int Hkv, int hd,
                       int n_split, int max_prefix, float* o_part, float* ml,
                       T* out, hipStream_t st) {
-  const AttnShape a = attn_shape(rows_per_seq_cap, H / Hkv, p.n_seqs * Hkv);
+  const AttnShape a =
+      attn_shape(rows_per_seq_cap, H / Hkv, p.n_seqs * Hkv, (int)sizeof(T));
   // the caller picks n_split so that a split spans at most 512 pages (the
   // kernel's page-table stage): max_prefix <= 512 * 16 * n_split
   int split_tokens = (max_prefix + n_split - 1) / n_split;
-  split_tokens = ((split_tokens + 31) / 32) * 32;
-  if (split_tokens == 0) split_tokens = 32;
+  split_tokens = ((split_tokens + 63) / 64) * 64;
+  if (split_tokens == 0) split_tokens = 64;
   const dim3 grid(a.groups, p.n_seqs * Hkv, n_split);
   const float scale = 1.0f / sqrtf((float)hd);
+  if constexpr (sizeof(T) == 2) {
+#define SB_ATTN32(HD_, NW_)                                                    \
+  if (hd == HD_ && a.nq == NW_) {                                             \
+    tree_attn32_kernel<HD_, NW_><<<grid, NW_ * 64, 0, st>>>(                  \
+        q, p, kv, H, Hkv, split_tokens, scale, o_part, ml, out);              \
+    if (n_split > 1) launch_attn_merge<T>(p, H, hd, n_split, o_part, ml, out, st); \
+    return;                                                                   \
+  }
+    SB_ATTN32(128, 8) SB_ATTN32(128, 4) SB_ATTN32(64, 8) SB_ATTN32(64, 4)
+#undef SB_ATTN32
+  } else {
 #define SB_ATTN(HD_, NQ_, QT_)                                                 \
   if (hd == HD_ && a.nq == NQ_ && a.qt == QT_) {                              \
     tree_attn_kernel<T, HD_, NQ_, QT_><<<grid, NQ_ * 64, 0, st>>>(            \
@@ -454,11 +784,12 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
     if (n_split > 1) launch_attn_merge<T>(p, H, hd, n_split, o_part, ml, out, st); \
     return;                                                                   \
   }
-  SB_ATTN(128, 8, 2) SB_ATTN(128, 8, 1) SB_ATTN(128, 4, 1)
-  SB_ATTN(128, 2, 1) SB_ATTN(128, 1, 1)
-  SB_ATTN(64, 8, 2) SB_ATTN(64, 8, 1) SB_ATTN(64, 4, 1)
-  SB_ATTN(64, 2, 1) SB_ATTN(64, 1, 1)
+    SB_ATTN(128, 8, 2) SB_ATTN(128, 8, 1) SB_ATTN(128, 4, 1)
+    SB_ATTN(128, 2, 1) SB_ATTN(128, 1, 1)
+    SB_ATTN(64, 8, 2) SB_ATTN(64, 8, 1) SB_ATTN(64, 4, 1)
+    SB_ATTN(64, 2, 1) SB_ATTN(64, 1, 1)
 #undef SB_ATTN
+  }
 }
 
 template <typename T>
@@ -478,8 +809,8 @@ void launch_attn_merge(const CallPlan& p, int H, int hd, int n_split,
 #undef SB_MERGE
 }
 
-int attn_qgroups(int rows_per_seq_cap, int G, int seq_heads) {
-  return attn_shape(rows_per_seq_cap, G, seq_heads).groups;
+int attn_qgroups(int rows_per_seq_cap, int G, int seq_heads, int es) {
+  return attn_shape(rows_per_seq_cap, G, seq_heads, es).groups;
 }
 
 template void launch_tree_attn<float>(const float*, const CallPlan&,

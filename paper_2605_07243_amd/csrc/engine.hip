@@ -569,8 +569,9 @@ void layer_body(sb_ctx* c, const sb_layer_weights& lw, int layer,
   const int cap_tokens = c->cfg.max_pages * 16;
   const int max_prefix = c->T_bound > 0 ? std::min(c->T_bound, cap_tokens)
                                         : cap_tokens;
-  const int groups = attn_qgroups(rows_per_seq, D.H / D.Hkv, p.n_seqs * D.Hkv) *
-                     p.n_seqs * D.Hkv;
+  const int groups =
+      attn_qgroups(rows_per_seq, D.H / D.Hkv, p.n_seqs * D.Hkv, D.es) *
+      p.n_seqs * D.Hkv;
   // enough workgroups for the chip, splits of at least 128 keys (the
   // kernel keeps four 32-key tiles in flight; shorter splits measured slower)
   int n_split = std::max(1, ceil_div(512, groups));

@@ -119,9 +119,9 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
                       int rows_per_seq_cap, int H, int Hkv, int hd,
                       int n_split, int max_prefix, float* o_part, float* ml,
                       T* out, hipStream_t st);
-// Query-tile groups per (sequence, KV head) of a launch (seq_heads = the
-// launch's sequences x KV heads).
-int attn_qgroups(int rows_per_seq_cap, int G, int seq_heads);
+// Query groups (workgroups) per (sequence, KV head) of a launch (seq_heads
+// = the launch's sequences x KV heads, es = element bytes).
+int attn_qgroups(int rows_per_seq_cap, int G, int seq_heads, int es);
 
 // Vocabulary reductions over fp32 logits [cap][V].
 void launch_vocab_partial(const float* logits, const int* n, int cap, int V,
