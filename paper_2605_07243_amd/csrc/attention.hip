@@ -736,9 +736,11 @@ AttnShape attn_shape(int rows_per_seq_cap, int G, int seq_heads, int es) {
   AttnShape a{};
   if (es == 2) {
     // bf16: waves of 32 query vectors, 4 or 8 per workgroup (at least four
-    // waves share the tile loads; waves past the queries only load)
+    // waves share the tile loads; waves past the queries only load).  Eight
+    // when enough (sequence, KV head) pairs fill the chip, else four: more
+    // workgroups for the latency-bound few-sequence case.
     const int qblocks = (rows_per_seq_cap * G + 31) / 32;
-    a.nq = qblocks > 4 ? 8 : 4;
+    a.nq = (qblocks > 4 && seq_heads >= 32) ? 8 : 4;
     a.qt = 1;
     a.groups = (qblocks + a.nq - 1) / a.nq;
     return a;
