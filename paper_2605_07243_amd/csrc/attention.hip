@@ -730,22 +730,27 @@ namespace {
 // each split's chain short (measured: 16 sequences x 8 KV heads gain 14%,
 // one sequence loses 8-15%).
 struct AttnShape {
+  bool mfma32;   // bf16 32x32x16 kernel (else 16-row q-tiles)
   int nq, qt, groups;
 };
 AttnShape attn_shape(int rows_per_seq_cap, int G, int seq_heads, int es) {
   AttnShape a{};
-  if (es == 2) {
-    // bf16: waves of 32 query vectors, 4 or 8 per workgroup (at least four
-    // waves share the tile loads; waves past the queries only load).  Eight
-    // when enough (sequence, KV head) pairs fill the chip, else four: more
-    // workgroups for the latency-bound few-sequence case.
+  if (es == 2 && seq_heads >= 32) {
+    // many (sequence, KV head) pairs: the 32x32x16 kernel, waves of 32
+    // query vectors, 4 or 8 per workgroup (at least four waves share the
+    // tile loads; waves past the queries only load).  With few pairs the
+    // parallelism has to come from the splits and the 16-row q-tiles of
+    // the other kernel keep each split's chain shorter (measured faster for
+    // one sequence).
     const int qblocks = (rows_per_seq_cap * G + 31) / 32;
-    a.nq = (qblocks > 4 && seq_heads >= 32) ? 8 : 4;
+    a.mfma32 = true;
+    a.nq = qblocks > 4 ? 8 : 4;
     a.qt = 1;
     a.groups = (qblocks + a.nq - 1) / a.nq;
     return a;
   }
   const int qtiles = (rows_per_seq_cap * G + 15) / 16;
+  a.mfma32 = false;
   a.nq = qtiles >= 8 ? 8 : (qtiles >= 4 ? 4 : (qtiles >= 2 ? 2 : 1));
   a.qt = (qtiles > 8 && seq_heads >= 32) ? 2 : 1;  // 8 x 2 fits 256 VGPRs
   a.groups = (qtiles + a.nq * a.qt - 1) / (a.nq * a.qt);
@@ -769,6 +774,7 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
   const dim3 grid(a.groups, p.n_seqs * Hkv, n_split);
   const float scale = 1.0f / sqrtf((float)hd);
   if constexpr (sizeof(T) == 2) {
+    if (a.mfma32) {
 #define SB_ATTN32(HD_, NW_)                                                    \
   if (hd == HD_ && a.nq == NW_) {                                             \
     tree_attn32_kernel<HD_, NW_><<<grid, NW_ * 64, 0, st>>>(                  \
@@ -778,7 +784,9 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
   }
     SB_ATTN32(128, 8) SB_ATTN32(128, 4) SB_ATTN32(64, 8) SB_ATTN32(64, 4)
 #undef SB_ATTN32
-  } else {
+    }
+  }
+  {
 #define SB_ATTN(HD_, NQ_, QT_)                                                 \
   if (hd == HD_ && a.nq == NQ_ && a.qt == QT_) {                              \
     tree_attn_kernel<T, HD_, NQ_, QT_><<<grid, NQ_ * 64, 0, st>>>(            \
