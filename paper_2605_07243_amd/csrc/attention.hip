@@ -118,7 +118,7 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
   const int n_tiles = n_pre + (L + 31) / 32;
   // the split's page-table entries, read once so that no tile fetch waits
   // on a dependent global load
-  constexpr int MAXP = 512;
+  constexpr int MAXP = 1024;
   __shared__ int pg_sh[MAXP];
   const int pg0 = t0 >> 4;
   const int n_pg = t1 > t0 ? ((t1 + 15) >> 4) - pg0 : 0;
@@ -361,7 +361,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
   constexpr int DEPTH = NW >= 8 ? 2 : 3;     // staging registers: 16 PER each
   __shared__ __attribute__((aligned(16))) bf16_t ksh[2][KT][LDK];
   __shared__ __attribute__((aligned(16))) bf16_t vsh[2][HD][LDV];
-  constexpr int MAXP = 512;
+  constexpr int MAXP = 1024;
   __shared__ int pg_sh[MAXP];
   const int s = blockIdx.y / Hkv, kh = blockIdx.y % Hkv;
   const int G = H / Hkv;
@@ -766,8 +766,8 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
                       T* out, hipStream_t st) {
   const AttnShape a =
       attn_shape(rows_per_seq_cap, H / Hkv, p.n_seqs * Hkv, (int)sizeof(T));
-  // the caller picks n_split so that a split spans at most 512 pages (the
-  // kernel's page-table stage): max_prefix <= 512 * 16 * n_split
+  // the caller picks n_split so that a split spans at most 1024 pages (the
+  // kernels' page-table stage): max_prefix <= 1024 * 16 * n_split
   int split_tokens = (max_prefix + n_split - 1) / n_split;
   split_tokens = ((split_tokens + 63) / 64) * 64;
   if (split_tokens == 0) split_tokens = 64;

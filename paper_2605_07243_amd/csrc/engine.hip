@@ -576,8 +576,8 @@ void layer_body(sb_ctx* c, const sb_layer_weights& lw, int layer,
   // kernel keeps four 32-key tiles in flight; shorter splits measured slower)
   int n_split = std::max(1, ceil_div(512, groups));
   n_split = std::min(n_split, std::max(1, max_prefix / 128));
-  // a split spans at most 512 pages of 16 keys
-  n_split = std::max(n_split, ceil_div(max_prefix, 512 * 16));
+  // a split spans at most 1024 pages of 16 keys
+  n_split = std::max(n_split, ceil_div(max_prefix, 1024 * 16));
   n_split = std::min(n_split, D.n_split);
   {
     ProfScope ps(c, st, SB_PROF_ATTN);
