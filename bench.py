@@ -26,6 +26,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0   # dense bf16 MFMA, MI355X
+BUCKET_SEED = 11
 METRIC = ("block-expansion steps/s + tree-attn HBM GB/s; accepted tokens/s "
           "(8B-shape)")
 
@@ -86,14 +87,15 @@ def gemm_traffic(workload):
     return d["bytes_per_dispatch"]
 
 
-def cpu_baseline(w, T, budget_s=10.0):
+def cpu_baseline(w, T, budget_s=10.0, paper_buckets=False):
     """Time the CPU oracle on a bounded sample of the workload: whole
     iterations of the real shapes (M block expansions of the drafter over a
     prefix of T entries, then the verify forward of the drafted tree through
     n_layers decoder layers and the LM head), repeated until budget_s of CPU
     time has passed.  To bound memory, the verify layers all use the weights
     and prefix cache of one generated layer: the arithmetic per layer is that
-    of a real layer."""
+    of a real layer.  paper_buckets: force the drafter rows' buckets from
+    the seeded paper-frequency draws, as the GPU run does."""
     import dataclasses
 
     import numpy as np
@@ -124,7 +126,9 @@ def cpu_baseline(w, T, budget_s=10.0):
     k, v = synth.random_kv(1, "bench.d", T, s, w1.dtype)
     st.dkv.k[0], st.dkv.v[0] = k.astype(np.float64), v.astype(np.float64)
 
-    def iteration():
+    def iteration(i):
+        forced = (synth.paper_buckets(BUCKET_SEED, i, 1, w1.rows_per_seq)[0]
+                  if paper_buckets else None)
         tree = specdec.DraftTree(st.root, w1.budget)
         rows = []
         seg = dr.new_segment(w1.rows_per_seq)
@@ -135,7 +139,7 @@ def cpu_baseline(w, T, budget_s=10.0):
             if not starts:
                 break
             rec = specdec.expand_block(dr, st, tree, rows, seg, starts, w1.K,
-                                       m, w1.branch_map)
+                                       m, w1.branch_map, forced)
             if m < w1.M:
                 picks = specdec.select_starts(tree, rows, rec["alive"],
                                               rec["chain"], rec["first_new"],
@@ -159,7 +163,7 @@ def cpu_baseline(w, T, budget_s=10.0):
     t_start = time.perf_counter()
     iters, t_draft, rows, n = 0, 0.0, 0, 0
     while True:
-        td, rows, n = iteration()
+        td, rows, n = iteration(iters)
         t_draft += td
         iters += 1
         elapsed = time.perf_counter() - t_start
@@ -186,10 +190,17 @@ def cpu_baseline(w, T, budget_s=10.0):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama3-8b-k4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--buckets", choices=("natural", "paper"),
+                    default="natural",
+                    help="natural: the rank head's argmax decides each "
+                         "drafter row's bucket; paper: buckets are forced "
+                         "from seeded draws with the class frequencies of "
+                         "a trained drafter (b0..b3 = 75.2/15.0/4.1/5.7%%), "
+                         "which shapes the trees like the paper's")
     ap.add_argument("--calib-mib", type=int, default=0,
                     help="before warmup, run a plain elementwise copy "
                          "(torch.neg) of this many MiB three times, to "
@@ -220,6 +231,22 @@ def main():
     torch.cuda.synchronize()
     log(f"prefill {sum(len(p) for p in prompts)} tokens in "
         f"{time.perf_counter() - t:.2f}s")
+    # forced buckets: one [n_seqs][row_cap] draw per iteration (warmup, timed
+    # pass, profiled pass), resident on the device before timing
+    sched = None
+    if args.buckets == "paper":
+        import numpy as np
+        n_iter = args.warmup + 2 * args.steps
+        sched = torch.as_tensor(np.stack(
+            [synth.paper_buckets(BUCKET_SEED, i, rt.S, rt.row_cap)
+             for i in range(n_iter)])).to(rt.dev)
+    it = [0]
+
+    def next_iteration():
+        if sched is not None:
+            rt.set_buckets(sched[it[0]])
+        it[0] += 1
+
     if args.calib_mib:
         src = torch.ones(args.calib_mib << 18, device=rt.dev)
         dst = torch.empty_like(src)
@@ -228,6 +255,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     for i in range(args.warmup):
+        next_iteration()
         rt.iteration()
     torch.cuda.synchronize()
     log("warmup done")
@@ -240,6 +268,7 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
+        next_iteration()
         ev[i][0].record(stream)
         for m in range(1, w.M + 1):
             rt.expand(m)
@@ -255,6 +284,16 @@ def main():
     later_ms = sum(e[1].elapsed_time(e[w.M]) for e in ev)
     draft_ms = block1_ms + later_ms
     rest_ms = sum(e[w.M].elapsed_time(e[w.M + 1]) for e in ev)
+
+    def median(xs):
+        xs = sorted(xs)
+        h = len(xs) // 2
+        return xs[h] if len(xs) % 2 else 0.5 * (xs[h - 1] + xs[h])
+
+    med_step = median([e[0].elapsed_time(e[w.M + 1]) for e in ev])
+    med_block1 = median([e[0].elapsed_time(e[1]) for e in ev])
+    med_later = (median([e[1].elapsed_time(e[w.M]) / (w.M - 1) for e in ev])
+                 if w.M > 1 else None)
     log(f"timed {args.steps} steps in {dt:.3f}s: {committed} tokens, "
         f"draft {draft_ms / args.steps:.3f} ms/step (block 1 "
         f"{block1_ms / args.steps:.3f}), verify+accept+commit "
@@ -266,6 +305,7 @@ def main():
     verify_rows = 0
     rt.profile(True)
     for i in range(args.steps):
+        next_iteration()
         for m in range(1, w.M + 1):
             rt.expand(m)
             rows_block.append(int(rt.dout["n_call"][0]))
@@ -318,13 +358,22 @@ def main():
                    "n_seqs": w.n_seqs, "prompt_len": list(w.prompt_len),
                    "K": w.K, "M": w.M, "B_max": w.B_max,
                    "budget": w.budget, "branch_map": list(w.branch_map),
-                   "buckets": "natural (random rank head)"},
+                   "buckets": ("natural (random rank head)"
+                               if sched is None else
+                               "paper-frequency (forced, seeded draws "
+                               "75.2/15.0/4.1/5.7%)")},
         "block_expansion_steps_per_s": round(w.M * args.steps /
                                              (draft_ms * 1e-3), 2),
         "block1_steps_per_s": round(args.steps / (block1_ms * 1e-3), 2),
         "later_block_steps_per_s": (round((w.M - 1) * args.steps /
                                           (later_ms * 1e-3), 2)
                                     if w.M > 1 else None),
+        "median_ms_per_step": round(med_step, 4),
+        "median_block1_ms": round(med_block1, 4),
+        "median_later_block_ms": (round(med_later, 4) if med_later is not None
+                                  else None),
+        "verify_nodes_per_step": round(verify_rows / args.steps, 2),
+        "drafter_rows_per_step": round(sum(rows_block) / args.steps, 2),
         "tree_attn_gbps": round(attn_gbps, 1),
         "tree_attn_frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
         "accepted_tokens_per_s": round(committed / dt, 3),
@@ -357,7 +406,8 @@ def main():
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
         try:
-            out["cpu_baseline"] = cpu_baseline(w, max(w.prompt_len))
+            out["cpu_baseline"] = cpu_baseline(
+                w, max(w.prompt_len), paper_buckets=sched is not None)
         except MemoryError as e:
             out["cpu_baseline"] = {"error": f"oracle sample did not fit: {e}"}
     print(json.dumps(out), flush=True)

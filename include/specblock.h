@@ -304,6 +304,18 @@ int sb_commit(sb_ctx* ctx, sb_seqs* seqs, const sb_tree* tree,
  * true T makes attention skip the entries beyond it. */
 int sb_set_length_bound(sb_ctx* ctx, int32_t max_T);
 
+/* Forced rank-head buckets, a synthetic workload knob for random-init
+ * weights: with buckets != NULL, every later sb_draft_block_expand takes
+ * the bucket of row r of sequence s from buckets[s * row_cap + r] instead of
+ * the argmax of the rank-head scores (Sec. 3.2, Eq. 4; psi and the scores
+ * are still computed), so that a caller can shape trees with given bucket
+ * frequencies (e.g. the class frequencies of the rank-head quality table,
+ * App. B).  buckets: device int32 [max_seqs][row_cap], owned by the caller,
+ * read on the call's stream by each sb_draft_block_expand (its contents may
+ * change between calls); values outside 0..3 are clamped to that range.
+ * NULL restores the argmax.  Errors: SB_EINVAL (NULL ctx, misaligned). */
+int sb_set_bucket_override(sb_ctx* ctx, const int32_t* buckets);
+
 /* Kernel timing.  While enabled, the library brackets every launch of the
  * projection GEMM, the tree attention (split kernel + merge) and the
  * vocabulary reduction with HIP events on the call's stream and accumulates

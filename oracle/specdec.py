@@ -95,10 +95,13 @@ def prefill(target: Target, drafter: Drafter, prompt) -> SeqState:
 
 
 def expand_block(drafter: Drafter, st: SeqState, tree: DraftTree, rows: list,
-                 seg, starts: list, K: int, block: int, branch_map):
+                 seg, starts: list, K: int, block: int, branch_map,
+                 forced=None):
     """One block expansion (one batched drafter forward over all starts),
     followed by psi, the rank head, branching and sibling attachment.
-    Returns a record of everything the step computed."""
+    ``forced``, when given, replaces the rank head's bucket of row r (row id
+    within this iteration) by forced[r] clamped to 0..3; the scores are still
+    computed.  Returns a record of everything the step computed."""
     base = len(rows)
     block_rows = []
     for s, sp in enumerate(starts):
@@ -125,7 +128,8 @@ def expand_block(drafter: Drafter, st: SeqState, tree: DraftTree, rows: list,
         r.topk = topk_ids(z[i], TOPK)
         r.psi = psi(z[i])
         r.scores = rank_scores(drafter.rank_w, drafter.rank_b, h[i], r.psi)
-        r.bucket = bucket_of_scores(r.scores)
+        r.bucket = (bucket_of_scores(r.scores) if forced is None
+                    else min(max(int(forced[base + i]), 0), 3))
         r.branch = int(branch_map[r.bucket])
     first_new = len(tree.nodes)
     alive, chain = attach_block(tree, rows, block_rows, len(starts),
@@ -162,11 +166,13 @@ def continuing_row(tree: DraftTree, rows: list, n: int, K: int):
 
 
 def iteration(target: Target, drafter: Drafter, st: SeqState, w,
-              branch_map=None, plant=None) -> dict:
+              branch_map=None, plant=None, buckets=None) -> dict:
     """One verifier iteration (Alg. 2) for one sequence; mutates ``st``.
 
     ``plant(tree, rows)``, when given, may rewrite node tokens after drafting
-    and before verification (tests plant known continuations with it)."""
+    and before verification (tests plant known continuations with it).
+    ``buckets``, when given, forces the bucket of every drafter row of this
+    iteration (indexed by row id), a synthetic workload knob."""
     branch_map = tuple(branch_map or w.branch_map)
     K = w.K
     tree = DraftTree(st.root, w.budget)
@@ -179,7 +185,7 @@ def iteration(target: Target, drafter: Drafter, st: SeqState, w,
         if not starts:
             break
         rec = expand_block(drafter, st, tree, rows, seg, starts, K, m,
-                           branch_map)
+                           branch_map, buckets)
         rec["starts"] = starts
         expansions.append(rec)
         if m < w.M:
@@ -228,13 +234,15 @@ def iteration(target: Target, drafter: Drafter, st: SeqState, w,
 
 
 def speculative_decode(target: Target, drafter: Drafter, prompt, w,
-                       n_new: int, branch_map=None, plant=None):
-    """Prefill, then iterate until at least n_new tokens are committed."""
+                       n_new: int, branch_map=None, plant=None, buckets=None):
+    """Prefill, then iterate until at least n_new tokens are committed.
+    ``buckets(i)``, when given, returns the forced buckets of iteration i."""
     st = prefill(target, drafter, prompt)
     out = [st.root]
     taus = []
     while len(out) < n_new:
-        rec = iteration(target, drafter, st, w, branch_map, plant)
+        rec = iteration(target, drafter, st, w, branch_map, plant,
+                        None if buckets is None else buckets(len(taus)))
         out += rec["committed"]
         taus.append(rec["tau"])
     return out[:n_new], taus

@@ -123,6 +123,8 @@ struct sb_ctx {
   int* zero = nullptr;
   // running upper bound of every sequence's T (0: unknown)
   int T_bound = 0;
+  // forced drafter-row buckets [max_seqs][row_cap] (NULL: rank-head argmax)
+  const int* bucket_in = nullptr;
   // kernel timing
   struct ProfRec {
     int cls;
@@ -711,7 +713,8 @@ int draft_expand_impl(sb_ctx* c, int m, const sb_seqs* sq, const sb_kv* dkv,
     launch_vocab_partial(logits, p.n, p.cap, D.V, D.n_chunks, SB_TOPK,
                          c->vpart, st);
     const DraftRowOut ro{o->topk_id, o->topk_logit, o->lse, o->psi,
-                         o->bucket, o->branch, t->h_last, D.row_cap};
+                         o->bucket, o->branch, t->h_last, c->bucket_in,
+                         D.row_cap};
     const int4 bmap = make_int4(c->cfg.branch_map[0], c->cfg.branch_map[1],
                                 c->cfg.branch_map[2], c->cfg.branch_map[3]);
     launch_draft_finalize(c->vpart, D.n_chunks, p, c->x,
@@ -957,6 +960,14 @@ int sb_set_length_bound(sb_ctx* c, int32_t max_T) {
   if (!c) return SB_EINVAL;
   if (max_T < 0) return fail(c, SB_EINVAL, "max_T must be >= 0");
   c->T_bound = max_T;
+  return SB_OK;
+}
+
+int sb_set_bucket_override(sb_ctx* c, const int32_t* buckets) {
+  if (!c) return SB_EINVAL;
+  if (reinterpret_cast<uintptr_t>(buckets) % alignof(int32_t))
+    return fail(c, SB_EINVAL, "bucket override must be 4-byte aligned");
+  c->bucket_in = buckets;
   return SB_OK;
 }
 

@@ -135,6 +135,7 @@ struct DraftRowOut {
   int* bucket;
   int* branch;
   float* h_last;        // tree h_last [S][row_cap][d] (also the rank-head input)
+  const int* bucket_in; // optional forced buckets [S][row_cap] (else argmax)
   int row_cap;
 };
 void launch_draft_finalize(const float* part, int n_chunks, const CallPlan& p,

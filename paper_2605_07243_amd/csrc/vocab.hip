@@ -209,8 +209,8 @@ __device__ __forceinline__ void merge_row(const float* __restrict__ part,
 }
 
 // Drafter rows: psi = [log p of top-10, z1-z2, z1-z3, z1-z5, p1, entropy],
-// rank-head scores W_r [h^(L), psi] + b_r, bucket = argmax (ties low),
-// branch = map[bucket].  Also stores h^(L) into the tree's row cache.
+// rank-head scores W_r [h^(L), psi] + b_r, bucket = argmax (ties low) or,
+// when forced buckets are given, the forced one; branch = map[bucket].  Also stores h^(L) into the tree's row cache.
 __global__ __launch_bounds__(256) void draft_finalize_kernel(
     const float* __restrict__ part, int n_chunks, CallPlan p,
     const float* __restrict__ x, const float* __restrict__ rank_w,
@@ -276,6 +276,7 @@ __global__ __launch_bounds__(256) void draft_finalize_kernel(
         best = b;
       }
     }
+    if (out.bucket_in) best = min(max(out.bucket_in[o], 0), 3);
     const int map[4] = {bmap.x, bmap.y, bmap.z, bmap.w};
     out.bucket[o] = best;
     out.branch[o] = map[best];

@@ -297,6 +297,22 @@ class Runtime:
         T or the caches directly."""
         self._check(self.lib.sb_set_length_bound(self.ctx, int(max_T)))
 
+    def set_buckets(self, buckets):
+        """Force the drafter rows' buckets from a device int32 tensor
+        [n_seqs][row_cap] (read by every later expand; its contents may be
+        rewritten between calls), or restore the rank-head argmax (None)."""
+        if buckets is None:
+            self._buckets = None
+            self._check(self.lib.sb_set_bucket_override(self.ctx, None))
+            return
+        if (buckets.dtype != torch.int32 or not buckets.is_cuda
+                or tuple(buckets.shape) != (self.S, self.row_cap)
+                or not buckets.is_contiguous()):
+            raise ValueError("buckets must be a contiguous int32 device "
+                             f"tensor of shape ({self.S}, {self.row_cap})")
+        self._buckets = buckets
+        self._check(self.lib.sb_set_bucket_override(self.ctx, _ptr(buckets)))
+
     def profile(self, enable: bool):
         self._check(self.lib.sb_profile(self.ctx, 1 if enable else 0))
 

@@ -248,6 +248,27 @@ def prompts(w: Workload, seed: int = 1, lengths=None) -> list:
             for n in lengths]
 
 
+# Class frequencies of the rank-head buckets b0..b3 of a trained 8B-class
+# drafter (App. B, rank-head quality table), in tenths of a percent.
+PAPER_BUCKET_PERMILLE = (752, 150, 41, 57)
+
+
+def paper_buckets(seed: int, iteration: int, n_seqs: int,
+                  row_cap: int) -> np.ndarray:
+    """Forced drafter-row buckets of one iteration, int32 [n_seqs][row_cap]:
+    i.i.d. draws with the frequencies PAPER_BUCKET_PERMILLE, from a stream
+    keyed by (seed, iteration, sequence), so that a sequence's draws do not
+    depend on the batch it runs in."""
+    edges = np.cumsum(PAPER_BUCKET_PERMILLE)[:-1]
+    out = np.empty((n_seqs, row_cap), np.int32)
+    for s in range(n_seqs):
+        u = np.random.default_rng(
+            [seed, zlib.crc32(b"paper_buckets"), iteration, s]).integers(
+                0, 1000, size=row_cap)
+        out[s] = np.searchsorted(edges, u, side="right")
+    return out
+
+
 def random_kv(seed: int, name: str, n_tokens: int, s: ModelShape,
               dtype: str, std: float = 1.0):
     """Synthetic K and V of one layer, [n_tokens, n_kv_heads, head_dim]."""

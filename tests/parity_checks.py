@@ -88,15 +88,16 @@ def planter(stream, depth, vocab, snap):
     return plant
 
 
-def oracle_iteration(tgt, dr, st, w, plant_depth=0):
-    """One oracle iteration on a copy of ``st``; returns (state after, record,
-    drafted tree before planting)."""
+def oracle_iteration(tgt, dr, st, w, plant_depth=0, buckets=None):
+    """One oracle iteration on a copy of ``st`` (``buckets``: forced row
+    buckets); returns (state after, record, drafted tree before planting)."""
     after = copy.deepcopy(st)
     snap = []
     stream = continuation(tgt, st, plant_depth) if plant_depth else []
     rec = specdec.iteration(tgt, dr, after, w,
                             plant=planter(stream, plant_depth,
-                                          w.target.vocab, snap))
+                                          w.target.vocab, snap),
+                            buckets=buckets)
     return after, rec, snap[0]
 
 
@@ -136,9 +137,12 @@ def own_topk(z, k=10):
     return np.lexsort((np.arange(len(z)), -z))[:k]
 
 
-def check_rows(rt, s, exp, rows, lg_call, mine, dr, branch_map, tol, tally):
+def check_rows(rt, s, exp, rows, lg_call, mine, dr, branch_map, tol, tally,
+               forced=None):
     """Per-row checks of one expansion for sequence s; returns whether every
-    bucket equals the oracle's (then the tree's shape must too)."""
+    bucket equals the oracle's (then the tree's shape must too).  With
+    ``forced`` (the row buckets both sides were given) the buckets must
+    equal it exactly."""
     d = rt.dout
     lg = lg_call[mine]
     e = rel_err(lg, exp["logits"])
@@ -175,12 +179,16 @@ def check_rows(rt, s, exp, rows, lg_call, mine, dr, branch_map, tol, tally):
         # against the oracle's up to twice the score error
         sg = rank_w @ np.concatenate([hg, pg]) + rank_b
         bg = int(d["bucket"][s, o])
-        top2 = np.sort(sg)[::-1]
-        if bg != int(np.argmax(sg)):
-            assert top2[0] - sg[bg] < 1e-3 * max(1.0, abs(top2[0])), (s, o)
         es = float(np.abs(sg - r.scores).max())
-        if bg != r.bucket:
-            assert r.scores[r.bucket] - r.scores[bg] <= 2 * es + 1e-4, (s, o)
+        if forced is not None:
+            want = min(max(int(forced[o]), 0), 3)
+            assert bg == want and r.bucket == want, (s, o, bg, r.bucket)
+        else:
+            top2 = np.sort(sg)[::-1]
+            if bg != int(np.argmax(sg)):
+                assert top2[0] - sg[bg] < 1e-3 * max(1.0, abs(top2[0])), (s, o)
+            if bg != r.bucket:
+                assert r.scores[r.bucket] - r.scores[bg] <= 2 * es + 1e-4, (s, o)
         assert int(d["branch"][s, o]) == branch_map[bg]
         b = max(branch_map[bg], r.branch)
         ok = bg == r.bucket and list(ids[:b]) == list(r.topk[:b])
@@ -212,11 +220,13 @@ def check_tree_exact(rt, s, tree, rows, lo, hi, tol_cum):
     assert np.array_equal(anc[lo:hi], _anc_words(tree, hi, anc.shape[-1])[lo:hi]), s
 
 
-def run_and_compare(rt, seqs, w, tgt, dr, tol, tally, log=print):
+def run_and_compare(rt, seqs, w, tgt, dr, tol, tally, log=print,
+                    forced=None):
     """Drive one device iteration over all sequences, comparing the sampled
     ones; ``seqs`` maps seq -> (state before, state after, record, drafted
     tree).  The device's state for those sequences must equal the 'before'
-    state when called."""
+    state when called.  ``forced``: [n_seqs][row_cap] buckets both sides
+    were given, or None."""
     bmap = tuple(w.branch_map)
     for m in range(1, w.M + 1):
         log(f"expand {m}")
@@ -238,7 +248,8 @@ def run_and_compare(rt, seqs, w, tgt, dr, tol, tally, log=print):
             assert list(crow[mine]) == list(range(exp["base"],
                                                   exp["base"] + exp["R"]))
             exact = check_rows(rt, s, exp, rec["rows"], lg, mine, dr, bmap,
-                               tol, tally)
+                               tol, tally,
+                               None if forced is None else forced[s])
             lo = exp["first_new"]
             hi = exps[m]["first_new"] if m < len(exps) else len(drafted)
             nxt = [sp.node for sp in exps[m]["starts"]] if m < len(exps) else []

@@ -16,6 +16,7 @@ the device runs them all.
 """
 import numpy as np
 import pytest
+import torch
 
 import synth
 from oracle import specdec
@@ -60,6 +61,17 @@ def log(msg):
 
 @pytest.mark.parametrize("name", list(CASES))
 def test_iteration_full_layer_shape(name):
+    _iteration(name, paper_buckets=False)
+
+
+@pytest.mark.parametrize("name", ["8b-k4", "8b-batch16-paged"])
+def test_iteration_paper_frequency_buckets(name):
+    """The same comparison with every drafter row's bucket forced from the
+    seeded paper-frequency draws (both sides read the same array)."""
+    _iteration(name, paper_buckets=True)
+
+
+def _iteration(name, paper_buckets):
     wname, layers, sample = CASES[name]
     w = synth.with_layers(synth.WORKLOADS[wname], layers)
     log(f"[{name}] weights")
@@ -73,14 +85,27 @@ def test_iteration_full_layer_shape(name):
     del weights
     for s, st in enumerate(states):
         inject(rt, s, st)
+    forced = None
+    if paper_buckets:
+        forced = synth.paper_buckets(7, 0, w.n_seqs, rt.row_cap)
+        rt.set_buckets(torch.as_tensor(forced).to(rt.dev))
     seqs = {}
     for s in sample:
         depth = (w.K + 2 + 3 * s) % (2 * w.K + 1)
         log(f"[{name}] oracle seq {s} (T {states[s].T}, planted depth {depth})")
-        seqs[s] = (states[s],) + oracle_iteration(tgt, dr, states[s], w, depth)
+        seqs[s] = (states[s],) + oracle_iteration(
+            tgt, dr, states[s], w, depth,
+            None if forced is None else forced[s])
     tally = Tally()
     run_and_compare(rt, seqs, w, tgt, dr, TOL, tally,
-                    log=lambda m: log(f"[{name}] {m}"))
+                    log=lambda m: log(f"[{name}] {m}"), forced=forced)
     log(f"[{name}] {tally}; tau {[seqs[s][2]['tau'] for s in seqs]}")
+    if forced is not None:
+        for s in seqs:
+            R = sum(e["R"] for e in seqs[s][2]["expansions"])
+            got = rt.dout["bucket"][s, :R].cpu().numpy()
+            assert (got == forced[s][:R]).all(), s
+            assert [r.bucket for r in seqs[s][2]["rows"]] == list(forced[s][:R])
+        rt.set_buckets(None)
     assert tally.rows == sum(sum(e["R"] for e in seqs[s][2]["expansions"])
                              for s in seqs)
