@@ -62,10 +62,11 @@ def gemm_flops(w, verify_rows, rows_block, n_seqs):
     layer = (s.n_heads + 2 * s.n_kv_heads) * s.head_dim * d \
         + d * s.n_heads * s.head_dim + 2 * F * d + d * F
     lm = s.vocab * d
+    lm_d = (w.draft_vocab or s.vocab) * d
     fl = 2.0 * verify_rows * (s.n_layers * layer + lm)
     for i, rows in enumerate(rows_block):
         fl += 2.0 * rows * (3 * d * d + w.drafter_layers * (layer + 2 * d * d)
-                            + lm)
+                            + lm_d)
         if i % w.M == 0:
             fl += 2.0 * n_seqs * 3 * d * d
     return fl
@@ -355,6 +356,8 @@ def main():
         "config": {"workload": w.name,
                    "target": (f"Llama-3-shaped, {w.target.n_layers} layers, "
                               f"d {w.target.d_model}"),
+                   "drafter_layers": w.drafter_layers,
+                   "draft_vocab": w.draft_vocab or w.target.vocab,
                    "n_seqs": w.n_seqs, "prompt_len": list(w.prompt_len),
                    "K": w.K, "M": w.M, "B_max": w.B_max,
                    "budget": w.budget, "branch_map": list(w.branch_map),

@@ -83,6 +83,11 @@ typedef struct sb_config {
   int32_t max_pages;        /* page-table row length (pages per sequence),
                                1..16384                                       */
   int32_t prefill_chunk;    /* rows per prefill step (multiple of 16)         */
+  int32_t draft_vocab;      /* drafter output vocabulary: 0 = the target's;
+                               else a multiple of 16 in 10..vocab, the
+                               drafter's reduced vocabulary (App. A: the most
+                               frequent target tokens), mapped to target ids
+                               by sb_drafter_weights.d2t                      */
 } sb_config;
 
 /* One decoder layer.  elem matrices; float gains. */
@@ -113,9 +118,12 @@ typedef struct sb_drafter_weights {
   const void* w_fuse;      /* elem [d][3d]: W_fuse [norm c, norm e, norm q]   */
   const sb_layer_weights* layers;   /* host array [drafter_layers]            */
   const void* final_norm;  /* float [d]                                       */
-  const void* lm_head;     /* elem [V][d]                                     */
+  const void* lm_head;     /* elem [Vd][d], Vd = draft_vocab or V             */
   const void* rank_w;      /* float [4][d + 15]: rank head over [h^(L), psi]  */
   const void* rank_b;      /* float [4]                                       */
+  const int32_t* d2t;      /* device int32 [Vd]: target id of drafter id i,
+                              strictly increasing in [0, V) (checked by
+                              sb_bind); NULL only when Vd == V (identity)    */
 } sb_drafter_weights;
 
 /* Paged K/V cache of one model.  Entry i of sequence s lives in page
@@ -169,15 +177,15 @@ typedef struct sb_tree {
 
 /* Per-row results of one block expansion, indexed [S][row_cap]. */
 typedef struct sb_draft_out {
-  int32_t* topk_id;     /* [S][row_cap][10] ids, larger logit first, ties to
-                           the smaller id                                    */
+  int32_t* topk_id;     /* [S][row_cap][10] target ids (drafter ids through
+                           d2t), larger logit first, ties to the smaller id  */
   float* topk_logit;    /* [S][row_cap][10]                                  */
-  float* lse;           /* [S][row_cap] log-sum-exp of the row's logits      */
+  float* lse;           /* [S][row_cap] log-sum-exp of the row's Vd logits   */
   float* psi;           /* [S][row_cap][15] App. B summary                   */
   int32_t* bucket;      /* [S][row_cap] rank-head bucket 0..3 (Eq. 4)        */
   int32_t* branch;      /* [S][row_cap] b(bucket)                            */
-  float* logits;        /* optional (NULL = not written): [call_cap][V] in
-                           call-row order                                    */
+  float* logits;        /* optional (NULL = not written): [call_cap][Vd] in
+                           call-row order, drafter ids                       */
   int32_t* call_seq;    /* [call_cap] sequence of call row i                 */
   int32_t* call_row;    /* [call_cap] its row id within the sequence         */
   int32_t* n_call;      /* [1] rows in this call                             */
@@ -262,8 +270,10 @@ int sb_prefill(sb_ctx* ctx, const sb_seqs* seqs, const int32_t* prompt,
  * drafter layer the shift W_shift [h_k, h_{k-1}] (Eq. 3, h_0 := h_1) and the
  * decoder layer, attending to the drafter prefix (entries 1..T), the rows of
  * earlier blocks on the start's path and its own rows <= k.  Then the final
- * norm, LM head, top-10 / log-sum-exp / entropy, psi, the rank head
- * (argmax, ties to the lower bucket), b = branch_map[bucket], sibling
+ * norm, the LM head over the drafter vocabulary, top-10 (mapped to target
+ * ids through d2t) / log-sum-exp / entropy, psi, the rank head (argmax,
+ * ties to the lower bucket, unless sb_set_bucket_override forces the
+ * buckets), b = branch_map[bucket], sibling
  * attachment in (k, start, rank) order within the budget, and the next
  * starts (chain ends first, then rank>=2 siblings of b1/b2 rows by cum_logp,
  * at most B_max, none when the tree is full).

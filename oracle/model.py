@@ -129,7 +129,10 @@ class Drafter:
     * a final RMSNorm precedes the drafter LM head; the cached h^(L) is the
       pre-norm state;
     * the drafter shares the target's token embedding (the paper freezes the
-      drafter's embedding at the target's) and its vocabulary.
+      drafter's embedding at the target's); its LM head covers the target's
+      vocabulary or a reduced one (App. A: the most frequent target tokens)
+      whose ids map to target ids through ``d2t`` (strictly increasing, so
+      "smaller id" means the same in both numberings).
     """
 
     def __init__(self, raw: dict, shape, dtype: str, n_layers: int,
@@ -148,6 +151,8 @@ class Drafter:
                        for i in range(n_layers)]
         self.final_norm = g("final_norm")
         self.lm_head = g("lm_head")
+        self.d2t = (np.asarray(raw["d.d2t"], dtype=np.int64)
+                    if "d.d2t" in raw else None)
         self.rank_w = g("rank_w")
         self.rank_b = g("rank_b")
         self.n_layers = n_layers
@@ -159,6 +164,11 @@ class Drafter:
     def new_segment(self, cap: int) -> Segment:
         s = self.shape
         return Segment(self.n_layers, cap, s.n_kv_heads, s.head_dim)
+
+    def to_target(self, ids) -> np.ndarray:
+        """Target token ids of drafter output ids."""
+        ids = np.asarray(ids, dtype=np.int64)
+        return ids if self.d2t is None else self.d2t[ids]
 
     def cond_from_taps(self, taps3):
         """Eq. 1: c = W_cond [h_low, h_mid, h_top] (taps3: [3, d])."""
@@ -172,7 +182,7 @@ class Drafter:
         start row_start[r] and block position row_k[r] (1-based), and its
         shift partner is row row_pred[r] of this call (itself when k = 1,
         the convention h_{t,0} = h_{t,1}).
-        Returns (logits [R, V], h_last [R, d]).
+        Returns (logits [R, Vd] over the drafter's vocabulary, h_last [R, d]).
         """
         eps = self.shape.norm_eps
         num = self.num

@@ -125,7 +125,8 @@ def expand_block(drafter: Drafter, st: SeqState, tree: DraftTree, rows: list,
     for i, r in enumerate(new):
         r.logits, r.h_last = z[i], h[i]
         r.lse = float(logsumexp(z[i]))
-        r.topk = topk_ids(z[i], TOPK)
+        r.topk_d = topk_ids(z[i], TOPK)
+        r.topk = drafter.to_target(r.topk_d)
         r.psi = psi(z[i])
         r.scores = rank_scores(drafter.rank_w, drafter.rank_b, h[i], r.psi)
         r.bucket = (bucket_of_scores(r.scores) if forced is None

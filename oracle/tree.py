@@ -92,7 +92,8 @@ class DraftRow:
     logits: np.ndarray = None
     h_last: np.ndarray = None
     lse: float = 0.0
-    topk: np.ndarray = None
+    topk: np.ndarray = None      # top-10 target token ids
+    topk_d: np.ndarray = None    # the same as drafter output ids
     psi: np.ndarray = None
     scores: np.ndarray = None
     bucket: int = -1
@@ -122,7 +123,7 @@ def attach_block(tree: DraftTree, rows: list, block_rows: list, n_starts,
                     break
                 tok = int(r.topk[rank - 1])
                 n = tree.add(tok, parent, block_rows[s][k - 1], rank,
-                             r.logits[tok] - r.lse)
+                             r.logits[r.topk_d[rank - 1]] - r.lse)
                 if rank == 1:
                     chain[s] = n
                     got_chain = True

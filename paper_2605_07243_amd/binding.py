@@ -32,7 +32,8 @@ class Config(C.Structure):
                 ("tap_layers", i32 * 3), ("K", i32), ("M", i32),
                 ("B_max", i32), ("budget", i32), ("branch_map", i32 * 4),
                 ("dtype", i32), ("max_seqs", i32), ("page_size", i32),
-                ("max_pages", i32), ("prefill_chunk", i32)]
+                ("max_pages", i32), ("prefill_chunk", i32),
+                ("draft_vocab", i32)]
 
 
 class LayerWeights(C.Structure):
@@ -50,7 +51,8 @@ class DrafterWeights(C.Structure):
     _fields_ = [("w_cond", vp), ("norm_c", vp), ("norm_e", vp),
                 ("norm_q", vp), ("pos_query", vp), ("w_fuse", vp),
                 ("layers", C.POINTER(LayerWeights)), ("final_norm", vp),
-                ("lm_head", vp), ("rank_w", vp), ("rank_b", vp)]
+                ("lm_head", vp), ("rank_w", vp), ("rank_b", vp),
+                ("d2t", vp)]
 
 
 class KV(C.Structure):

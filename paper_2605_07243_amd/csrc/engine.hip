@@ -35,9 +35,9 @@ struct Carver {
 };
 
 struct Dims {
-  int S, d, H, Hkv, hd, F, V, L, LD, qkv_n, es;
+  int S, d, H, Hkv, hd, F, V, Vd, L, LD, qkv_n, es;
   int K, M, B_max, budget, row_cap, rw, bw, vis_words, R_cap, chunk;
-  int tpages, dpages, n_chunks, n_split;
+  int tpages, dpages, n_chunks, n_chunks_d, n_split;
   size_t part_elems;
 };
 
@@ -50,6 +50,7 @@ Dims derive(const sb_config& c) {
   D.hd = c.target.head_dim;
   D.F = c.target.d_ff;
   D.V = c.target.vocab;
+  D.Vd = c.draft_vocab > 0 ? c.draft_vocab : c.target.vocab;
   D.L = c.target.n_layers;
   D.LD = c.drafter_layers;
   D.qkv_n = (D.H + 2 * D.Hkv) * D.hd;
@@ -68,6 +69,7 @@ Dims derive(const sb_config& c) {
   D.tpages = ceil_div(std::max(D.budget, D.chunk), 16);
   D.dpages = ceil_div(std::max(D.row_cap, D.chunk), 16);
   D.n_chunks = std::max(1, std::min(64, D.V / 2048));
+  D.n_chunks_d = std::max(1, std::min(64, D.Vd / 2048));
   D.n_split = 32;
   // partial-sum buffer: the largest ks * N over the projections
   size_t mx = 0;
@@ -265,12 +267,19 @@ static int validate_cfg(const sb_config* c, std::string& msg) {
     msg = "vocab and the QKV width must be multiples of 16";
     return SB_ESHAPE;
   }
+  if (c->draft_vocab != 0 &&
+      (c->draft_vocab < SB_TOPK || c->draft_vocab > t.vocab ||
+       c->draft_vocab % 16)) {
+    msg = "draft_vocab must be 0 or a multiple of 16 in 10..vocab";
+    return SB_ESHAPE;
+  }
   {
     const int es = c->dtype == SB_BF16 ? 2 : 4;
     const int d = t.d_model, F = t.d_ff, hq = t.n_heads * t.head_dim;
     const int qkv = (t.n_heads + 2 * t.n_kv_heads) * t.head_dim;
+    const int vd = c->draft_vocab > 0 ? c->draft_vocab : t.vocab;
     const int shapes[][2] = {{qkv, d},   {d, hq},    {2 * F, d}, {d, F},
-                             {d, 3 * d}, {d, 2 * d}, {t.vocab, d}};
+                             {d, 3 * d}, {d, 2 * d}, {t.vocab, d}, {vd, d}};
     for (const auto& nk : shapes)
       if (!sb::gemm_shape_ok(nk[0], nk[1], es) || (es == 2 && F % 16)) {
         msg = es == 2 ? "bf16 projections need output widths % 32 == 0 and "
@@ -426,6 +435,20 @@ int sb_bind(sb_ctx* c, const sb_target_weights* tw,
       bad_ptr(dw->final_norm, 4) || bad_ptr(dw->lm_head, 16) ||
       bad_ptr(dw->rank_w, 4) || bad_ptr(dw->rank_b, 4))
     return fail(c, SB_EINVAL, "drafter weight pointer NULL or misaligned");
+  if (dw->d2t == nullptr && c->D.Vd != c->D.V)
+    return fail(c, SB_EINVAL, "a reduced drafter vocabulary needs d2t");
+  if (dw->d2t != nullptr) {
+    if (bad_ptr(dw->d2t, 4)) return fail(c, SB_EINVAL, "d2t misaligned");
+    // setup-time check of the id map (it indexes the embedding later)
+    std::vector<int32_t> m(c->D.Vd);
+    if (hipMemcpy(m.data(), dw->d2t, m.size() * sizeof(int32_t),
+                  hipMemcpyDefault) != hipSuccess)
+      return fail(c, SB_EHIP, "d2t: copy to host failed");
+    for (int i = 0; i < c->D.Vd; ++i)
+      if (m[i] < 0 || m[i] >= c->D.V || (i > 0 && m[i] <= m[i - 1]))
+        return fail(c, SB_EINVAL,
+                    "d2t must be strictly increasing target ids in [0, vocab)");
+  }
   for (int i = 0; i < c->D.L; ++i) {
     const int rc = check_layer(c, tw->layers[i], false);
     if (rc) return rc;
@@ -671,15 +694,15 @@ void cond_rows(sb_ctx* c, const float* taps, const int* idx, const int* n,
 // LM head: logits[i] = W_lm A[i] for the plan's rows (one K-chunk, written
 // straight into the logits buffer).
 template <typename T>
-void lm_head(sb_ctx* c, const void* A, const void* W, float* logits,
+void lm_head(sb_ctx* c, const void* A, const void* W, int V, float* logits,
              const int* n, int cap, hipStream_t st) {
   const Dims& D = c->D;
   const double es = sizeof(T);
   ProfScope ps(c, st, SB_PROF_GEMM,
-               (double)D.V * D.d * es + (double)cap * D.d * es + (double)cap * D.V * 4,
-               2.0 * cap * D.V * D.d);
+               (double)V * D.d * es + (double)cap * D.d * es + (double)cap * V * 4,
+               2.0 * cap * V * D.d);
   launch_gemm_xwt<T>(static_cast<const T*>(A), D.d, static_cast<const T*>(W),
-                     D.V, D.d, logits, (size_t)cap * D.V, n, cap, 1, st);
+                     V, D.d, logits, (size_t)cap * V, n, cap, 1, st);
 }
 
 TreeDims tree_dims(const sb_ctx* c, int n_seqs) {
@@ -707,17 +730,17 @@ int draft_expand_impl(sb_ctx* c, int m, const sb_seqs* sq, const sb_kv* dkv,
   const Prefix pf{dkv, c->dseg_k, c->dseg_v, D.dpages};
   drafter_forward<T>(c, p, cond_base, pf, D.B_max * D.K, true, st);
   float* logits = o->logits ? o->logits : c->logits;
-  lm_head<T>(c, c->A, c->dw.lm_head, logits, p.n, p.cap, st);
+  lm_head<T>(c, c->A, c->dw.lm_head, D.Vd, logits, p.n, p.cap, st);
   {
     ProfScope ps(c, st, SB_PROF_VOCAB);
-    launch_vocab_partial(logits, p.n, p.cap, D.V, D.n_chunks, SB_TOPK,
+    launch_vocab_partial(logits, p.n, p.cap, D.Vd, D.n_chunks_d, SB_TOPK,
                          c->vpart, st);
     const DraftRowOut ro{o->topk_id, o->topk_logit, o->lse, o->psi,
                          o->bucket, o->branch, t->h_last, c->bucket_in,
-                         D.row_cap};
+                         c->dw.d2t, D.Vd, D.row_cap};
     const int4 bmap = make_int4(c->cfg.branch_map[0], c->cfg.branch_map[1],
                                 c->cfg.branch_map[2], c->cfg.branch_map[3]);
-    launch_draft_finalize(c->vpart, D.n_chunks, p, c->x,
+    launch_draft_finalize(c->vpart, D.n_chunks_d, p, c->x,
                           static_cast<const float*>(c->dw.rank_w),
                           static_cast<const float*>(c->dw.rank_b), D.d, bmap,
                           ro, st);
@@ -738,7 +761,7 @@ int verify_impl(sb_ctx* c, const sb_seqs* sq, const sb_tree* t,
   const Prefix pf{tkv, c->tseg_k, c->tseg_v, D.tpages};
   target_forward<T>(c, p, pf, D.budget, out->taps, st);
   float* logits = out->logits ? out->logits : c->logits;
-  lm_head<T>(c, c->A, c->tw.lm_head, logits, p.n, p.cap, st);
+  lm_head<T>(c, c->A, c->tw.lm_head, D.V, logits, p.n, p.cap, st);
   {
     ProfScope ps(c, st, SB_PROF_VOCAB);
     launch_vocab_partial(logits, p.n, p.cap, D.V, D.n_chunks, 1, c->vpart, st);
@@ -805,7 +828,7 @@ int prefill_impl(sb_ctx* c, const sb_seqs* sq, const int32_t* prompt, int ld,
       launch_seg_to_cache<T>(p, tp, S, D.L, D.Hkv, D.hd, st);
       if (a + n == len) {
         const T* last = static_cast<const T*>(c->A) + (size_t)(n - 1) * D.d;
-        lm_head<T>(c, last, c->tw.lm_head, c->logits, c->one, 1, st);
+        lm_head<T>(c, last, c->tw.lm_head, D.V, c->logits, c->one, 1, st);
         launch_vocab_partial(c->logits, c->one, 1, D.V, D.n_chunks, 1,
                              c->vpart, st);
         launch_verify_finalize(c->vpart, D.n_chunks, c->one, 1, c->zero,

@@ -136,6 +136,8 @@ struct DraftRowOut {
   int* branch;
   float* h_last;        // tree h_last [S][row_cap][d] (also the rank-head input)
   const int* bucket_in; // optional forced buckets [S][row_cap] (else argmax)
+  const int* d2t;       // drafter id -> target id [n_vocab] (NULL: identity)
+  int n_vocab;          // drafter vocabulary (ids of the partial records)
   int row_cap;
 };
 void launch_draft_finalize(const float* part, int n_chunks, const CallPlan& p,

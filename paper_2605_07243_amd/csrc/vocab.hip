@@ -208,9 +208,12 @@ __device__ __forceinline__ void merge_row(const float* __restrict__ part,
   U = u;
 }
 
-// Drafter rows: psi = [log p of top-10, z1-z2, z1-z3, z1-z5, p1, entropy],
+// Drafter rows: top-10 ids (drafter ids mapped to target ids when the
+// drafter has a reduced vocabulary), log-sum-exp,
+// psi = [log p of top-10, z1-z2, z1-z3, z1-z5, p1, entropy],
 // rank-head scores W_r [h^(L), psi] + b_r, bucket = argmax (ties low) or,
-// when forced buckets are given, the forced one; branch = map[bucket].  Also stores h^(L) into the tree's row cache.
+// when forced buckets are given, the forced one; branch = map[bucket].
+// Also stores h^(L) into the tree's row cache.
 __global__ __launch_bounds__(256) void draft_finalize_kernel(
     const float* __restrict__ part, int n_chunks, CallPlan p,
     const float* __restrict__ x, const float* __restrict__ rank_w,
@@ -230,7 +233,9 @@ __global__ __launch_bounds__(256) void draft_finalize_kernel(
       const float lse = M + logf(S);
       const float ent = lse - U / S;
       for (int k = 0; k < SB_TOPK_K; ++k) {
-        out.topk_id[(size_t)o * SB_TOPK_K + k] = bi[k];
+        const int id = bi[k];
+        out.topk_id[(size_t)o * SB_TOPK_K + k] =
+            (out.d2t != nullptr && id >= 0 && id < out.n_vocab) ? out.d2t[id] : id;
         out.topk_logit[(size_t)o * SB_TOPK_K + k] = bv[k];
         psi_s[k] = bv[k] - lse;
       }

@@ -51,6 +51,7 @@ class Runtime:
         self.dev = torch.device(device)
         s = w.target
         self.S = n_seqs or w.n_seqs
+        self.Vd = w.draft_vocab or s.vocab
         if max_pages is None:
             max_pages = (max(w.prompt_len) + 64 * (w.M * w.K + 1) + 15) // 16
         self.max_pages = max_pages
@@ -67,6 +68,7 @@ class Runtime:
         cfg.page_size = 16
         cfg.max_pages = max_pages
         cfg.prefill_chunk = prefill_chunk
+        cfg.draft_vocab = w.draft_vocab
         self.cfg = cfg
         ctx = C.c_void_p()
         rc = self.lib.sb_create(C.byref(cfg), C.byref(ctx))
@@ -151,16 +153,32 @@ class Runtime:
                   pos_query=get("d.pos_query", (w.K, d)),
                   w_fuse=pack(get("d.w_fuse", (d, 3 * d))),
                   final_norm=get("d.final_norm", (d,), "ones"),
-                  lm_head=pack(get("d.lm_head", (s.vocab, d))),
+                  lm_head=pack(get("d.lm_head", (self.Vd, d))),
                   rank_w=get("d.rank_w", (4, d + 15), fp32=True),
-                  rank_b=get("d.rank_b", (4,), "zeros"))
+                  rank_b=get("d.rank_b", (4,), "zeros"),
+                  d2t=self._d2t(src, seed))
         self._keep = (keep, embed, tfin, tlm, dt, tl, dl)
         self.tw_c = B.TargetWeights(_ptr(embed), tl, _ptr(tfin), _ptr(tlm))
         self.dw_c = B.DrafterWeights(
             _ptr(dt["w_cond"]), _ptr(dt["norm_c"]), _ptr(dt["norm_e"]),
             _ptr(dt["norm_q"]), _ptr(dt["pos_query"]), _ptr(dt["w_fuse"]), dl,
             _ptr(dt["final_norm"]), _ptr(dt["lm_head"]), _ptr(dt["rank_w"]),
-            _ptr(dt["rank_b"]))
+            _ptr(dt["rank_b"]), _ptr(dt["d2t"]))
+
+    def _d2t(self, src, seed):
+        """Drafter id -> target id map of a reduced drafter vocabulary (None
+        for the full one): from the weights when given, else a seeded
+        sorted random subset of the target vocabulary."""
+        V, Vd = self.w.target.vocab, self.Vd
+        if Vd == V:
+            return None
+        if src is not None:
+            m = torch.as_tensor(np.asarray(src["d.d2t"], np.int32))
+        else:
+            g = torch.Generator().manual_seed(seed + 7)
+            m = torch.randperm(V, generator=g)[:Vd].sort().values.to(
+                torch.int32)
+        return m.to(self.dev).contiguous()
 
     def _buffers(self, page_seed):
         w, s, dev, S = self.w, self.w.target, self.dev, self.S
@@ -248,7 +266,7 @@ class Runtime:
     def expand(self, m, want_logits=False):
         if want_logits:
             if self.dout["logits"] is None:
-                self.dout["logits"] = torch.zeros(self.call_cap, self.V,
+                self.dout["logits"] = torch.zeros(self.call_cap, self.Vd,
                                                   dtype=torch.float32,
                                                   device=self.dev)
             lg = self.dout["logits"]

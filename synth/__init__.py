@@ -60,6 +60,7 @@ class Workload:
     prompt_len: tuple          # (lo, hi) inclusive; lo == hi for fixed length
     page_size: int = 16
     branch_map: tuple = (2, 4, 6, 4)
+    draft_vocab: int = 0       # drafter output vocabulary (0: the target's)
 
     @property
     def tap_layers(self) -> tuple:
@@ -89,6 +90,13 @@ WORKLOADS = {
                                         LLAMA3_8B, 1, K=4, M=2, B_max=8,
                                         budget=64, n_seqs=16,
                                         prompt_len=(512, 2048)),
+    # the paper's own drafter shape: two decoder layers, 32000-token
+    # reduced output vocabulary, K 4, M 2, 60-node trees (Sec. 4, App. A)
+    "llama3-8b-paper-drafter": Workload("llama3-8b-paper-drafter", "bf16",
+                                        LLAMA3_8B, 2, K=4, M=2, B_max=8,
+                                        budget=60, n_seqs=1,
+                                        prompt_len=(1024, 1024),
+                                        draft_vocab=32000),
     "llama3-70b-k6": Workload("llama3-70b-k6", "bf16", LLAMA3_70B, 1, K=6,
                               M=2, B_max=8, budget=96, n_seqs=4,
                               prompt_len=(2048, 2048)),
@@ -181,7 +189,7 @@ def target_specs(s: ModelShape):
     return specs
 
 
-def drafter_specs(s: ModelShape, n_layers: int, K: int):
+def drafter_specs(s: ModelShape, n_layers: int, K: int, draft_vocab: int = 0):
     d = s.d_model
     specs = [("d.w_cond", (d, 3 * d), "normal"),
              ("d.norm_c", (d,), "ones"),
@@ -193,7 +201,7 @@ def drafter_specs(s: ModelShape, n_layers: int, K: int):
         specs.append((f"d.layers.{i}.w_shift", (d, 2 * d), "normal"))
         specs += _layer_specs(f"d.layers.{i}.", s)
     specs += [("d.final_norm", (d,), "ones"),
-              ("d.lm_head", (s.vocab, d), "normal"),
+              ("d.lm_head", (draft_vocab or s.vocab, d), "normal"),
               ("d.rank_w", (4, d + 15), "normal"),
               ("d.rank_b", (4,), "zeros")]
     return specs
@@ -227,9 +235,21 @@ def target_weights(w: Workload, seed: int = 0, jitter: float = 0.0) -> dict:
     return make_weights(target_specs(w.target), seed, w.dtype, jitter=jitter)
 
 
+def draft_vocab_map(seed: int, vocab: int, draft_vocab: int) -> np.ndarray:
+    """Target ids of a reduced drafter vocabulary, int32 [draft_vocab],
+    strictly increasing: a seeded random subset standing in for the most
+    frequent target tokens (no token statistics exist for random weights)."""
+    ids = _rng(seed, "d2t").choice(vocab, size=draft_vocab, replace=False)
+    return np.sort(ids).astype(np.int32)
+
+
 def drafter_weights(w: Workload, seed: int = 0, jitter: float = 0.0) -> dict:
-    return make_weights(drafter_specs(w.target, w.drafter_layers, w.K), seed,
-                        w.dtype, jitter=jitter)
+    out = make_weights(drafter_specs(w.target, w.drafter_layers, w.K,
+                                     w.draft_vocab), seed, w.dtype,
+                       jitter=jitter)
+    if w.draft_vocab and w.draft_vocab != w.target.vocab:
+        out["d.d2t"] = draft_vocab_map(seed, w.target.vocab, w.draft_vocab)
+    return out
 
 
 def prompt_lengths(w: Workload, seed: int = 2) -> np.ndarray:

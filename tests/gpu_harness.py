@@ -15,9 +15,7 @@ from oracle.model import Drafter, Target
 def models(w, seed=0, jitter=0.1):
     tw = synth.make_weights(synth.target_specs(w.target), seed, w.dtype,
                             jitter=jitter)
-    dw = synth.make_weights(synth.drafter_specs(w.target, w.drafter_layers,
-                                                w.K), seed, w.dtype,
-                            jitter=jitter)
+    dw = synth.drafter_weights(w, seed, jitter=jitter)
     tgt = Target(tw, w.target, w.dtype, w.tap_layers)
     dr = Drafter(dw, w.target, w.dtype, w.drafter_layers, tgt.embed)
     return {**tw, **dw}, tgt, dr

@@ -157,15 +157,17 @@ def check_rows(rt, s, exp, rows, lg_call, mine, dr, branch_map, tol, tally,
         zg, zr = lg[i].astype(np.float64), r.logits
         E = float(np.abs(zg - zr).max())
         ids = host(d["topk_id"][s, o])
-        # the device's top-k is its own logits' top-k, values copied exactly
-        assert list(ids) == list(own_topk(lg[i])), (s, o)
-        assert np.array_equal(host(d["topk_logit"][s, o]), lg[i][ids]), (s, o)
+        # the device's top-k is its own logits' top-k (drafter ids, reported
+        # as target ids), values copied exactly
+        own = own_topk(lg[i])
+        assert list(ids) == list(dr.to_target(own)), (s, o)
+        assert np.array_equal(host(d["topk_logit"][s, o]), lg[i][own]), (s, o)
         lse_own = np.logaddexp.reduce(zg)
         assert abs(float(d["lse"][s, o]) - lse_own) < 1e-3 * max(1, abs(lse_own))
         # valid under the oracle's logits up to 2E
         zs = np.sort(zr)[::-1]
         assert len(set(ids.tolist())) == len(ids)
-        assert np.all(np.abs(zr[ids] - zs[:len(ids)]) <= 2 * E + 1e-6), (s, o)
+        assert np.all(np.abs(zr[own] - zs[:len(own)]) <= 2 * E + 1e-6), (s, o)
         # psi, h^(L)
         # psi: log-probabilities, gaps and p1 move by at most 2E each; the
         # entropy by at most 2E (H + 1)

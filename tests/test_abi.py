@@ -72,6 +72,11 @@ def cfg(**kw):
     (dict(dtype=B.SB_BF16, t_d_ff=1056), B.SB_ESHAPE),
     (dict(dtype=B.SB_BF16, t_d_model=288), B.SB_ESHAPE),
     (dict(dtype=B.SB_BF16, t_vocab=1040), B.SB_ESHAPE),
+    # reduced drafter vocabulary: 10..vocab, multiple of 16 (bf16: of 32)
+    (dict(draft_vocab=8), B.SB_ESHAPE),
+    (dict(draft_vocab=1040), B.SB_ESHAPE),
+    (dict(draft_vocab=1000), B.SB_ESHAPE),
+    (dict(dtype=B.SB_BF16, draft_vocab=528), B.SB_ESHAPE),
 ])
 def test_create_rejects_bad_configs(lib, kw, code):
     c = cfg(**kw)
@@ -111,7 +116,7 @@ def bound(lib):
     dl = (B.LayerWeights * 1)(B.LayerWeights(*[f.at()] * 7))
     tw = B.TargetWeights(f.at(), layers, f.at(), f.at())
     dw = B.DrafterWeights(f.at(), f.at(), f.at(), f.at(), f.at(), f.at(), dl,
-                          f.at(), f.at(), f.at(), f.at())
+                          f.at(), f.at(), f.at(), f.at(), None)
     need = lib.sb_workspace_bytes(C.byref(c))
     # too small, misaligned, then right: none of these touches the device
     assert lib.sb_bind(ctx, C.byref(tw), C.byref(dw), f.at(), need - 1) == \
@@ -219,3 +224,57 @@ def test_pack_weight_validation(lib, args, code):
     assert lib.sb_pack_weight(C.c_void_p(src), C.c_void_p(dst), rows, cols,
                               dtype, gate_up, None) == code
     assert lib.sb_last_error(None)
+
+
+def test_reduced_vocab_needs_map(lib):
+    c = cfg(draft_vocab=512)
+    ctx = C.c_void_p()
+    assert lib.sb_create(C.byref(c), C.byref(ctx)) == B.SB_OK
+    f = Fake()
+    layers = (B.LayerWeights * 2)(*[B.LayerWeights(*[f.at()] * 6, None)
+                                    for _ in range(2)])
+    dl = (B.LayerWeights * 1)(B.LayerWeights(*[f.at()] * 7))
+    tw = B.TargetWeights(f.at(), layers, f.at(), f.at())
+    dw = B.DrafterWeights(*([f.at()] * 6), dl, *([f.at()] * 4), None)
+    need = lib.sb_workspace_bytes(C.byref(c))
+    assert lib.sb_bind(ctx, C.byref(tw), C.byref(dw), f.at(), need) == \
+        B.SB_EINVAL
+    assert b"d2t" in lib.sb_last_error(ctx)
+    lib.sb_destroy(ctx)
+
+
+def test_struct_layouts_match_header(tmp_path):
+    """Every ctypes structure has the size and field offsets that a C
+    compiler gives the header's struct."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    structs = {"sb_model_dims": B.ModelDims, "sb_config": B.Config,
+               "sb_layer_weights": B.LayerWeights,
+               "sb_target_weights": B.TargetWeights,
+               "sb_drafter_weights": B.DrafterWeights, "sb_kv": B.KV,
+               "sb_seqs": B.Seqs, "sb_tree": B.Tree, "sb_draft_out": B.DraftOut,
+               "sb_verify_out": B.VerifyOut, "sb_accept_out": B.AcceptOut,
+               "sb_kernel_stat": B.KernelStat}
+    lines = ['#include <stdio.h>', '#include <stddef.h>',
+             f'#include "{HEADER}"', 'int main(void) {']
+    for cname, py in structs.items():
+        lines.append(f'printf("{cname} %zu\\n", sizeof({cname}));')
+        for fname, _ in py._fields_:
+            lines.append(f'printf("{cname}.{fname} %zu\\n", '
+                         f'offsetof({cname}, {fname}));')
+    lines.append("return 0; }")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run([cc, str(src), "-o", str(exe)], check=True)
+    got = dict(l.split() for l in
+               subprocess.run([str(exe)], check=True, capture_output=True,
+                              text=True).stdout.splitlines())
+    for cname, py in structs.items():
+        assert int(got[cname]) == C.sizeof(py), cname
+        for fname, _ in py._fields_:
+            assert int(got[f"{cname}.{fname}"]) == getattr(py, fname).offset, \
+                (cname, fname)

@@ -2,10 +2,11 @@
 (d 4096, 32/8 heads, FFN 14336, vocabulary 128256) with K = 4 / budget 60,
 with K = 8 / B_max 16 / budget 128 over a 4096-token prefix, and with 16
 ragged paged sequences; 70B-shaped (d 8192, 64/8 heads, FFN 28672) with
-K = 6 / budget 96 over 4 sequences.  Every kernel runs in the launch
-configuration the benchmark times (same dims, budgets, row and page
-capacities); only the target is shallower (1-2 layers) so that the float64
-oracle can recompute every call.
+K = 6 / budget 96 over 4 sequences; and the paper's drafter shape (two
+layers, 32000-token reduced vocabulary) on the 8B target.  Every kernel
+runs in the launch configuration the benchmark times (same dims, budgets,
+row and page capacities); only the target is shallower (1-2 layers) so that
+the float64 oracle can recompute every call.
 
 The committed prefix is synthetic (seeded random K/V of the workload's
 prompt lengths, the same on both sides).  One iteration is compared call by
@@ -33,6 +34,8 @@ CASES = {
     "8b-k8-long": ("llama3-8b-k8-long", 1, None),
     "8b-batch16-paged": ("llama3-8b-batch16-paged", 1, (0, 5, 10, 15)),
     "70b-k6": ("llama3-70b-k6", 1, (0, 3)),
+    # two drafter layers, 32000-token drafter vocabulary mapped to target ids
+    "8b-paper-drafter": ("llama3-8b-paper-drafter", 1, None),
 }
 
 

@@ -16,6 +16,7 @@ def _rows(draw_branch, draw_bucket, rng, n_starts, K, vocab):
             r.logits = z
             r.lse = float(np.log(np.exp(z).sum()))
             r.topk = np.argsort(-z, kind="stable")[:10]
+            r.topk_d = r.topk
             r.bucket = draw_bucket()
             r.branch = draw_branch(r.bucket)
             ids.append(len(rows))
