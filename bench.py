@@ -88,15 +88,15 @@ def gemm_traffic(workload):
     return d["bytes_per_dispatch"]
 
 
-def cpu_baseline(w, T, budget_s=10.0, paper_buckets=False):
+def cpu_baseline(w, T, budget_s=10.0, buckets="natural"):
     """Time the CPU oracle on a bounded sample of the workload: whole
     iterations of the real shapes (M block expansions of the drafter over a
     prefix of T entries, then the verify forward of the drafted tree through
     n_layers decoder layers and the LM head), repeated until budget_s of CPU
     time has passed.  To bound memory, the verify layers all use the weights
     and prefix cache of one generated layer: the arithmetic per layer is that
-    of a real layer.  paper_buckets: force the drafter rows' buckets from
-    the seeded paper-frequency draws, as the GPU run does."""
+    of a real layer.  buckets: "paper" / "uniform" force the drafter rows'
+    buckets as the GPU run does (seeded paper-frequency draws / all b1)."""
     import dataclasses
 
     import numpy as np
@@ -128,8 +128,11 @@ def cpu_baseline(w, T, budget_s=10.0, paper_buckets=False):
     st.dkv.k[0], st.dkv.v[0] = k.astype(np.float64), v.astype(np.float64)
 
     def iteration(i):
-        forced = (synth.paper_buckets(BUCKET_SEED, i, 1, w1.rows_per_seq)[0]
-                  if paper_buckets else None)
+        forced = None
+        if buckets == "paper":
+            forced = synth.paper_buckets(BUCKET_SEED, i, 1, w1.rows_per_seq)[0]
+        elif buckets == "uniform":
+            forced = synth.uniform_buckets(1, w1.rows_per_seq)[0]
         tree = specdec.DraftTree(st.root, w1.budget)
         rows = []
         seg = dr.new_segment(w1.rows_per_seq)
@@ -195,13 +198,17 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama3-8b-k4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--buckets", choices=("natural", "paper"),
+    ap.add_argument("--buckets", choices=("natural", "paper", "uniform"),
                     default="natural",
                     help="natural: the rank head's argmax decides each "
                          "drafter row's bucket; paper: buckets are forced "
                          "from seeded draws with the class frequencies of "
                          "a trained drafter (b0..b3 = 75.2/15.0/4.1/5.7%%), "
-                         "which shapes the trees like the paper's")
+                         "which shapes the trees like the paper's; uniform: "
+                         "the fixed-k tree of the rank-guided-branching "
+                         "ablation (every row b1, every bucket branches "
+                         "--uniform-k)")
+    ap.add_argument("--uniform-k", type=int, default=3)
     ap.add_argument("--calib-mib", type=int, default=0,
                     help="before warmup, run a plain elementwise copy "
                          "(torch.neg) of this many MiB three times, to "
@@ -220,6 +227,8 @@ def main():
     from paper_2605_07243_amd.runtime import Runtime
 
     w = synth.WORKLOADS[args.workload]
+    if args.buckets == "uniform":
+        w = synth.uniform_tree(w, args.uniform_k)
     es = 2 if w.dtype == "bf16" else 4
     log(f"workload {w.name}: allocating and generating weights on device")
     t = time.perf_counter()
@@ -235,12 +244,15 @@ def main():
     # forced buckets: one [n_seqs][row_cap] draw per iteration (warmup, timed
     # pass, profiled pass), resident on the device before timing
     sched = None
+    n_iter = args.warmup + 2 * args.steps
     if args.buckets == "paper":
         import numpy as np
-        n_iter = args.warmup + 2 * args.steps
         sched = torch.as_tensor(np.stack(
             [synth.paper_buckets(BUCKET_SEED, i, rt.S, rt.row_cap)
              for i in range(n_iter)])).to(rt.dev)
+    elif args.buckets == "uniform":
+        sched = torch.as_tensor(synth.uniform_buckets(
+            rt.S, rt.row_cap)).to(rt.dev).expand(n_iter, -1, -1)
     it = [0]
 
     def next_iteration():
@@ -361,10 +373,12 @@ def main():
                    "n_seqs": w.n_seqs, "prompt_len": list(w.prompt_len),
                    "K": w.K, "M": w.M, "B_max": w.B_max,
                    "budget": w.budget, "branch_map": list(w.branch_map),
-                   "buckets": ("natural (random rank head)"
-                               if sched is None else
-                               "paper-frequency (forced, seeded draws "
-                               "75.2/15.0/4.1/5.7%)")},
+                   "buckets": {
+                       "natural": "natural (random rank head)",
+                       "paper": "paper-frequency (forced, seeded draws "
+                                "75.2/15.0/4.1/5.7%)",
+                       "uniform": f"uniform fixed-{args.uniform_k} tree "
+                                  "(forced b1)"}[args.buckets]},
         "block_expansion_steps_per_s": round(w.M * args.steps /
                                              (draft_ms * 1e-3), 2),
         "block1_steps_per_s": round(args.steps / (block1_ms * 1e-3), 2),
@@ -410,7 +424,7 @@ def main():
         log("cpu baseline (oracle) ...")
         try:
             out["cpu_baseline"] = cpu_baseline(
-                w, max(w.prompt_len), paper_buckets=sched is not None)
+                w, max(w.prompt_len), buckets=args.buckets)
         except MemoryError as e:
             out["cpu_baseline"] = {"error": f"oracle sample did not fit: {e}"}
     print(json.dumps(out), flush=True)

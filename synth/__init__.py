@@ -289,6 +289,21 @@ def paper_buckets(seed: int, iteration: int, n_seqs: int,
     return out
 
 
+def uniform_tree(w: Workload, k: int) -> Workload:
+    """The "uniform fixed-k tree" ablation of rank-guided branching at the
+    same node budget (Sec. 4, ablations): every drafter row is forced into
+    bucket b1 (uniform_buckets) and every bucket branches k, so each row
+    contributes its top-k tokens and every sibling is a next-block start
+    candidate."""
+    return dataclasses.replace(w, name=f"{w.name}-uniform{k}",
+                               branch_map=(k, k, k, k))
+
+
+def uniform_buckets(n_seqs: int, row_cap: int) -> np.ndarray:
+    """Forced buckets of the uniform tree: b1 for every row."""
+    return np.ones((n_seqs, row_cap), np.int32)
+
+
 def random_kv(seed: int, name: str, n_tokens: int, s: ModelShape,
               dtype: str, std: float = 1.0):
     """Synthetic K and V of one layer, [n_tokens, n_kv_heads, head_dim]."""

@@ -9,7 +9,9 @@ class frequencies of the rank-head quality table (App. B).  Pins:
 * the tree shapes that the forced buckets imply (all b0: a chain plus one
   sibling per row; all b3 with b(b3) = 0: no drafted node at all);
 * out-of-range values clamp to 0..3;
-* greedy acceptance stays lossless under forced buckets (north-star (c)).
+* greedy acceptance stays lossless under forced buckets (north-star (c));
+* the uniform fixed-k tree of the rank-guided-branching ablation (Sec. 4):
+  all rows b1, every bucket branching k.
 """
 import copy
 
@@ -111,3 +113,30 @@ def test_lossless_under_paper_buckets(seed):
         buckets=lambda i: synth.paper_buckets(seed, i, 1, w.rows_per_seq)[0])
     assert out == ref
     assert all(t >= 1 for t in taus)
+
+
+def test_uniform_fixed_k_tree():
+    """The rank-guided-branching ablation: every row contributes its top-k
+    tokens under the same parent, and every sibling is a start candidate
+    (chain end first, then siblings by cumulative log-probability)."""
+    k = 3
+    w = synth.uniform_tree(_wl(K=3, M=2, B_max=3, budget=60), k)
+    assert w.branch_map == (k, k, k, k)
+    tgt, dr = _models(w)
+    st = specdec.prefill(tgt, dr, synth.prompts(w)[0])
+    rec = specdec.iteration(tgt, dr, st, w,
+                            buckets=synth.uniform_buckets(1, w.rows_per_seq)[0])
+    tree, e1 = rec["tree"], rec["expansions"][0]
+    assert e1["first_new"] == 1
+    block1 = tree.nodes[1:1 + w.K * k]
+    assert len(block1) == w.K * k
+    for kk in range(w.K):
+        sib = block1[kk * k:(kk + 1) * k]
+        assert [n.rank for n in sib] == list(range(1, k + 1))
+        assert len({n.parent for n in sib}) == 1
+        assert sib[0].depth == kk + 1
+    chain_end = 1 + (w.K - 1) * k
+    sibs = [i for i in range(1, 1 + w.K * k) if tree.nodes[i].rank >= 2]
+    by_cum = sorted(sibs, key=lambda i: (-tree.nodes[i].cum_logp, i))
+    want = [chain_end] + by_cum[:w.B_max - 1]
+    assert [sp.node for sp in rec["expansions"][1]["starts"]] == want
