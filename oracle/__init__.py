@@ -21,6 +21,9 @@ Decoding with Dynamic Tree Drafting):
 * ``specdec``   prefill, one verifier iteration (Alg. 2: M block expansions,
                 tree verification, greedy acceptance, commit) and plain greedy
                 decoding of the target for the lossless check.
+* ``sampling``  stochastic tree verification at temperature T > 0 (the
+                paper's T = 1.0 setting): recursive rejection sampling of a
+                node's children as point-mass drafts, then the residual draw.
 
 Readings of points the paper leaves open are listed with the code that takes
 them.  Floating point is float64 throughout; ``Numerics("bf16")`` additionally

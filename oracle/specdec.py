@@ -32,6 +32,7 @@ import numpy as np
 from .model import Drafter, Prefix, Target
 from .rank import TOPK, bucket_of_scores, psi, rank_scores, topk_ids
 from .numerics import logsumexp
+from .sampling import accept_sample
 from .tree import (DraftRow, DraftTree, Start, accept, attach_block,
                    select_starts)
 
@@ -167,13 +168,16 @@ def continuing_row(tree: DraftTree, rows: list, n: int, K: int):
 
 
 def iteration(target: Target, drafter: Drafter, st: SeqState, w,
-              branch_map=None, plant=None, buckets=None) -> dict:
+              branch_map=None, plant=None, buckets=None,
+              sampling=None) -> dict:
     """One verifier iteration (Alg. 2) for one sequence; mutates ``st``.
 
     ``plant(tree, rows)``, when given, may rewrite node tokens after drafting
     and before verification (tests plant known continuations with it).
     ``buckets``, when given, forces the bucket of every drafter row of this
-    iteration (indexed by row id), a synthetic workload knob."""
+    iteration (indexed by row id), a synthetic workload knob.
+    ``sampling`` = (temperature, u_acc, u_bonus) replaces greedy acceptance
+    by stochastic tree verification (``sampling.accept_sample``)."""
     branch_map = tuple(branch_map or w.branch_map)
     K = w.K
     tree = DraftTree(st.root, w.budget)
@@ -206,7 +210,11 @@ def iteration(target: Target, drafter: Drafter, st: SeqState, w,
                                     [tree.anc_or_self(i) for i in range(n)],
                                     st.tkv, tseg)
     greedy = np.array([argmax_low(z) for z in vlogits])
-    path, bonus = accept(tree, greedy)
+    if sampling is None:
+        path, bonus = accept(tree, greedy)
+    else:
+        smp = accept_sample(tree, vlogits, *sampling)
+        path, bonus = smp["path"], smp["bonus"]
     # commit
     T = st.T
     keep = [0] + path
@@ -235,15 +243,19 @@ def iteration(target: Target, drafter: Drafter, st: SeqState, w,
 
 
 def speculative_decode(target: Target, drafter: Drafter, prompt, w,
-                       n_new: int, branch_map=None, plant=None, buckets=None):
+                       n_new: int, branch_map=None, plant=None, buckets=None,
+                       sampling=None):
     """Prefill, then iterate until at least n_new tokens are committed.
-    ``buckets(i)``, when given, returns the forced buckets of iteration i."""
+    ``buckets(i)``, when given, returns the forced buckets of iteration i;
+    ``sampling(i)`` the (temperature, u_acc, u_bonus) of iteration i."""
     st = prefill(target, drafter, prompt)
     out = [st.root]
     taus = []
     while len(out) < n_new:
+        i = len(taus)
         rec = iteration(target, drafter, st, w, branch_map, plant,
-                        None if buckets is None else buckets(len(taus)))
+                        None if buckets is None else buckets(i),
+                        None if sampling is None else sampling(i))
         out += rec["committed"]
         taus.append(rec["tau"])
     return out[:n_new], taus
