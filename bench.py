@@ -209,6 +209,11 @@ def main():
                          "ablation (every row b1, every bucket branches "
                          "--uniform-k)")
     ap.add_argument("--uniform-k", type=int, default=3)
+    ap.add_argument("--temperature", type=float, default=0.0,
+                    help="0: greedy acceptance; > 0: stochastic tree "
+                         "verification at this temperature (the paper's "
+                         "sampling setting is 1.0), with seeded uniforms "
+                         "resident on the device")
     ap.add_argument("--calib-mib", type=int, default=0,
                     help="before warmup, run a plain elementwise copy "
                          "(torch.neg) of this many MiB three times, to "
@@ -260,6 +265,25 @@ def main():
             rt.set_buckets(sched[it[0]])
         it[0] += 1
 
+    sampling = args.temperature > 0
+    if sampling:
+        g = torch.Generator(device=rt.dev)
+        g.manual_seed(13)
+        u_acc = torch.rand((n_iter, rt.S, w.budget), generator=g,
+                           device=rt.dev)
+        u_bon = torch.rand((n_iter, rt.S, w.budget), generator=g,
+                           device=rt.dev)
+
+    def verify_accept():
+        """Verification and acceptance of the iteration just drafted."""
+        if sampling:
+            rt.verify(want_logits=True)
+            i = it[0] - 1
+            rt.accept_sample(args.temperature, u_acc[i], u_bon[i])
+        else:
+            rt.verify()
+            rt.accept()
+
     if args.calib_mib:
         src = torch.ones(args.calib_mib << 18, device=rt.dev)
         dst = torch.empty_like(src)
@@ -269,7 +293,10 @@ def main():
         del src, dst
     for i in range(args.warmup):
         next_iteration()
-        rt.iteration()
+        for m in range(1, w.M + 1):
+            rt.expand(m)
+        verify_accept()
+        rt.commit()
     torch.cuda.synchronize()
     log("warmup done")
 
@@ -286,8 +313,7 @@ def main():
         for m in range(1, w.M + 1):
             rt.expand(m)
             ev[i][m].record(stream)
-        rt.verify()
-        rt.accept()
+        verify_accept()
         rt.commit()
         ev[i][w.M + 1].record(stream)
     torch.cuda.synchronize()
@@ -323,8 +349,7 @@ def main():
             rt.expand(m)
             rows_block.append(int(rt.dout["n_call"][0]))
         verify_rows += int(rt.tree["n_nodes"].sum())
-        rt.verify()
-        rt.accept()
+        verify_accept()
         rt.commit()
     torch.cuda.synchronize()
     rt.profile(False)
@@ -378,7 +403,9 @@ def main():
                        "paper": "paper-frequency (forced, seeded draws "
                                 "75.2/15.0/4.1/5.7%)",
                        "uniform": f"uniform fixed-{args.uniform_k} tree "
-                                  "(forced b1)"}[args.buckets]},
+                                  "(forced b1)"}[args.buckets],
+                   "decoding": (f"sampling T={args.temperature:g}"
+                                if sampling else "greedy")},
         "block_expansion_steps_per_s": round(w.M * args.steps /
                                              (draft_ms * 1e-3), 2),
         "block1_steps_per_s": round(args.steps / (block1_ms * 1e-3), 2),

@@ -295,6 +295,32 @@ int sb_tree_verify(sb_ctx* ctx, const sb_seqs* seqs, const sb_tree* tree,
 int sb_accept(sb_ctx* ctx, int32_t n_seqs, const sb_tree* tree,
               const int32_t* argmax, sb_accept_out* out, void* stream);
 
+/* Stochastic acceptance at temperature T > 0, the paper's sampling setting
+ * (T = 1.0, Sec. 4), which it verifies by rejection sampling without
+ * giving the algorithm; this is the lossless multi-candidate scheme.  At
+ * node n, with p_n = softmax(z_n / T) over the target vocabulary, the
+ * children are tested in node-id order, each as a point-mass draft against
+ * the residual r (p_n without the tokens rejected so far, renormalised):
+ * child c with token x is accepted when u_accept[s][c] < r(x) and the walk
+ * moves to c; otherwise x leaves the residual (a child whose token was
+ * already rejected is skipped).  When no child is accepted, the bonus is the
+ * smallest token id whose cumulative residual mass exceeds u_bonus[s][n]
+ * times the residual total.  Every emitted token is then distributed as the
+ * target's own sample at that position.
+ * logits: device float [sum of n_nodes][V], the target logits of
+ *   sb_tree_verify (verify_out.logits) in call-row order (sequence-major,
+ *   node order) for the same n_seqs and tree;
+ * u_accept, u_bonus: device float [n_seqs][budget], uniforms in [0, 1)
+ *   indexed by node id (the caller draws them; the library draws nothing);
+ * out: as sb_accept (path, n_accepted, bonus; tau = n_accepted + 1), for
+ *   sb_commit.
+ * Errors: SB_EINVAL (temperature not positive and finite, NULL or
+ * misaligned pointers), SB_ESHAPE (n_seqs), SB_ESTATE (not bound). */
+int sb_accept_sample(sb_ctx* ctx, int32_t n_seqs, const sb_tree* tree,
+                     const float* logits, float temperature,
+                     const float* u_accept, const float* u_bonus,
+                     sb_accept_out* out, void* stream);
+
 /* Commit: target K/V of the root and accepted nodes (from the last
  * sb_tree_verify) become entries T..T+a; drafter entries for positions
  * T+1..T+a reuse the K/V of the rows that proposed the accepted nodes, and

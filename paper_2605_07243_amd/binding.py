@@ -100,7 +100,7 @@ EXPORTS = ["sb_row_capacity", "sb_workspace_bytes", "sb_create", "sb_destroy",
            "sb_last_error", "sb_bind", "sb_prefill", "sb_draft_block_expand",
            "sb_tree_verify", "sb_accept", "sb_commit", "sb_set_length_bound",
            "sb_profile", "sb_profile_read", "sb_pack_weight",
-           "sb_set_bucket_override"]
+           "sb_set_bucket_override", "sb_accept_sample"]
 
 _lib = None
 
@@ -146,6 +146,9 @@ def load(path: str = LIB_PATH):
     lib.sb_commit.restype = C.c_int
     lib.sb_set_length_bound.argtypes = [vp, i32]
     lib.sb_set_length_bound.restype = C.c_int
+    lib.sb_accept_sample.argtypes = [vp, i32, vp, vp, C.c_float, vp, vp,
+                                     vp, vp]
+    lib.sb_accept_sample.restype = C.c_int
     lib.sb_set_bucket_override.argtypes = [vp, vp]
     lib.sb_set_bucket_override.restype = C.c_int
     lib.sb_profile.argtypes = [vp, i32]

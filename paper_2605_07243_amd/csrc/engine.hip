@@ -106,6 +106,7 @@ struct sb_ctx {
   float* o_part = nullptr;
   float* ml = nullptr;
   float* logits = nullptr;
+  float* node_lse = nullptr;   // [S][budget] log-sum-exp of z / T per node
   float* vpart = nullptr;
   float* cond_buf = nullptr;
   float* taps_pf = nullptr;
@@ -165,6 +166,7 @@ static size_t layout(const Dims& D, void* base, sb_ctx* c) {
   float* o_part = cv.take<float>((size_t)D.n_split * R * D.H * D.hd * 4);
   float* ml = cv.take<float>((size_t)D.n_split * R * D.H * 2 * 4);
   float* logits = cv.take<float>(R * D.V * 4);
+  float* node_lse = cv.take<float>((size_t)D.S * D.budget * 4);
   float* vpart = cv.take<float>(R * D.n_chunks * kVocabRec10 * 4);
   float* cond_buf = cv.take<float>(R * D.d * 4);
   float* taps_pf = cv.take<float>((size_t)(D.chunk + 1) * 3 * D.d * 4);
@@ -214,6 +216,7 @@ static size_t layout(const Dims& D, void* base, sb_ctx* c) {
     c->o_part = o_part;
     c->ml = ml;
     c->logits = logits;
+    c->node_lse = node_lse;
     c->vpart = vpart;
     c->cond_buf = cond_buf;
     c->taps_pf = taps_pf;
@@ -938,6 +941,30 @@ int sb_accept(sb_ctx* c, int32_t n_seqs, const sb_tree* tree,
     return fail(c, SB_EINVAL, "accept pointer NULL or misaligned");
   launch_accept(tree_dims(c, n_seqs), *tree, argmax, *out, S_(stream));
   return hip_check(c, "sb_accept");
+}
+
+int sb_accept_sample(sb_ctx* c, int32_t n_seqs, const sb_tree* tree,
+                     const float* logits, float temperature,
+                     const float* u_accept, const float* u_bonus,
+                     sb_accept_out* out, void* stream) {
+  int rc = check_common(c);
+  if (rc) return rc;
+  if (n_seqs < 1 || n_seqs > c->cfg.max_seqs)
+    return fail(c, SB_ESHAPE, "n_seqs must be in 1..max_seqs");
+  if ((rc = check_tree(c, tree))) return rc;
+  if (!(temperature > 0.f) || !(temperature < 3.0e38f))
+    return fail(c, SB_EINVAL, "temperature must be positive and finite");
+  if (bad_ptr(logits, 4) || bad_ptr(u_accept, 4) || bad_ptr(u_bonus, 4) ||
+      !out || bad_ptr(out->path, 4) || bad_ptr(out->n_accepted, 4) ||
+      bad_ptr(out->bonus, 4))
+    return fail(c, SB_EINVAL, "accept_sample pointer NULL or misaligned");
+  const hipStream_t st = S_(stream);
+  const float inv_t = 1.0f / temperature;
+  launch_node_lse(logits, c->D.V, inv_t, tree->n_nodes, n_seqs, c->D.budget,
+                  c->node_lse, st);
+  launch_accept_sample(tree_dims(c, n_seqs), *tree, logits, c->D.V, inv_t,
+                       c->node_lse, u_accept, u_bonus, *out, st);
+  return hip_check(c, "sb_accept_sample");
 }
 
 int sb_commit(sb_ctx* c, sb_seqs* seqs, const sb_tree* tree,

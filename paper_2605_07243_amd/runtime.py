@@ -295,6 +295,24 @@ class Runtime:
             self.ctx, self.S, C.byref(self.tree_c),
             _ptr(self.vout["argmax"]), C.byref(self.aout_c), self.stream))
 
+    def accept_sample(self, temperature, u_accept, u_bonus):
+        """Stochastic acceptance over the logits of the last
+        verify(want_logits=True); u_accept, u_bonus: device float tensors
+        [n_seqs][budget] of uniforms in [0, 1)."""
+        if self.vout["logits"] is None:
+            raise RuntimeError("accept_sample needs verify(want_logits=True)")
+        for u in (u_accept, u_bonus):
+            if (u.dtype != torch.float32 or not u.is_cuda
+                    or tuple(u.shape) != (self.S, self.w.budget)
+                    or not u.is_contiguous()):
+                raise ValueError("uniforms must be contiguous float32 device "
+                                 f"tensors of shape ({self.S}, "
+                                 f"{self.w.budget})")
+        self._check(self.lib.sb_accept_sample(
+            self.ctx, self.S, C.byref(self.tree_c), _ptr(self.vout["logits"]),
+            float(temperature), _ptr(u_accept), _ptr(u_bonus),
+            C.byref(self.aout_c), self.stream))
+
     def commit(self):
         vc = B.VerifyOut(_ptr(self.vout["argmax"]), _ptr(self.vout["taps"]),
                          C.c_void_p(0))

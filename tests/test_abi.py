@@ -278,3 +278,22 @@ def test_struct_layouts_match_header(tmp_path):
         for fname, _ in py._fields_:
             assert int(got[f"{cname}.{fname}"]) == getattr(py, fname).offset, \
                 (cname, fname)
+
+
+def test_accept_sample_validation(bound):
+    lib, ctx, f = bound
+    tree = _tree(f)
+    out = B.AcceptOut(f.at(), f.at(), f.at())
+    call = lambda n=1, z=f.at(), T=1.0, ua=f.at(), ub=f.at(), o=out: \
+        lib.sb_accept_sample(ctx, n, C.byref(tree), z, T, ua, ub,  # noqa
+                             C.byref(o), None)
+    assert call(T=0.0) == B.SB_EINVAL
+    assert call(T=-1.0) == B.SB_EINVAL
+    assert call(T=float("inf")) == B.SB_EINVAL
+    assert call(T=float("nan")) == B.SB_EINVAL
+    assert b"temperature" in lib.sb_last_error(ctx)
+    assert call(z=None) == B.SB_EINVAL
+    assert call(ua=f.at(2)) == B.SB_EINVAL
+    assert call(o=B.AcceptOut(f.at(), None, f.at())) == B.SB_EINVAL
+    assert call(n=0) == B.SB_ESHAPE
+    assert call(n=2) == B.SB_ESHAPE
