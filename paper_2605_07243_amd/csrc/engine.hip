@@ -106,7 +106,7 @@ struct sb_ctx {
   float* o_part = nullptr;
   float* ml = nullptr;
   float* logits = nullptr;
-  float* node_lse = nullptr;   // [S][budget] log-sum-exp of z / T per node
+  float2* node_stats = nullptr;  // [S][budget][tiles] softmax stats of z / T
   float* vpart = nullptr;
   float* cond_buf = nullptr;
   float* taps_pf = nullptr;
@@ -166,7 +166,8 @@ static size_t layout(const Dims& D, void* base, sb_ctx* c) {
   float* o_part = cv.take<float>((size_t)D.n_split * R * D.H * D.hd * 4);
   float* ml = cv.take<float>((size_t)D.n_split * R * D.H * 2 * 4);
   float* logits = cv.take<float>(R * D.V * 4);
-  float* node_lse = cv.take<float>((size_t)D.S * D.budget * 4);
+  float2* node_stats = cv.take<float2>((size_t)D.S * D.budget *
+                                       sample_tiles(D.V) * 8);
   float* vpart = cv.take<float>(R * D.n_chunks * kVocabRec10 * 4);
   float* cond_buf = cv.take<float>(R * D.d * 4);
   float* taps_pf = cv.take<float>((size_t)(D.chunk + 1) * 3 * D.d * 4);
@@ -216,7 +217,7 @@ static size_t layout(const Dims& D, void* base, sb_ctx* c) {
     c->o_part = o_part;
     c->ml = ml;
     c->logits = logits;
-    c->node_lse = node_lse;
+    c->node_stats = node_stats;
     c->vpart = vpart;
     c->cond_buf = cond_buf;
     c->taps_pf = taps_pf;
@@ -958,12 +959,15 @@ int sb_accept_sample(sb_ctx* c, int32_t n_seqs, const sb_tree* tree,
       !out || bad_ptr(out->path, 4) || bad_ptr(out->n_accepted, 4) ||
       bad_ptr(out->bonus, 4))
     return fail(c, SB_EINVAL, "accept_sample pointer NULL or misaligned");
+  if (c->D.V > sample_max_vocab())
+    return fail(c, SB_ESHAPE, "sb_accept_sample supports vocab <= " +
+                                  std::to_string(sample_max_vocab()));
   const hipStream_t st = S_(stream);
   const float inv_t = 1.0f / temperature;
-  launch_node_lse(logits, c->D.V, inv_t, tree->n_nodes, n_seqs, c->D.budget,
-                  c->node_lse, st);
+  launch_node_stats(logits, c->D.V, inv_t, tree->n_nodes, n_seqs, c->D.budget,
+                    c->node_stats, st);
   launch_accept_sample(tree_dims(c, n_seqs), *tree, logits, c->D.V, inv_t,
-                       c->node_lse, u_accept, u_bonus, *out, st);
+                       c->node_stats, u_accept, u_bonus, *out, st);
   return hip_check(c, "sb_accept_sample");
 }
 

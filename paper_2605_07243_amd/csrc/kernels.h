@@ -184,12 +184,14 @@ void launch_attach(const TreeDims& td, const sb_tree& t, const sb_draft_out& o,
 void launch_plan_verify(const TreeDims& td, const sb_tree& t, const int* T,
                         const CallPlan& p, hipStream_t st);
 // Stochastic acceptance (sampling.hip).
-void launch_node_lse(const float* logits, int V, float inv_t,
-                     const int* n_nodes, int n_seqs, int budget, float* lse,
-                     hipStream_t st);
+int sample_tiles(int V);       // statistics tiles per node row
+int sample_max_vocab();
+void launch_node_stats(const float* logits, int V, float inv_t,
+                       const int* n_nodes, int n_seqs, int budget,
+                       float2* stats, hipStream_t st);
 void launch_accept_sample(const TreeDims& td, const sb_tree& t,
                           const float* logits, int V, float inv_t,
-                          const float* lse, const float* u_acc,
+                          const float2* stats, const float* u_acc,
                           const float* u_bonus, const sb_accept_out& o,
                           hipStream_t st);
 void launch_accept(const TreeDims& td, const sb_tree& t, const int* argmax,
