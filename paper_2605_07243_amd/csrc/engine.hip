@@ -501,23 +501,38 @@ hipEvent_t next_event(sb_ctx* c) {
   return c->ev_pool[c->ev_used++];
 }
 
-// Brackets one or more launches with events when profiling is on.
+// Times the launches of one class inside its scope.  The projection GEMM
+// (one launch per scope) takes events attached to its dispatch, which mark
+// the kernel's own start and end; other classes record stream events around
+// their launches.
 struct ProfScope {
   sb_ctx* c;
   hipStream_t st;
   int cls;
   double bytes, flops;
-  hipEvent_t a = nullptr;
+  hipEvent_t a = nullptr, b = nullptr;
   ProfScope(sb_ctx* c_, hipStream_t st_, int cls_, double bytes_ = 0,
             double flops_ = 0)
       : c(c_), st(st_), cls(cls_), bytes(bytes_), flops(flops_) {
-    if (c->prof && (a = next_event(c)) != nullptr) (void)hipEventRecord(a, st);
+    if (!c->prof || (a = next_event(c)) == nullptr) return;
+    if (cls == SB_PROF_GEMM) {
+      if ((b = next_event(c)) != nullptr) gemm_time_next_launch(a, b);
+      else a = nullptr;
+    } else {
+      (void)hipEventRecord(a, st);
+    }
   }
   ~ProfScope() {
     if (!a) return;
-    hipEvent_t b = next_event(c);
-    if (!b) return;
-    (void)hipEventRecord(b, st);
+    if (cls == SB_PROF_GEMM) {
+      if (gemm_time_pending()) {   // no launch took the events
+        gemm_time_next_launch(nullptr, nullptr);
+        return;
+      }
+    } else {
+      if ((b = next_event(c)) == nullptr) return;
+      (void)hipEventRecord(b, st);
+    }
     c->recs.push_back({cls, a, b, bytes, flops});
   }
 };

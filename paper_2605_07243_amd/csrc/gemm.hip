@@ -35,6 +35,8 @@
 //
 // f32 (gemm_xwt_kernel): row-major weights, fragments load straight into
 // registers and eight v_mfma_f32_16x16x4_f32 per 32-wide step.
+#include <hip/hip_ext.h>
+
 #include <algorithm>
 
 #include "common.h"
@@ -403,6 +405,28 @@ GemmPlan gemm_plan(int N, int K, int m_cap, int elem_bytes) {
   return g;
 }
 
+namespace {
+
+// Timing events for the next projection-GEMM launch, set by the library's
+// profiler and consumed by one launch: attached to the dispatch itself, they
+// record the kernel's own start and end (no marker packets in the stream).
+thread_local hipEvent_t g_ev_start = nullptr, g_ev_stop = nullptr;
+
+void take_events(hipEvent_t& a, hipEvent_t& b) {
+  a = g_ev_start;
+  b = g_ev_stop;
+  g_ev_start = g_ev_stop = nullptr;
+}
+
+}  // namespace
+
+void gemm_time_next_launch(hipEvent_t start, hipEvent_t stop) {
+  g_ev_start = start;
+  g_ev_stop = stop;
+}
+
+bool gemm_time_pending() { return g_ev_start != nullptr; }
+
 int gemm_ksplit(int N, int K, int elem_bytes) {
   // fewest row tiles -> most K-chunks
   return gemm_plan(N, K, 1, elem_bytes).ks;
@@ -421,9 +445,11 @@ void launch_tile(const GemmPlan& g, const bf16_t* X, int ldx, const bf16_t* W,
   const dim3 grid(n_mt * n_nt * ks);
 #define SB_LAUNCH(MF_, NF_, PF_)                                              \
   if (g.mf == MF_ && g.nf == NF_ && g.pf == PF_) {                            \
-    gemm_tile_kernel<MF_, NF_, PF_, SWIGLU><<<grid, 256, 0, st>>>(            \
-        X, ldx, W, K, P, N, part_stride, m_count, k_chunk, n_mt, n_nt, act,   \
-        F);                                                                   \
+    hipEvent_t ea, eb;                                                        \
+    take_events(ea, eb);                                                      \
+    hipExtLaunchKernelGGL(gemm_tile_kernel<MF_, NF_, PF_, SWIGLU>, grid,      \
+                          dim3(256), 0, st, ea, eb, 0, X, ldx, W, K, P, N,    \
+                          part_stride, m_count, k_chunk, n_mt, n_nt, act, F); \
     return;                                                                   \
   }
   SB_LAUNCH(1, 1, 2)
@@ -457,15 +483,20 @@ int launch_gemm_xwt(const T* X, int ldx, const T* W, int N, int K, float* P,
     const int ks = (K + k_chunk - 1) / k_chunk;
     const int mz = (m_cap + 63) / 64;
     const dim3 block(256);
+    hipEvent_t ea, eb;
+    take_events(ea, eb);
     if (m_cap <= 16) {
-      gemm_xwt_kernel<1><<<dim3(N / 16, ks, 1), block, 0, st>>>(
-          X, ldx, W, K, P, N, part_stride, m_count, k_chunk);
+      hipExtLaunchKernelGGL(gemm_xwt_kernel<1>, dim3(N / 16, ks, 1), block, 0,
+                            st, ea, eb, 0, X, ldx, W, K, P, N, part_stride,
+                            m_count, k_chunk);
     } else if (m_cap <= 32) {
-      gemm_xwt_kernel<2><<<dim3(N / 16, ks, 1), block, 0, st>>>(
-          X, ldx, W, K, P, N, part_stride, m_count, k_chunk);
+      hipExtLaunchKernelGGL(gemm_xwt_kernel<2>, dim3(N / 16, ks, 1), block, 0,
+                            st, ea, eb, 0, X, ldx, W, K, P, N, part_stride,
+                            m_count, k_chunk);
     } else {
-      gemm_xwt_kernel<4><<<dim3(N / 16, ks, mz), block, 0, st>>>(
-          X, ldx, W, K, P, N, part_stride, m_count, k_chunk);
+      hipExtLaunchKernelGGL(gemm_xwt_kernel<4>, dim3(N / 16, ks, mz), block, 0,
+                            st, ea, eb, 0, X, ldx, W, K, P, N, part_stride,
+                            m_count, k_chunk);
     }
     return ks;
   }

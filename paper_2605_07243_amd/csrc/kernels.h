@@ -58,6 +58,9 @@ struct GemmPlan {
 bool gemm_shape_ok(int N, int K, int elem_bytes);
 GemmPlan gemm_plan(int N, int K, int m_cap, int elem_bytes);
 // Largest K-split any call of this shape may use (partial-buffer sizing).
+// Kernel-attached timing of the next projection-GEMM launch (profiling).
+void gemm_time_next_launch(hipEvent_t start, hipEvent_t stop);
+bool gemm_time_pending();
 int gemm_ksplit(int N, int K, int elem_bytes);
 // P[ks][m][n] = X[m] . W[n] over K-chunk ks for the first *m_count rows.
 // bf16 W is fragment-packed, f32 W row-major.  ksplit <= 0: the plan's
