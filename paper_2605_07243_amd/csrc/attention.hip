@@ -15,6 +15,7 @@
 // needs only a 4-lane reduction and P never leaves registers.  V pages are
 // stored transposed ([hd][16 slots]) so the V^T operand is two 8/16-byte
 // loads.  Splits are combined with log-sum-exp weights.
+#include <hip/hip_ext.h>
 #include "common.h"
 #include "kernels.h"
 
@@ -718,7 +719,7 @@ __global__ __launch_bounds__(merge_threads<NS>()) void attn_merge_kernel_t(
 template <typename T>
 void launch_attn_merge(const CallPlan& p, int H, int hd, int n_split,
                        const float* o_part, const float* ml, T* out,
-                       hipStream_t st);
+                       hipStream_t st, hipEvent_t stop);
 
 namespace {
 
@@ -759,11 +760,30 @@ AttnShape attn_shape(int rows_per_seq_cap, int G, int seq_heads, int es) {
 
 }  // namespace
 
+namespace {
+
+// Timing events for the next tree-attention call (kernel start, merge or
+// kernel end), set by the library's profiler and consumed by one call.
+thread_local hipEvent_t g_attn_start = nullptr, g_attn_stop = nullptr;
+
+}  // namespace
+
+void attn_time_next_launch(hipEvent_t start, hipEvent_t stop) {
+  g_attn_start = start;
+  g_attn_stop = stop;
+}
+
+bool attn_time_pending() { return g_attn_start != nullptr; }
+
 template <typename T>
 void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
                       int rows_per_seq_cap, int H, int Hkv, int hd,
                       int n_split, int max_prefix, float* o_part, float* ml,
                       T* out, hipStream_t st) {
+  hipEvent_t ea = g_attn_start, eb = g_attn_stop;
+  g_attn_start = g_attn_stop = nullptr;
+  // with a merge, the kernel carries the start event and the merge the stop
+  hipEvent_t ka = ea, kb = n_split > 1 ? nullptr : eb;
   const AttnShape a =
       attn_shape(rows_per_seq_cap, H / Hkv, p.n_seqs * Hkv, (int)sizeof(T));
   // the caller picks n_split so that a split spans at most 1024 pages (the
@@ -777,9 +797,11 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
     if (a.mfma32) {
 #define SB_ATTN32(HD_, NW_)                                                    \
   if (hd == HD_ && a.nq == NW_) {                                             \
-    tree_attn32_kernel<HD_, NW_><<<grid, NW_ * 64, 0, st>>>(                  \
-        q, p, kv, H, Hkv, split_tokens, scale, o_part, ml, out);              \
-    if (n_split > 1) launch_attn_merge<T>(p, H, hd, n_split, o_part, ml, out, st); \
+    hipExtLaunchKernelGGL(tree_attn32_kernel<HD_, NW_>, grid, dim3(NW_ * 64), \
+                          0, st, ka, kb, 0, q, p, kv, H, Hkv, split_tokens,   \
+                          scale, o_part, ml, out);                            \
+    if (n_split > 1)                                                          \
+      launch_attn_merge<T>(p, H, hd, n_split, o_part, ml, out, st, eb);       \
     return;                                                                   \
   }
     SB_ATTN32(128, 8) SB_ATTN32(128, 4) SB_ATTN32(64, 8) SB_ATTN32(64, 4)
@@ -789,9 +811,11 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
   {
 #define SB_ATTN(HD_, NQ_, QT_)                                                 \
   if (hd == HD_ && a.nq == NQ_ && a.qt == QT_) {                              \
-    tree_attn_kernel<T, HD_, NQ_, QT_><<<grid, NQ_ * 64, 0, st>>>(            \
-        q, p, kv, H, Hkv, split_tokens, scale, o_part, ml, out);              \
-    if (n_split > 1) launch_attn_merge<T>(p, H, hd, n_split, o_part, ml, out, st); \
+    hipExtLaunchKernelGGL(tree_attn_kernel<T, HD_, NQ_, QT_>, grid,           \
+                          dim3(NQ_ * 64), 0, st, ka, kb, 0, q, p, kv, H, Hkv, \
+                          split_tokens, scale, o_part, ml, out);              \
+    if (n_split > 1)                                                          \
+      launch_attn_merge<T>(p, H, hd, n_split, o_part, ml, out, st, eb);       \
     return;                                                                   \
   }
     SB_ATTN(128, 8, 2) SB_ATTN(128, 8, 1) SB_ATTN(128, 4, 1)
@@ -805,14 +829,16 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
 template <typename T>
 void launch_attn_merge(const CallPlan& p, int H, int hd, int n_split,
                        const float* o_part, const float* ml, T* out,
-                       hipStream_t st) {
+                       hipStream_t st, hipEvent_t stop) {
   // every split's (m, l) and partial row is loaded at once (no dependent
   // chain); the template size is n_split rounded up, extra slots read as
   // empty splits
 #define SB_MERGE(NS_)                                                          \
   if (n_split <= NS_) {                                                       \
-    attn_merge_kernel_t<NS_><<<p.cap, merge_threads<NS_>(), 0, st>>>(         \
-        o_part, ml, p.n, p.cap, H, hd, n_split, out, sizeof(T));              \
+    hipExtLaunchKernelGGL(attn_merge_kernel_t<NS_>, dim3(p.cap),              \
+                          dim3(merge_threads<NS_>()), 0, st, nullptr, stop,   \
+                          0, o_part, ml, p.n, p.cap, H, hd, n_split, out,     \
+                          (int)sizeof(T));                                    \
     return;                                                                   \
   }
   SB_MERGE(2) SB_MERGE(4) SB_MERGE(8) SB_MERGE(16) SB_MERGE(32)

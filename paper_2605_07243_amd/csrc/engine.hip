@@ -502,9 +502,9 @@ hipEvent_t next_event(sb_ctx* c) {
 }
 
 // Times the launches of one class inside its scope.  The projection GEMM
-// (one launch per scope) takes events attached to its dispatch, which mark
-// the kernel's own start and end; other classes record stream events around
-// their launches.
+// (one launch per scope) and the tree attention (kernel + merge) take events
+// attached to their dispatches, which mark the kernels' own start and end;
+// other classes record stream events around their launches.
 struct ProfScope {
   sb_ctx* c;
   hipStream_t st;
@@ -515,9 +515,10 @@ struct ProfScope {
             double flops_ = 0)
       : c(c_), st(st_), cls(cls_), bytes(bytes_), flops(flops_) {
     if (!c->prof || (a = next_event(c)) == nullptr) return;
-    if (cls == SB_PROF_GEMM) {
-      if ((b = next_event(c)) != nullptr) gemm_time_next_launch(a, b);
-      else a = nullptr;
+    if (cls == SB_PROF_GEMM || cls == SB_PROF_ATTN) {
+      if ((b = next_event(c)) == nullptr) a = nullptr;
+      else if (cls == SB_PROF_GEMM) gemm_time_next_launch(a, b);
+      else attn_time_next_launch(a, b);
     } else {
       (void)hipEventRecord(a, st);
     }
@@ -527,6 +528,11 @@ struct ProfScope {
     if (cls == SB_PROF_GEMM) {
       if (gemm_time_pending()) {   // no launch took the events
         gemm_time_next_launch(nullptr, nullptr);
+        return;
+      }
+    } else if (cls == SB_PROF_ATTN) {
+      if (attn_time_pending()) {
+        attn_time_next_launch(nullptr, nullptr);
         return;
       }
     } else {

@@ -61,6 +61,9 @@ GemmPlan gemm_plan(int N, int K, int m_cap, int elem_bytes);
 // Kernel-attached timing of the next projection-GEMM launch (profiling).
 void gemm_time_next_launch(hipEvent_t start, hipEvent_t stop);
 bool gemm_time_pending();
+// Kernel-attached timing of the next tree-attention call (kernel + merge).
+void attn_time_next_launch(hipEvent_t start, hipEvent_t stop);
+bool attn_time_pending();
 int gemm_ksplit(int N, int K, int elem_bytes);
 // P[ks][m][n] = X[m] . W[n] over K-chunk ks for the first *m_count rows.
 // bf16 W is fragment-packed, f32 W row-major.  ksplit <= 0: the plan's
