@@ -203,6 +203,17 @@ typedef struct sb_accept_out {
   int32_t* path;        /* [S][M K] accepted node ids, root excluded         */
   int32_t* n_accepted;  /* [S] a: accepted draft tokens                      */
   int32_t* bonus;       /* [S] target token after the last accepted node     */
+  float* r_reject;      /* optional (NULL = not written): [S] the verifier-
+                           derived signal's r (Sec. 3.4, Eq. 8): the
+                           drafter's probability of the bonus token at the
+                           rejected position, from the drafter row that
+                           predicted the position after the last accepted
+                           node (its cached h^(L) through the final norm
+                           and LM head, over its log-sum-exp); 0 when the
+                           bonus is outside a reduced drafter vocabulary,
+                           -1 when no drafter row predicts that position.
+                           A query's signal is s = sum of (1 - r) over its
+                           iterations with r >= 0.                          */
 } sb_accept_out;
 
 typedef struct sb_ctx sb_ctx;

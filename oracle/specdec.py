@@ -167,6 +167,27 @@ def continuing_row(tree: DraftTree, rows: list, n: int, K: int):
     return None
 
 
+def reject_signal(drafter: Drafter, tree: DraftTree, rows: list, path: list,
+                  bonus: int, K: int):
+    """The verifier-derived signal's r at the rejected position (Sec. 3.4,
+    Eq. 8): the drafter's probability of the target's token (the bonus) at
+    the position after the last accepted node, from the drafter row that
+    predicted that position (the row continuing that node).  None when no
+    row did; 0 when the bonus is outside a reduced drafter vocabulary."""
+    cur = path[-1] if path else 0
+    j = continuing_row(tree, rows, cur, K)
+    if j is None:
+        return None
+    z = rows[j].logits
+    if drafter.d2t is None:
+        idx = bonus
+    else:
+        idx = int(np.searchsorted(drafter.d2t, bonus))
+        if idx >= len(drafter.d2t) or drafter.d2t[idx] != bonus:
+            return 0.0
+    return float(np.exp(z[idx] - logsumexp(z)))
+
+
 def iteration(target: Target, drafter: Drafter, st: SeqState, w,
               branch_map=None, plant=None, buckets=None,
               sampling=None) -> dict:
@@ -215,6 +236,7 @@ def iteration(target: Target, drafter: Drafter, st: SeqState, w,
     else:
         smp = accept_sample(tree, vlogits, *sampling)
         path, bonus = smp["path"], smp["bonus"]
+    r_reject = reject_signal(drafter, tree, rows, path, bonus, K)
     # commit
     T = st.T
     keep = [0] + path
@@ -239,6 +261,7 @@ def iteration(target: Target, drafter: Drafter, st: SeqState, w,
     return dict(tree=tree, rows=rows, expansions=expansions,
                 verify_logits=vlogits, greedy=greedy, taps=vtaps, path=path,
                 bonus=bonus, tau=len(path) + 1, committed=committed,
+                r_reject=r_reject,
                 fallback=fallback, T_before=T)
 
 

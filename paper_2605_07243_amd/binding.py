@@ -86,7 +86,8 @@ class VerifyOut(C.Structure):
 
 
 class AcceptOut(C.Structure):
-    _fields_ = [("path", vp), ("n_accepted", vp), ("bonus", vp)]
+    _fields_ = [("path", vp), ("n_accepted", vp), ("bonus", vp),
+                ("r_reject", vp)]
 
 
 class KernelStat(C.Structure):

@@ -107,6 +107,7 @@ struct sb_ctx {
   float* ml = nullptr;
   float* logits = nullptr;
   float2* node_stats = nullptr;  // [S][budget][tiles] softmax stats of z / T
+  float* row_lse = nullptr;      // [S][row_cap] drafter rows' log-sum-exp
   float* vpart = nullptr;
   float* cond_buf = nullptr;
   float* taps_pf = nullptr;
@@ -166,6 +167,7 @@ static size_t layout(const Dims& D, void* base, sb_ctx* c) {
   float* o_part = cv.take<float>((size_t)D.n_split * R * D.H * D.hd * 4);
   float* ml = cv.take<float>((size_t)D.n_split * R * D.H * 2 * 4);
   float* logits = cv.take<float>(R * D.V * 4);
+  float* row_lse = cv.take<float>((size_t)D.S * D.row_cap * 4);
   float2* node_stats = cv.take<float2>((size_t)D.S * D.budget *
                                        sample_tiles(D.V) * 8);
   float* vpart = cv.take<float>(R * D.n_chunks * kVocabRec10 * 4);
@@ -218,6 +220,7 @@ static size_t layout(const Dims& D, void* base, sb_ctx* c) {
     c->ml = ml;
     c->logits = logits;
     c->node_stats = node_stats;
+    c->row_lse = row_lse;
     c->vpart = vpart;
     c->cond_buf = cond_buf;
     c->taps_pf = taps_pf;
@@ -762,7 +765,7 @@ int draft_expand_impl(sb_ctx* c, int m, const sb_seqs* sq, const sb_kv* dkv,
                          c->vpart, st);
     const DraftRowOut ro{o->topk_id, o->topk_logit, o->lse, o->psi,
                          o->bucket, o->branch, t->h_last, c->bucket_in,
-                         c->dw.d2t, D.Vd, D.row_cap};
+                         c->dw.d2t, c->row_lse, D.Vd, D.row_cap};
     const int4 bmap = make_int4(c->cfg.branch_map[0], c->cfg.branch_map[1],
                                 c->cfg.branch_map[2], c->cfg.branch_map[3]);
     launch_draft_finalize(c->vpart, D.n_chunks_d, p, c->x,
@@ -951,6 +954,30 @@ int sb_tree_verify(sb_ctx* c, const sb_seqs* seqs, const sb_tree* tree,
                     : verify_impl<float>(c, seqs, tree, target_kv, out, S_(stream));
 }
 
+}  // extern "C"
+
+namespace {
+
+// The verifier-derived signal of sb_accept / sb_accept_sample, when asked.
+void reject_signal(sb_ctx* c, int n_seqs, const sb_tree& t,
+                   const sb_accept_out& o, hipStream_t st) {
+  if (o.r_reject == nullptr) return;
+  const float eps = c->cfg.target.norm_eps;
+  const float* g = static_cast<const float*>(c->dw.final_norm);
+  if (is_bf16(c))
+    launch_reject_signal<bf16_t>(tree_dims(c, n_seqs), t, o, c->row_lse,
+                                 static_cast<const bf16_t*>(c->dw.lm_head), g,
+                                 eps, c->dw.d2t, c->D.Vd, o.r_reject, st);
+  else
+    launch_reject_signal<float>(tree_dims(c, n_seqs), t, o, c->row_lse,
+                                static_cast<const float*>(c->dw.lm_head), g,
+                                eps, c->dw.d2t, c->D.Vd, o.r_reject, st);
+}
+
+}  // namespace
+
+extern "C" {
+
 int sb_accept(sb_ctx* c, int32_t n_seqs, const sb_tree* tree,
               const int32_t* argmax, sb_accept_out* out, void* stream) {
   int rc = check_common(c);
@@ -959,9 +986,11 @@ int sb_accept(sb_ctx* c, int32_t n_seqs, const sb_tree* tree,
     return fail(c, SB_ESHAPE, "n_seqs must be in 1..max_seqs");
   if ((rc = check_tree(c, tree))) return rc;
   if (bad_ptr(argmax, 4) || !out || bad_ptr(out->path, 4) ||
-      bad_ptr(out->n_accepted, 4) || bad_ptr(out->bonus, 4))
+      bad_ptr(out->n_accepted, 4) || bad_ptr(out->bonus, 4) ||
+      (out->r_reject && bad_ptr(out->r_reject, 4)))
     return fail(c, SB_EINVAL, "accept pointer NULL or misaligned");
   launch_accept(tree_dims(c, n_seqs), *tree, argmax, *out, S_(stream));
+  reject_signal(c, n_seqs, *tree, *out, S_(stream));
   return hip_check(c, "sb_accept");
 }
 
@@ -978,7 +1007,7 @@ int sb_accept_sample(sb_ctx* c, int32_t n_seqs, const sb_tree* tree,
     return fail(c, SB_EINVAL, "temperature must be positive and finite");
   if (bad_ptr(logits, 4) || bad_ptr(u_accept, 4) || bad_ptr(u_bonus, 4) ||
       !out || bad_ptr(out->path, 4) || bad_ptr(out->n_accepted, 4) ||
-      bad_ptr(out->bonus, 4))
+      bad_ptr(out->bonus, 4) || (out->r_reject && bad_ptr(out->r_reject, 4)))
     return fail(c, SB_EINVAL, "accept_sample pointer NULL or misaligned");
   if (c->D.V > sample_max_vocab())
     return fail(c, SB_ESHAPE, "sb_accept_sample supports vocab <= " +
@@ -989,6 +1018,7 @@ int sb_accept_sample(sb_ctx* c, int32_t n_seqs, const sb_tree* tree,
                     c->node_stats, st);
   launch_accept_sample(tree_dims(c, n_seqs), *tree, logits, c->D.V, inv_t,
                        c->node_stats, u_accept, u_bonus, *out, st);
+  reject_signal(c, n_seqs, *tree, *out, st);
   return hip_check(c, "sb_accept_sample");
 }
 

@@ -143,6 +143,7 @@ struct DraftRowOut {
   float* h_last;        // tree h_last [S][row_cap][d] (also the rank-head input)
   const int* bucket_in; // optional forced buckets [S][row_cap] (else argmax)
   const int* d2t;       // drafter id -> target id [n_vocab] (NULL: identity)
+  float* lse_copy;      // the library's own copy of lse [S][row_cap]
   int n_vocab;          // drafter vocabulary (ids of the partial records)
   int row_cap;
 };
@@ -189,6 +190,13 @@ void launch_attach(const TreeDims& td, const sb_tree& t, const sb_draft_out& o,
                    const int* blk_row0, const int* blk_nst, hipStream_t st);
 void launch_plan_verify(const TreeDims& td, const sb_tree& t, const int* T,
                         const CallPlan& p, hipStream_t st);
+// Verifier-derived signal at the rejected position (tree.hip).
+template <typename T>
+void launch_reject_signal(const TreeDims& td, const sb_tree& t,
+                          const sb_accept_out& acc, const float* row_lse,
+                          const T* lm_head, const float* gain, float eps,
+                          const int* d2t, int Vd, float* r_out,
+                          hipStream_t st);
 // Stochastic acceptance (sampling.hip).
 int sample_tiles(int V);       // statistics tiles per node row
 int sample_max_vocab();

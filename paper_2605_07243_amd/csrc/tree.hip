@@ -306,6 +306,23 @@ __global__ __launch_bounds__(64) void accept_kernel(TreeDims td, sb_tree t,
   }
 }
 
+// The drafter row at position pos(cur) + 1 on a path through node cur: the
+// next row of cur's block when cur is a chain node short of K, else row 1 of
+// a block started at cur; -1 when the tree has none.
+__device__ int continuing_row(const TreeDims& td, const sb_tree& t, int s,
+                              int cur) {
+  const size_t nb = (size_t)s * td.budget;
+  const size_t rb = (size_t)s * td.row_cap;
+  const int nrows = t.n_rows[s];
+  if (cur == 0) return nrows > 0 ? 0 : -1;
+  const int r = t.row[nb + cur];
+  if (t.rank[nb + cur] == 1 && t.row_k[rb + r] < td.K && r + 1 < nrows)
+    return r + 1;
+  for (int j = 0; j < nrows; ++j)
+    if (t.row_start[rb + j] == cur && t.row_k[rb + j] == 1) return j;
+  return -1;
+}
+
 // Commit planning: last accepted node, the drafter row continuing it (or a
 // catch-up row when the tree has none) and the catch-up call plan.
 __global__ void commit_plan_kernel(TreeDims td, sb_tree t, sb_accept_out acc,
@@ -318,22 +335,7 @@ __global__ void commit_plan_kernel(TreeDims td, sb_tree t, sb_accept_out acc,
     const size_t rb = (size_t)s * td.row_cap;
     const int a = acc.n_accepted[s];
     const int cur = a > 0 ? acc.path[(size_t)s * path_cap + a - 1] : 0;
-    int cont = -1;
-    const int nrows = t.n_rows[s];
-    if (cur == 0) {
-      if (nrows > 0) cont = 0;
-    } else {
-      const int r = t.row[nb + cur];
-      if (t.rank[nb + cur] == 1 && t.row_k[rb + r] < td.K && r + 1 < nrows)
-        cont = r + 1;
-    }
-    if (cont < 0) {
-      for (int j = 0; j < nrows; ++j)
-        if (t.row_start[rb + j] == cur && t.row_k[rb + j] == 1) {
-          cont = j;
-          break;
-        }
-    }
+    const int cont = continuing_row(td, t, s, cur);
     ci.T_old[s] = T[s];
     ci.a[s] = a;
     ci.cur[s] = cur;
@@ -586,10 +588,112 @@ void launch_plan_verify(const TreeDims& td, const sb_tree& t, const int* T,
                         const CallPlan& p, hipStream_t st) {
   plan_verify_kernel<<<1, 256, 0, st>>>(td, t, T, p);
 }
+// Verifier-derived update signal (Sec. 3.4, Eq. 8): at the rejected position
+// (the one after the last accepted node, where the bonus token stands), the
+// drafter's probability r of the target's token, from the row that predicted
+// that position: r = exp(z[bonus] - lse) with z[bonus] = W_lm[bonus] .
+// norm(h^(L)) recomputed from the row's cached h^(L) (the final RMSNorm and
+// the LM-head operand rounding of the drafter forward), lse the row's
+// log-sum-exp.  -1 when no drafter row predicts that position; 0 when the
+// bonus token is outside a reduced drafter vocabulary.
+template <typename T>
+__global__ __launch_bounds__(256) void reject_signal_kernel(
+    TreeDims td, sb_tree t, sb_accept_out acc, const float* __restrict__ row_lse,
+    const T* __restrict__ lm_head, const float* __restrict__ gain, float eps,
+    const int* __restrict__ d2t, int Vd, float* __restrict__ r_out) {
+  __shared__ float red[4];
+  __shared__ int sh_id;
+  const int s = blockIdx.x, tid = threadIdx.x;
+  const int path_cap = td.M * td.K;
+  const int a = acc.n_accepted[s];
+  const int cur = a > 0 ? acc.path[(size_t)s * path_cap + a - 1] : 0;
+  const int cont = continuing_row(td, t, s, cur);
+  if (cont < 0) {
+    if (tid == 0) r_out[s] = -1.f;
+    return;
+  }
+  const int bonus = acc.bonus[s];
+  if (tid == 0) {
+    int id = -1;
+    if (d2t == nullptr) {
+      id = (bonus >= 0 && bonus < Vd) ? bonus : -1;
+    } else {   // d2t is strictly increasing: binary search
+      int lo = 0, hi = Vd - 1;
+      while (lo <= hi) {
+        const int mid = (lo + hi) >> 1;
+        const int v = d2t[mid];
+        if (v == bonus) {
+          id = mid;
+          break;
+        }
+        if (v < bonus) lo = mid + 1;
+        else hi = mid - 1;
+      }
+    }
+    sh_id = id;
+  }
+  __syncthreads();
+  const int id = sh_id;
+  if (id < 0) {
+    if (tid == 0) r_out[s] = 0.f;
+    return;
+  }
+  const int d = td.d;
+  const size_t o = (size_t)s * td.row_cap + cont;
+  const float* h = t.h_last + o * d;
+  const int lane = tid & 63, w = tid >> 6;
+  float ss = 0.f;
+  for (int k = tid; k < d; k += 256) ss += h[k] * h[k];
+  ss = wave_sum(ss);
+  if (lane == 0) red[w] = ss;
+  __syncthreads();
+  const float rs = 1.0f / sqrtf((red[0] + red[1] + red[2] + red[3]) / (float)d + eps);
+  __syncthreads();
+  float z = 0.f;
+  for (int k = tid; k < d; k += 256) {
+    const float x = Elem<T>::to_f32(Elem<T>::from_f32(h[k] * rs * gain[k]));
+    size_t wi;
+    if constexpr (sizeof(T) == 2) {
+      // fragment-packed LM head (32-row x 64-column blocks)
+      const int c = k & 63;
+      const int l = (id & 31) + 32 * (c >> 5);
+      wi = ((((size_t)(id >> 5) * (d >> 6) + (k >> 6)) * 4 + ((c & 31) >> 3)) *
+            512) + (size_t)l * 8 + (k & 7);
+    } else {
+      wi = (size_t)id * d + k;
+    }
+    z += Elem<T>::to_f32(lm_head[wi]) * x;
+  }
+  z = wave_sum(z);
+  if (lane == 0) red[w] = z;
+  __syncthreads();
+  if (tid == 0)
+    r_out[s] = __expf((red[0] + red[1] + red[2] + red[3]) - row_lse[o]);
+}
+
 void launch_accept(const TreeDims& td, const sb_tree& t, const int* argmax,
                    const sb_accept_out& o, hipStream_t st) {
   accept_kernel<<<td.S, 64, 0, st>>>(td, t, argmax, o);
 }
+template <typename T>
+void launch_reject_signal(const TreeDims& td, const sb_tree& t,
+                          const sb_accept_out& acc, const float* row_lse,
+                          const T* lm_head, const float* gain, float eps,
+                          const int* d2t, int Vd, float* r_out,
+                          hipStream_t st) {
+  reject_signal_kernel<T><<<td.S, 256, 0, st>>>(td, t, acc, row_lse, lm_head,
+                                                gain, eps, d2t, Vd, r_out);
+}
+template void launch_reject_signal<float>(const TreeDims&, const sb_tree&,
+                                          const sb_accept_out&, const float*,
+                                          const float*, const float*, float,
+                                          const int*, int, float*,
+                                          hipStream_t);
+template void launch_reject_signal<bf16_t>(const TreeDims&, const sb_tree&,
+                                           const sb_accept_out&, const float*,
+                                           const bf16_t*, const float*, float,
+                                           const int*, int, float*,
+                                           hipStream_t);
 void launch_commit_plan(const TreeDims& td, const sb_tree& t,
                         const sb_accept_out& acc, const int* T,
                         const CommitInfo& ci, const CallPlan& fb,

@@ -245,6 +245,7 @@ __global__ __launch_bounds__(256) void draft_finalize_kernel(
       psi_s[13] = __expf(bv[0] - lse);
       psi_s[14] = ent;
       out.lse[o] = lse;
+      out.lse_copy[o] = lse;
       for (int k = 0; k < SB_PSI; ++k) out.psi[(size_t)o * SB_PSI + k] = psi_s[k];
     }
   }

@@ -238,9 +238,11 @@ class Runtime:
                          taps=torch.zeros(S, bud, 3, d, **f32), logits=None)
         self.aout = dict(path=torch.zeros(S, w.M * w.K, **i32),
                          n_accepted=torch.zeros(S, **i32),
-                         bonus=torch.zeros(S, **i32))
+                         bonus=torch.zeros(S, **i32),
+                         r_reject=torch.zeros(S, **f32))
         self.aout_c = B.AcceptOut(*[_ptr(self.aout[f]) for f in
-                                    ("path", "n_accepted", "bonus")])
+                                    ("path", "n_accepted", "bonus",
+                                     "r_reject")])
         self.V = V
 
     # ------------------------------------------------------------------

@@ -306,6 +306,13 @@ def run_and_compare(rt, seqs, w, tgt, dr, tol, tally, log=print,
         assert a == len(rec["path"]), (s, a, rec["path"])
         assert list(host(rt.aout["path"][s, :a])) == rec["path"]
         assert int(rt.aout["bonus"][s]) == rec["bonus"]
+        # verifier-derived signal: the device recomputes the bonus logit from
+        # the row's cached h^(L) (bf16 operand, fp32 sums) over its own lse
+        rg, rr = float(rt.aout["r_reject"][s]), rec["r_reject"]
+        if rr is None:
+            assert rg == -1.0, (s, rg)
+        else:
+            assert abs(rg - rr) <= 5e-2 * rr + 1e-7, (s, rg, rr)
         assert int(rt.T[s]) == after.T and int(rt.root[s]) == after.root
         assert rel_err(host(rt.cond_taps[s]), after.cond_taps).max() < tol
         T0, n = before.T, after.T - before.T

@@ -295,5 +295,6 @@ def test_accept_sample_validation(bound):
     assert call(z=None) == B.SB_EINVAL
     assert call(ua=f.at(2)) == B.SB_EINVAL
     assert call(o=B.AcceptOut(f.at(), None, f.at())) == B.SB_EINVAL
+    assert call(o=B.AcceptOut(f.at(), f.at(), f.at(), f.at(2))) == B.SB_EINVAL
     assert call(n=0) == B.SB_ESHAPE
     assert call(n=2) == B.SB_ESHAPE

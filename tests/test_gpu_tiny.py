@@ -110,6 +110,12 @@ def test_iteration_calls(tiny):
     assert a == len(rec["path"])
     assert list(host(rt.aout["path"][0, :a])) == rec["path"]
     assert int(rt.aout["bonus"][0]) == rec["bonus"]
+    # verifier-derived signal at the rejected position
+    rg, rr = float(rt.aout["r_reject"][0]), rec["r_reject"]
+    if rr is None:
+        assert rg == -1.0
+    else:
+        assert abs(rg - rr) <= 1e-3 * rr + 1e-9, (rg, rr)
     print("commit", flush=True)
     rt.commit()
     torch.cuda.synchronize()
