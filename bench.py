@@ -214,6 +214,11 @@ def main():
                          "verification at this temperature (the paper's "
                          "sampling setting is 1.0), with seeded uniforms "
                          "resident on the device")
+    ap.add_argument("--e2e-tokens", type=int, default=256,
+                    help="after the timed steps, decode until every sequence "
+                         "has this many new tokens and report the wall time "
+                         "of that loop (host loop and per-iteration "
+                         "synchronisation included); 0 skips it")
     ap.add_argument("--calib-mib", type=int, default=0,
                     help="before warmup, run a plain elementwise copy "
                          "(torch.neg) of this many MiB three times, to "
@@ -447,6 +452,37 @@ def main():
                      "avg_launch_us": round(gemm["ms"] * 1e3 /
                                             max(gemm["launches"], 1), 2)},
     }
+    if args.e2e_tokens > 0:
+        # end-to-end decode: iterations until every sequence has committed
+        # e2e_tokens more entries, the host reading T after each iteration
+        # (a serving loop's own check), within the page-table capacity
+        cap_T = rt.max_pages * 16 - (w.M * w.K + 1)
+        T_start = rt.T.clone().cpu()
+        iters, stop = 0, False
+        if sched is not None or sampling:
+            e2e_mode = "greedy acceptance, rank-head buckets"
+            rt.set_buckets(None)
+        else:
+            e2e_mode = "as the timed steps"
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        while not stop:
+            for m in range(1, w.M + 1):
+                rt.expand(m)
+            rt.verify()
+            rt.accept()
+            rt.commit()
+            iters += 1
+            Tn = rt.T.cpu()
+            stop = bool(((Tn - T_start) >= args.e2e_tokens).all()) or \
+                bool((Tn > cap_T).any())
+        dt_e2e = time.perf_counter() - t0
+        new = int((Tn - T_start).sum())
+        out["e2e"] = {"new_tokens_per_seq": int((Tn - T_start).min()),
+                      "iterations": iters, "wall_s": round(dt_e2e, 4),
+                      "tokens_per_s": round(new / dt_e2e, 3),
+                      "decoding": e2e_mode}
+        log(f"e2e: {new} tokens in {iters} iterations, {dt_e2e:.3f}s")
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
         try:
