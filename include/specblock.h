@@ -88,6 +88,8 @@ typedef struct sb_config {
                                drafter's reduced vocabulary (App. A: the most
                                frequent target tokens), mapped to target ids
                                by sb_drafter_weights.d2t                      */
+  int32_t adapt_cap;        /* positions per head-only update, 0..64 (0: no
+                               sb_adapt_push / sb_head_update)               */
 } sb_config;
 
 /* One decoder layer.  elem matrices; float gains. */
@@ -350,6 +352,59 @@ int sb_commit(sb_ctx* ctx, sb_seqs* seqs, const sb_tree* tree,
  * the page-table capacity max_pages * 16 is assumed).  A bound below the
  * true T makes attention skip the entries beyond it. */
 int sb_set_length_bound(sb_ctx* ctx, int32_t max_T);
+
+/* Serving-time adaptation, head-only action (Sec. 3.4; the per-query
+ * adaptation procedure of App. A.3; the bandit that picks the action is the
+ * caller's).  Rejected positions are buffered on the device; a head update
+ * steps a training copy of the drafter's LM head and rank head (the decoder
+ * trunk and the final norm stay frozen) and empties the buffer. */
+typedef struct sb_adapt_buffer {
+  float* h;           /* device [cap][d]: h^(L) of the drafter row that
+                         predicted each buffered position                   */
+  int32_t* target;    /* device [cap]: the token the target chose there     */
+  int32_t* count;     /* device [1]: positions held (caller zeroes it once) */
+  int32_t cap;        /* host: must equal cfg.adapt_cap                     */
+} sb_adapt_buffer;
+
+typedef struct sb_head_weights {
+  void* lm_head;      /* device elem [Vd][d], laid out like the bound
+                         drafter LM head (bf16: packed by sb_pack_weight)   */
+  float* rank_w;      /* device [4][d + 15]                                 */
+  float* rank_b;      /* device [4]                                         */
+} sb_head_weights;
+
+/* Append, for each of the n_seqs sequences whose rejected position (the one
+ * after the last accepted node of `acc`) has a predicting drafter row, that
+ * row's cached h^(L) and the bonus token, in sequence order, while the
+ * buffer has room (the rest are dropped).  Call after sb_accept /
+ * sb_accept_sample and before the next sb_draft_block_expand reuses the
+ * tree's rows.  Errors: SB_ESTATE (adapt_cap 0 or not bound), SB_EINVAL,
+ * SB_ESHAPE (n_seqs, buf->cap). */
+int sb_adapt_push(sb_ctx* ctx, int32_t n_seqs, const sb_tree* tree,
+                  const sb_accept_out* acc, sb_adapt_buffer* buf,
+                  void* stream);
+
+/* One head-only step on the buffered positions i (n = min(count, cap)):
+ * a_i = final_norm(h_i) (stored like the LM head's operand),
+ * p_i = softmax(W_train a_i) over the drafter vocabulary, p0_i the same
+ * with lm_head0 (the pre-deployment head, frozen); loss = mean over i of
+ *   -log p_i(y_i)                 (y_i = target[i] as a drafter id; no term
+ *                                  when it is outside a reduced vocabulary)
+ *   + kl_weight KL(p_i || p0_i)
+ *   - log softmax(W_r [h_i, psi_i] + b_r)(bucket of y_i's rank in p_i; b3
+ *                                  past rank 10 or outside the vocabulary)
+ * with psi_i and the rank labels taken before the step and held fixed; then
+ * train.lm_head, rank_w, rank_b -= lr * gradient (plain SGD; the LM head is
+ * rounded back to its element type), the mean loss (before the step) goes
+ * to loss_out (device float, optional) and count is reset to 0.  The update
+ * uses its own workspace, so it may run on another stream than inference
+ * (order it after the pushes it consumes); train.lm_head must be a copy
+ * distinct from the bound inference head and from lm_head0.  Errors:
+ * SB_ESTATE, SB_EINVAL (pointers, lr or kl_weight negative or not finite),
+ * SB_ESHAPE (buf->cap). */
+int sb_head_update(sb_ctx* ctx, sb_adapt_buffer* buf, const void* lm_head0,
+                   sb_head_weights* train, float lr, float kl_weight,
+                   float* loss_out, void* stream);
 
 /* Forced rank-head buckets, a synthetic workload knob for random-init
  * weights: with buckets != NULL, every later sb_draft_block_expand takes

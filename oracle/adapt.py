@@ -85,13 +85,12 @@ def head_loss(lm_w, rank_w, rank_b, lm_w0, A, h, ids, psis, buckets,
     return total / len(A)
 
 
-def head_grads(lm_w, rank_w, rank_b, lm_w0, A, h, ids, psis, buckets,
-               kl_weight):
-    """Gradients of head_loss with respect to W_lm, W_r and b_r."""
-    lm_w = np.asarray(lm_w, np.float64)
-    n = len(A)
-    Z = A @ lm_w.T
+def logit_grads(lm_w, lm_w0, A, ids, kl_weight):
+    """Gradient of head_loss with respect to the LM logits z_i = W_lm a_i
+    (rows already divided by the batch size)."""
+    Z = A @ np.asarray(lm_w, np.float64).T
     Z0 = A @ np.asarray(lm_w0, np.float64).T
+    n = len(A)
     G = np.zeros_like(Z)
     for i in range(n):
         logp = Z[i] - logsumexp(Z[i])
@@ -104,6 +103,14 @@ def head_grads(lm_w, rank_w, rank_b, lm_w0, A, h, ids, psis, buckets,
         kl = float(np.sum(p * (logp - logp0)))
         g += kl_weight * p * (logp - logp0 - kl)
         G[i] = g / n
+    return G
+
+
+def head_grads(lm_w, rank_w, rank_b, lm_w0, A, h, ids, psis, buckets,
+               kl_weight):
+    """Gradients of head_loss with respect to W_lm, W_r and b_r."""
+    n = len(A)
+    G = logit_grads(lm_w, lm_w0, A, ids, kl_weight)
     X = np.concatenate([np.asarray(h, np.float64), psis], axis=1)
     S = X @ np.asarray(rank_w, np.float64).T + np.asarray(rank_b, np.float64)
     Q = np.exp(S - np.array([logsumexp(s) for s in S])[:, None])

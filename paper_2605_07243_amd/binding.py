@@ -33,7 +33,7 @@ class Config(C.Structure):
                 ("B_max", i32), ("budget", i32), ("branch_map", i32 * 4),
                 ("dtype", i32), ("max_seqs", i32), ("page_size", i32),
                 ("max_pages", i32), ("prefill_chunk", i32),
-                ("draft_vocab", i32)]
+                ("draft_vocab", i32), ("adapt_cap", i32)]
 
 
 class LayerWeights(C.Structure):
@@ -53,6 +53,14 @@ class DrafterWeights(C.Structure):
                 ("layers", C.POINTER(LayerWeights)), ("final_norm", vp),
                 ("lm_head", vp), ("rank_w", vp), ("rank_b", vp),
                 ("d2t", vp)]
+
+
+class AdaptBuffer(C.Structure):
+    _fields_ = [("h", vp), ("target", vp), ("count", vp), ("cap", i32)]
+
+
+class HeadWeights(C.Structure):
+    _fields_ = [("lm_head", vp), ("rank_w", vp), ("rank_b", vp)]
 
 
 class KV(C.Structure):
@@ -101,7 +109,8 @@ EXPORTS = ["sb_row_capacity", "sb_workspace_bytes", "sb_create", "sb_destroy",
            "sb_last_error", "sb_bind", "sb_prefill", "sb_draft_block_expand",
            "sb_tree_verify", "sb_accept", "sb_commit", "sb_set_length_bound",
            "sb_profile", "sb_profile_read", "sb_pack_weight",
-           "sb_set_bucket_override", "sb_accept_sample"]
+           "sb_set_bucket_override", "sb_accept_sample", "sb_adapt_push",
+           "sb_head_update"]
 
 _lib = None
 
@@ -150,6 +159,11 @@ def load(path: str = LIB_PATH):
     lib.sb_accept_sample.argtypes = [vp, i32, vp, vp, C.c_float, vp, vp,
                                      vp, vp]
     lib.sb_accept_sample.restype = C.c_int
+    lib.sb_adapt_push.argtypes = [vp, i32, vp, vp, vp, vp]
+    lib.sb_adapt_push.restype = C.c_int
+    lib.sb_head_update.argtypes = [vp, vp, vp, vp, C.c_float, C.c_float, vp,
+                                   vp]
+    lib.sb_head_update.restype = C.c_int
     lib.sb_set_bucket_override.argtypes = [vp, vp]
     lib.sb_set_bucket_override.restype = C.c_int
     lib.sb_profile.argtypes = [vp, i32]

@@ -15,7 +15,8 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libspecblock.so")
 SOURCES = ["gemm.hip", "elementwise.hip", "attention.hip", "vocab.hip",
-           "tree.hip", "sampling.hip", "engine.hip"]
+           "tree.hip", "sampling.hip", "adapt.hip",
+           "engine.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17",
          # packed fp32 VALU forms are kept out of the generated code

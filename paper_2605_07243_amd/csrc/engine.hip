@@ -38,6 +38,7 @@ struct Dims {
   int S, d, H, Hkv, hd, F, V, Vd, L, LD, qkv_n, es;
   int K, M, B_max, budget, row_cap, rw, bw, vis_words, R_cap, chunk;
   int tpages, dpages, n_chunks, n_chunks_d, n_split;
+  int adapt_cap;
   size_t part_elems;
 };
 
@@ -70,6 +71,7 @@ Dims derive(const sb_config& c) {
   D.dpages = ceil_div(std::max(D.row_cap, D.chunk), 16);
   D.n_chunks = std::max(1, std::min(64, D.V / 2048));
   D.n_chunks_d = std::max(1, std::min(64, D.Vd / 2048));
+  D.adapt_cap = c.adapt_cap;
   D.n_split = 32;
   // partial-sum buffer: the largest ks * N over the projections
   size_t mx = 0;
@@ -87,6 +89,18 @@ Dims derive(const sb_config& c) {
 }
 
 }  // namespace
+
+struct AdaptBufs {
+  void* A;        // [adapt_cap][d] elem: LM-head operands
+  float* Z;       // [adapt_cap][Vd] training-head logits, then gradients
+  float* Z0;      // [adapt_cap][Vd] pre-deployment-head logits
+  float* part;    // vocabulary chunk records of Z (top-10)
+  float* part0;   // vocabulary chunk records of Z0 (top-1)
+  float* psi;     // [adapt_cap][15]
+  float* ds;      // [adapt_cap][4] rank-head score gradients
+  float* loss;    // [adapt_cap]
+  int* n;         // positions in this update
+};
 
 struct sb_ctx {
   sb_config cfg{};
@@ -108,6 +122,7 @@ struct sb_ctx {
   float* logits = nullptr;
   float2* node_stats = nullptr;  // [S][budget][tiles] softmax stats of z / T
   float* row_lse = nullptr;      // [S][row_cap] drafter rows' log-sum-exp
+  AdaptBufs ad{};                // head-update workspace
   float* vpart = nullptr;
   float* cond_buf = nullptr;
   float* taps_pf = nullptr;
@@ -168,6 +183,18 @@ static size_t layout(const Dims& D, void* base, sb_ctx* c) {
   float* ml = cv.take<float>((size_t)D.n_split * R * D.H * 2 * 4);
   float* logits = cv.take<float>(R * D.V * 4);
   float* row_lse = cv.take<float>((size_t)D.S * D.row_cap * 4);
+  // head-update region (its own buffers: the update may run on another
+  // stream while inference uses the ones above)
+  const size_t ac = (size_t)D.adapt_cap;
+  void* ad_A = cv.take<char>(ac * D.d * es);
+  float* ad_Z = cv.take<float>(ac * D.Vd * 4);
+  float* ad_Z0 = cv.take<float>(ac * D.Vd * 4);
+  float* ad_part = cv.take<float>(ac * D.n_chunks_d * kVocabRec10 * 4);
+  float* ad_part0 = cv.take<float>(ac * D.n_chunks_d * 5 * 4);
+  float* ad_psi = cv.take<float>(ac * SB_PSI_DIM * 4);
+  float* ad_ds = cv.take<float>(ac * 4 * 4);
+  float* ad_loss = cv.take<float>(ac * 4);
+  int* ad_n = cv.take<int>(4);
   float2* node_stats = cv.take<float2>((size_t)D.S * D.budget *
                                        sample_tiles(D.V) * 8);
   float* vpart = cv.take<float>(R * D.n_chunks * kVocabRec10 * 4);
@@ -221,6 +248,8 @@ static size_t layout(const Dims& D, void* base, sb_ctx* c) {
     c->logits = logits;
     c->node_stats = node_stats;
     c->row_lse = row_lse;
+    c->ad = AdaptBufs{ad_A, ad_Z, ad_Z0, ad_part, ad_part0, ad_psi, ad_ds,
+                      ad_loss, ad_n};
     c->vpart = vpart;
     c->cond_buf = cond_buf;
     c->taps_pf = taps_pf;
@@ -273,6 +302,19 @@ static int validate_cfg(const sb_config* c, std::string& msg) {
   if (t.vocab % 16 || ((t.n_heads + 2 * t.n_kv_heads) * t.head_dim) % 16) {
     msg = "vocab and the QKV width must be multiples of 16";
     return SB_ESHAPE;
+  }
+  if (c->adapt_cap < 0 || c->adapt_cap > 64) {
+    msg = "adapt_cap must be in 0..64";
+    return SB_EINVAL;
+  }
+  if (c->adapt_cap > 0) {
+    const int vd = c->draft_vocab > 0 ? c->draft_vocab : t.vocab;
+    const int cw = sb::adapt_column_width(c->dtype == SB_BF16 ? 2 : 4);
+    if (vd % sb::adapt_stripe_rows() || t.d_model % cw) {
+      msg = "head updates need the drafter vocabulary % 64 == 0 and d_model % " +
+            std::to_string(cw) + " == 0";
+      return SB_ESHAPE;
+    }
   }
   if (c->draft_vocab != 0 &&
       (c->draft_vocab < SB_TOPK || c->draft_vocab > t.vocab ||
@@ -1020,6 +1062,93 @@ int sb_accept_sample(sb_ctx* c, int32_t n_seqs, const sb_tree* tree,
                        c->node_stats, u_accept, u_bonus, *out, st);
   reject_signal(c, n_seqs, *tree, *out, st);
   return hip_check(c, "sb_accept_sample");
+}
+
+int sb_adapt_push(sb_ctx* c, int32_t n_seqs, const sb_tree* tree,
+                  const sb_accept_out* acc, sb_adapt_buffer* buf,
+                  void* stream) {
+  int rc = check_common(c);
+  if (rc) return rc;
+  if (c->D.adapt_cap < 1)
+    return fail(c, SB_ESTATE, "head updates need cfg.adapt_cap >= 1");
+  if (n_seqs < 1 || n_seqs > c->cfg.max_seqs)
+    return fail(c, SB_ESHAPE, "n_seqs must be in 1..max_seqs");
+  if ((rc = check_tree(c, tree))) return rc;
+  if (!acc || bad_ptr(acc->path, 4) || bad_ptr(acc->n_accepted, 4) ||
+      bad_ptr(acc->bonus, 4))
+    return fail(c, SB_EINVAL, "accept out pointer NULL or misaligned");
+  if (!buf || bad_ptr(buf->h, 4) || bad_ptr(buf->target, 4) ||
+      bad_ptr(buf->count, 4))
+    return fail(c, SB_EINVAL, "adapt buffer pointer NULL or misaligned");
+  if (buf->cap != c->D.adapt_cap)
+    return fail(c, SB_ESHAPE, "adapt buffer cap differs from cfg.adapt_cap");
+  launch_adapt_push(tree_dims(c, n_seqs), *tree, *acc, buf->h, buf->target,
+                    buf->count, buf->cap, S_(stream));
+  return hip_check(c, "sb_adapt_push");
+}
+
+}  // extern "C"
+
+namespace {
+
+template <typename T>
+int head_update_impl(sb_ctx* c, sb_adapt_buffer* buf, const void* lm_head0,
+                     sb_head_weights* w, float lr, float kl_weight,
+                     float* loss_out, hipStream_t st) {
+  const Dims& D = c->D;
+  const AdaptBufs& a = c->ad;
+  const int cap = D.adapt_cap;
+  T* A = static_cast<T*>(a.A);
+  launch_adapt_prep<T>(buf->h, buf->count, cap,
+                       static_cast<const float*>(c->dw.final_norm),
+                       c->cfg.target.norm_eps, D.d, A, a.n, st);
+  launch_gemm_xwt<T>(A, D.d, static_cast<const T*>(w->lm_head), D.Vd, D.d,
+                     a.Z, (size_t)cap * D.Vd, a.n, cap, 1, st);
+  launch_gemm_xwt<T>(A, D.d, static_cast<const T*>(lm_head0), D.Vd, D.d, a.Z0,
+                     (size_t)cap * D.Vd, a.n, cap, 1, st);
+  launch_vocab_partial(a.Z, a.n, cap, D.Vd, D.n_chunks_d, SB_TOPK, a.part, st);
+  launch_vocab_partial(a.Z0, a.n, cap, D.Vd, D.n_chunks_d, 1, a.part0, st);
+  launch_adapt_rows(a.Z, a.Z0, D.Vd, a.part, a.part0, D.n_chunks_d, a.n, cap,
+                    buf->h, D.d, buf->target, c->dw.d2t, w->rank_w, w->rank_b,
+                    kl_weight, a.psi, a.ds, a.loss, st);
+  launch_lm_update<T>(static_cast<T*>(w->lm_head), D.Vd, D.d, a.Z, A, a.n, lr,
+                      st);
+  launch_rank_update(w->rank_w, w->rank_b, a.ds, buf->h, a.psi, D.d, a.n, lr,
+                     a.loss, loss_out, buf->count, st);
+  return hip_check(c, "sb_head_update");
+}
+
+}  // namespace
+
+extern "C" {
+
+int sb_head_update(sb_ctx* c, sb_adapt_buffer* buf, const void* lm_head0,
+                   sb_head_weights* train, float lr, float kl_weight,
+                   float* loss_out, void* stream) {
+  int rc = check_common(c);
+  if (rc) return rc;
+  if (c->D.adapt_cap < 1)
+    return fail(c, SB_ESTATE, "head updates need cfg.adapt_cap >= 1");
+  if (!buf || bad_ptr(buf->h, 4) || bad_ptr(buf->target, 4) ||
+      bad_ptr(buf->count, 4))
+    return fail(c, SB_EINVAL, "adapt buffer pointer NULL or misaligned");
+  if (buf->cap != c->D.adapt_cap)
+    return fail(c, SB_ESHAPE, "adapt buffer cap differs from cfg.adapt_cap");
+  if (!train || bad_ptr(train->lm_head, 16) || bad_ptr(train->rank_w, 4) ||
+      bad_ptr(train->rank_b, 4) || bad_ptr(lm_head0, 16) ||
+      (loss_out && bad_ptr(loss_out, 4)))
+    return fail(c, SB_EINVAL, "head weights NULL or misaligned");
+  if (train->lm_head == lm_head0 || train->lm_head == c->dw.lm_head)
+    return fail(c, SB_EINVAL,
+                "the training LM head must be its own copy (not the "
+                "pre-deployment or the bound one)");
+  if (!(lr >= 0.f) || !(kl_weight >= 0.f) || !(lr < 3.0e38f) ||
+      !(kl_weight < 3.0e38f))
+    return fail(c, SB_EINVAL, "lr and kl_weight must be finite and >= 0");
+  return is_bf16(c) ? head_update_impl<bf16_t>(c, buf, lm_head0, train, lr,
+                                                kl_weight, loss_out, S_(stream))
+                    : head_update_impl<float>(c, buf, lm_head0, train, lr,
+                                              kl_weight, loss_out, S_(stream));
 }
 
 int sb_commit(sb_ctx* c, sb_seqs* seqs, const sb_tree* tree,

@@ -197,6 +197,29 @@ void launch_reject_signal(const TreeDims& td, const sb_tree& t,
                           const T* lm_head, const float* gain, float eps,
                           const int* d2t, int Vd, float* r_out,
                           hipStream_t st);
+// Head-only drafter update (tree.hip push, vocab.hip rows, adapt.hip).
+void launch_adapt_push(const TreeDims& td, const sb_tree& t,
+                       const sb_accept_out& acc, float* buf_h, int* buf_y,
+                       int* count, int cap, hipStream_t st);
+void launch_adapt_rows(float* Z, const float* Z0, int Vd, const float* part,
+                       const float* part0, int n_chunks, const int* n_eff,
+                       int cap, const float* h, int d, const int* targets,
+                       const int* d2t, const float* rank_w,
+                       const float* rank_b, float kl_w, float* psi_out,
+                       float* ds_out, float* loss_out, hipStream_t st);
+template <typename T>
+void launch_adapt_prep(const float* h, const int* count, int cap,
+                       const float* g, float eps, int d, T* A, int* n_eff,
+                       hipStream_t st);
+template <typename T>
+void launch_lm_update(T* W, int Vd, int d, const float* G, const T* A,
+                      const int* n_eff, float lr, hipStream_t st);
+void launch_rank_update(float* rank_w, float* rank_b, const float* ds,
+                        const float* h, const float* psi, int d,
+                        const int* n_eff, float lr, const float* loss,
+                        float* loss_out, int* count, hipStream_t st);
+int adapt_column_width(int elem_bytes);
+int adapt_stripe_rows();
 // Stochastic acceptance (sampling.hip).
 int sample_tiles(int V);       // statistics tiles per node row
 int sample_max_vocab();

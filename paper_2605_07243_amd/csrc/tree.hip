@@ -675,6 +675,49 @@ void launch_accept(const TreeDims& td, const sb_tree& t, const int* argmax,
                    const sb_accept_out& o, hipStream_t st) {
   accept_kernel<<<td.S, 64, 0, st>>>(td, t, argmax, o);
 }
+// Adaptation buffer push (Sec. 3.4): each sequence's rejected position
+// (the one after its last accepted node) whose drafter row exists appends
+// (that row's cached h^(L), the bonus token) to the buffer, in sequence
+// order, while room is left.  One workgroup.
+__global__ __launch_bounds__(256) void adapt_push_kernel(
+    TreeDims td, sb_tree t, sb_accept_out acc, float* __restrict__ buf_h,
+    int* __restrict__ buf_y, int* __restrict__ count, int cap) {
+  __shared__ int slot[SB_MAX_SEQS], src[SB_MAX_SEQS];
+  const int path_cap = td.M * td.K;
+  if (threadIdx.x < td.S) {
+    const int s = threadIdx.x;
+    const int a = acc.n_accepted[s];
+    const int cur = a > 0 ? acc.path[(size_t)s * path_cap + a - 1] : 0;
+    src[s] = continuing_row(td, t, s, cur);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int c = *count;
+    for (int s = 0; s < td.S; ++s) {
+      slot[s] = (src[s] >= 0 && c < cap) ? c : -1;
+      if (slot[s] >= 0) {
+        buf_y[slot[s]] = acc.bonus[s];
+        ++c;
+      }
+    }
+    *count = c;
+  }
+  __syncthreads();
+  const int d = td.d;
+  for (int s = 0; s < td.S; ++s) {
+    if (slot[s] < 0) continue;
+    const float* hs = t.h_last + ((size_t)s * td.row_cap + src[s]) * d;
+    float* hd = buf_h + (size_t)slot[s] * d;
+    for (int k = threadIdx.x; k < d; k += 256) hd[k] = hs[k];
+  }
+}
+
+void launch_adapt_push(const TreeDims& td, const sb_tree& t,
+                       const sb_accept_out& acc, float* buf_h, int* buf_y,
+                       int* count, int cap, hipStream_t st) {
+  adapt_push_kernel<<<1, 256, 0, st>>>(td, t, acc, buf_h, buf_y, count, cap);
+}
+
 template <typename T>
 void launch_reject_signal(const TreeDims& td, const sb_tree& t,
                           const sb_accept_out& acc, const float* row_lse,

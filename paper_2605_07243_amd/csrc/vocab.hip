@@ -316,4 +316,138 @@ void launch_verify_finalize(const float* part, int n_chunks, const int* n,
                                              argmax);
 }
 
+// Head-only drafter update (Sec. 3.4), one workgroup per buffered position
+// i: the drafter distribution p = softmax(z), z = W_train a (chunk records
+// part), and p0 = softmax(z0), z0 = W_0 a (records part0); psi of p; the
+// target's drafter id and rank in p, whose bucket is the rank-head label
+// (past rank 10, or outside the drafter vocabulary: b3); KL(p || p0); the
+// LM-logit gradient (1/n) [(p - e_y) + kl_w p (log p - log p0 - KL)]
+// written over z; the rank-head score gradient
+// ds = (1/n) (softmax(W_r [h, psi] + b_r) - e_label); the position's loss.
+__global__ __launch_bounds__(256) void adapt_row_kernel(
+    float* __restrict__ Z, const float* __restrict__ Z0, int Vd,
+    const float* __restrict__ part, const float* __restrict__ part0,
+    int n_chunks, const int* __restrict__ n_eff, const float* __restrict__ h,
+    int d, const int* __restrict__ targets, const int* __restrict__ d2t,
+    const float* __restrict__ rank_w, const float* __restrict__ rank_b,
+    float kl_w, float* __restrict__ psi_out, float* __restrict__ ds_out,
+    float* __restrict__ loss_out) {
+  __shared__ float psi_s[SB_PSI];
+  __shared__ float red[4];
+  __shared__ float sh_lse, sh_lse0, sh_zy;
+  __shared__ int sh_y;
+  const int i = blockIdx.x;
+  const int n = *n_eff;
+  if (i >= n) return;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  float* z = Z + (size_t)i * Vd;
+  const float* z0 = Z0 + (size_t)i * Vd;
+  if (tid < 64) {
+    float bv[SB_TOPK_K];
+    int bi[SB_TOPK_K];
+    float M, S, U;
+    merge_row<SB_TOPK_K>(part + (size_t)i * n_chunks * (2 * SB_TOPK_K + 3),
+                         n_chunks, bv, bi, M, S, U);
+    float bv0[1];
+    int bi0[1];
+    float M0, S0, U0;
+    merge_row<1>(part0 + (size_t)i * n_chunks * 5, n_chunks, bv0, bi0, M0, S0,
+                 U0);
+    if (tid == 0) {
+      const float lse = M + logf(S);
+      for (int k = 0; k < SB_TOPK_K; ++k) psi_s[k] = bv[k] - lse;
+      psi_s[10] = bv[0] - bv[1];
+      psi_s[11] = bv[0] - bv[2];
+      psi_s[12] = bv[0] - bv[4];
+      psi_s[13] = __expf(bv[0] - lse);
+      psi_s[14] = lse - U / S;
+      sh_lse = lse;
+      sh_lse0 = M0 + logf(S0);
+      // the target's drafter id (d2t strictly increasing), -1 if absent
+      const int t = targets[i];
+      int y = -1;
+      if (d2t == nullptr) {
+        y = (t >= 0 && t < Vd) ? t : -1;
+      } else {
+        int lo = 0, hi = Vd - 1;
+        while (lo <= hi) {
+          const int mid = (lo + hi) >> 1;
+          const int v = d2t[mid];
+          if (v == t) {
+            y = mid;
+            break;
+          }
+          if (v < t) lo = mid + 1;
+          else hi = mid - 1;
+        }
+      }
+      sh_y = y;
+      sh_zy = y >= 0 ? z[y] : 0.f;
+    }
+  }
+  __syncthreads();
+  const float lse = sh_lse, lse0 = sh_lse0, zy = sh_zy;
+  const int y = sh_y;
+  // pass 1: KL(p || p0) and the target's rank
+  float kl = 0.f, above = 0.f;
+  for (int v = tid; v < Vd; v += 256) {
+    const float zv = z[v];
+    const float lp = zv - lse, lp0 = z0[v] - lse0;
+    kl += __expf(lp) * (lp - lp0);
+    if (y >= 0 && (zv > zy || (zv == zy && v < y))) above += 1.f;
+  }
+  kl = block_sum(kl, red);
+  above = block_sum(above, red);
+  const float inv_n = 1.0f / (float)n;
+  // pass 2: the LM-logit gradient over z
+  for (int v = tid; v < Vd; v += 256) {
+    const float lp = z[v] - lse, lp0 = z0[v] - lse0;
+    const float p = __expf(lp);
+    // no cross-entropy term (and so no p term) for a target outside the
+    // drafter vocabulary
+    float g = y >= 0 ? p - (v == y ? 1.f : 0.f) : 0.f;
+    g += kl_w * p * (lp - lp0 - kl);
+    z[v] = g * inv_n;
+  }
+  // rank head over [h, psi]
+  const float* hr = h + (size_t)i * d;
+  const int ld = d + SB_PSI;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int j = tid; j < ld; j += 256) {
+    const float x = j < d ? hr[j] : psi_s[j - d];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[b] += rank_w[(size_t)b * ld + j] * x;
+  }
+  float sc[4];
+#pragma unroll
+  for (int b = 0; b < 4; ++b) sc[b] = block_sum(acc[b], red) + rank_b[b];
+  if (tid == 0) {
+    const int r = (int)above + 1;
+    const int label = y < 0 ? 3 : (r == 1 ? 0 : r <= 4 ? 1 : r <= 10 ? 2 : 3);
+    const float mx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
+    float se = 0.f;
+    for (int b = 0; b < 4; ++b) se += __expf(sc[b] - mx);
+    const float lsr = mx + logf(se);
+    for (int b = 0; b < 4; ++b)
+      ds_out[(size_t)i * 4 + b] =
+          (__expf(sc[b] - lsr) - (b == label ? 1.f : 0.f)) * inv_n;
+    for (int k = 0; k < SB_PSI; ++k) psi_out[(size_t)i * SB_PSI + k] = psi_s[k];
+    float loss = kl_w * kl - (sc[label] - lsr);
+    if (y >= 0) loss -= zy - lse;
+    loss_out[i] = loss;
+  }
+}
+
+void launch_adapt_rows(float* Z, const float* Z0, int Vd, const float* part,
+                       const float* part0, int n_chunks, const int* n_eff,
+                       int cap, const float* h, int d, const int* targets,
+                       const int* d2t, const float* rank_w,
+                       const float* rank_b, float kl_w, float* psi_out,
+                       float* ds_out, float* loss_out, hipStream_t st) {
+  adapt_row_kernel<<<cap, 256, 0, st>>>(Z, Z0, Vd, part, part0, n_chunks,
+                                        n_eff, h, d, targets, d2t, rank_w,
+                                        rank_b, kl_w, psi_out, ds_out,
+                                        loss_out);
+}
+
 }  // namespace sb

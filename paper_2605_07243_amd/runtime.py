@@ -45,7 +45,8 @@ class Runtime:
     """
 
     def __init__(self, w, weights=None, *, n_seqs=None, max_pages=None,
-                 prefill_chunk=128, device="cuda", page_seed=3, seed=0):
+                 prefill_chunk=128, device="cuda", page_seed=3, seed=0,
+                 adapt_cap=0):
         self.lib = B.load()
         self.w = w
         self.dev = torch.device(device)
@@ -69,6 +70,7 @@ class Runtime:
         cfg.max_pages = max_pages
         cfg.prefill_chunk = prefill_chunk
         cfg.draft_vocab = w.draft_vocab
+        cfg.adapt_cap = adapt_cap
         self.cfg = cfg
         ctx = C.c_void_p()
         rc = self.lib.sb_create(C.byref(cfg), C.byref(ctx))
@@ -334,6 +336,38 @@ class Runtime:
         """Bound of T over all sequences (0: unknown); needed after writing
         T or the caches directly."""
         self._check(self.lib.sb_set_length_bound(self.ctx, int(max_T)))
+
+    # ---- head-only adaptation ----------------------------------------
+    def adapt_buffer(self):
+        """Device buffer for sb_adapt_push / sb_head_update."""
+        cap = self.cfg.adapt_cap
+        b = dict(h=torch.zeros(cap, self.w.target.d_model, dtype=torch.float32,
+                               device=self.dev),
+                 target=torch.zeros(cap, dtype=torch.int32, device=self.dev),
+                 count=torch.zeros(1, dtype=torch.int32, device=self.dev))
+        b["c"] = B.AdaptBuffer(_ptr(b["h"]), _ptr(b["target"]),
+                               _ptr(b["count"]), cap)
+        return b
+
+    def head_copy(self):
+        """A training copy of the drafter's LM head and rank head."""
+        dt = self._keep[4]
+        return dict(lm_head=dt["lm_head"].clone(), rank_w=dt["rank_w"].clone(),
+                    rank_b=dt["rank_b"].clone())
+
+    def adapt_push(self, buf):
+        self._check(self.lib.sb_adapt_push(
+            self.ctx, self.S, C.byref(self.tree_c), C.byref(self.aout_c),
+            C.byref(buf["c"]), self.stream))
+
+    def head_update(self, buf, lm_head0, train, lr, kl_weight, loss=None,
+                    stream=None):
+        hw = B.HeadWeights(_ptr(train["lm_head"]), _ptr(train["rank_w"]),
+                           _ptr(train["rank_b"]))
+        st = self.stream if stream is None else C.c_void_p(stream.cuda_stream)
+        self._check(self.lib.sb_head_update(
+            self.ctx, C.byref(buf["c"]), _ptr(lm_head0), C.byref(hw),
+            float(lr), float(kl_weight), _ptr(loss), st))
 
     def set_buckets(self, buckets):
         """Force the drafter rows' buckets from a device int32 tensor

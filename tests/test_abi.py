@@ -77,6 +77,10 @@ def cfg(**kw):
     (dict(draft_vocab=1040), B.SB_ESHAPE),
     (dict(draft_vocab=1000), B.SB_ESHAPE),
     (dict(dtype=B.SB_BF16, draft_vocab=528), B.SB_ESHAPE),
+    # head updates: at most 64 positions; drafter vocabulary % 64, d % CW
+    (dict(adapt_cap=65), B.SB_EINVAL),
+    (dict(adapt_cap=-1), B.SB_EINVAL),
+    (dict(adapt_cap=8, draft_vocab=528), B.SB_ESHAPE),
 ])
 def test_create_rejects_bad_configs(lib, kw, code):
     c = cfg(**kw)
@@ -257,7 +261,9 @@ def test_struct_layouts_match_header(tmp_path):
                "sb_drafter_weights": B.DrafterWeights, "sb_kv": B.KV,
                "sb_seqs": B.Seqs, "sb_tree": B.Tree, "sb_draft_out": B.DraftOut,
                "sb_verify_out": B.VerifyOut, "sb_accept_out": B.AcceptOut,
-               "sb_kernel_stat": B.KernelStat}
+               "sb_kernel_stat": B.KernelStat,
+               "sb_adapt_buffer": B.AdaptBuffer,
+               "sb_head_weights": B.HeadWeights}
     lines = ['#include <stdio.h>', '#include <stddef.h>',
              f'#include "{HEADER}"', 'int main(void) {']
     for cname, py in structs.items():
@@ -298,3 +304,50 @@ def test_accept_sample_validation(bound):
     assert call(o=B.AcceptOut(f.at(), f.at(), f.at(), f.at(2))) == B.SB_EINVAL
     assert call(n=0) == B.SB_ESHAPE
     assert call(n=2) == B.SB_ESHAPE
+
+
+def test_adaptation_validation(bound):
+    lib, ctx, f = bound
+    tree = _tree(f)
+    acc = B.AcceptOut(f.at(), f.at(), f.at())
+    buf = B.AdaptBuffer(f.at(), f.at(), f.at(), 8)
+    hw = B.HeadWeights(f.at(256), f.at(), f.at())
+    # the bound context has adapt_cap 0
+    assert lib.sb_adapt_push(ctx, 1, C.byref(tree), C.byref(acc),
+                             C.byref(buf), None) == B.SB_ESTATE
+    assert lib.sb_head_update(ctx, C.byref(buf), f.at(512), C.byref(hw), 0.1,
+                              0.01, None, None) == B.SB_ESTATE
+    assert b"adapt_cap" in lib.sb_last_error(ctx)
+
+
+def test_adaptation_argument_checks(lib):
+    c = cfg(adapt_cap=8)
+    ctx = C.c_void_p()
+    assert lib.sb_create(C.byref(c), C.byref(ctx)) == B.SB_OK
+    f = Fake()
+    layers = (B.LayerWeights * 2)(*[B.LayerWeights(*[f.at()] * 6, None)
+                                    for _ in range(2)])
+    dl = (B.LayerWeights * 1)(B.LayerWeights(*[f.at()] * 7))
+    tw = B.TargetWeights(f.at(), layers, f.at(), f.at())
+    dw = B.DrafterWeights(*([f.at()] * 6), dl, *([f.at()] * 4), None)
+    need = lib.sb_workspace_bytes(C.byref(c))
+    ws = (C.c_char * (need + 512))()
+    wp = C.c_void_p((C.addressof(ws) + 255) & ~255)
+    assert lib.sb_bind(ctx, C.byref(tw), C.byref(dw), wp, need) == B.SB_OK
+    tree = _tree(f)
+    acc = B.AcceptOut(f.at(), f.at(), f.at())
+    ok_buf = B.AdaptBuffer(f.at(), f.at(), f.at(), 8)
+    push = lambda n=1, b=ok_buf: lib.sb_adapt_push(  # noqa: E731
+        ctx, n, C.byref(tree), C.byref(acc), C.byref(b), None)
+    assert push(b=B.AdaptBuffer(f.at(), f.at(), f.at(), 4)) == B.SB_ESHAPE
+    assert push(b=B.AdaptBuffer(f.at(), None, f.at(), 8)) == B.SB_EINVAL
+    assert push(n=0) == B.SB_ESHAPE
+    upd = lambda hw, lr=0.1, kl=0.01, w0=f.at(512): lib.sb_head_update(  # noqa
+        ctx, C.byref(ok_buf), w0, C.byref(hw), lr, kl, None, None)
+    good = B.HeadWeights(f.at(256), f.at(), f.at())
+    assert upd(good, lr=-1.0) == B.SB_EINVAL
+    assert upd(good, kl=float("nan")) == B.SB_EINVAL
+    assert upd(good, w0=f.at(256)) == B.SB_EINVAL       # same as train
+    assert upd(B.HeadWeights(f.at(), f.at(), f.at())) == B.SB_EINVAL  # bound
+    assert upd(B.HeadWeights(f.at(8), f.at(), f.at())) == B.SB_EINVAL
+    lib.sb_destroy(ctx)

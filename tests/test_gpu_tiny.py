@@ -23,7 +23,7 @@ def tiny():
     weights, tgt, dr = models(w)
     prompt = synth.prompts(w)[0]
     st = specdec.prefill(tgt, dr, prompt)
-    rt = runtime(w, weights, max_pages=32)
+    rt = runtime(w, weights, max_pages=32, adapt_cap=8)
     return w, tgt, dr, prompt, st, rt
 
 
@@ -116,6 +116,18 @@ def test_iteration_calls(tiny):
         assert rg == -1.0
     else:
         assert abs(rg - rr) <= 1e-3 * rr + 1e-9, (rg, rr)
+    # the adaptation buffer takes the rejected position's row and token
+    buf = rt.adapt_buffer()
+    rt.adapt_push(buf)
+    torch.cuda.synchronize()
+    cont = specdec.continuing_row(tree, rec["rows"], (rec["path"] or [0])[-1],
+                                  w.K)
+    if cont is None:
+        assert int(buf["count"][0]) == 0
+    else:
+        assert int(buf["count"][0]) == 1
+        assert int(buf["target"][0]) == rec["bonus"]
+        assert rel_err(host(buf["h"][0]), rec["rows"][cont].h_last) < TOL
     print("commit", flush=True)
     rt.commit()
     torch.cuda.synchronize()
