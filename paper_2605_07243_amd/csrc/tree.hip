@@ -649,20 +649,26 @@ __global__ __launch_bounds__(256) void reject_signal_kernel(
   __syncthreads();
   const float rs = 1.0f / sqrtf((red[0] + red[1] + red[2] + red[3]) / (float)d + eps);
   __syncthreads();
+  // eight consecutive columns per step: one 16-byte run of the packed
+  // (or row-major) LM-head row, all loads independent
   float z = 0.f;
-  for (int k = tid; k < d; k += 256) {
-    const float x = Elem<T>::to_f32(Elem<T>::from_f32(h[k] * rs * gain[k]));
+  for (int k0 = 8 * tid; k0 < d; k0 += 8 * 256) {
     size_t wi;
     if constexpr (sizeof(T) == 2) {
       // fragment-packed LM head (32-row x 64-column blocks)
-      const int c = k & 63;
+      const int c = k0 & 63;
       const int l = (id & 31) + 32 * (c >> 5);
-      wi = ((((size_t)(id >> 5) * (d >> 6) + (k >> 6)) * 4 + ((c & 31) >> 3)) *
-            512) + (size_t)l * 8 + (k & 7);
+      wi = ((((size_t)(id >> 5) * (d >> 6) + (k0 >> 6)) * 4 + ((c & 31) >> 3)) *
+            512) + (size_t)l * 8;
     } else {
-      wi = (size_t)id * d + k;
+      wi = (size_t)id * d + k0;
     }
-    z += Elem<T>::to_f32(lm_head[wi]) * x;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float x = Elem<T>::to_f32(
+          Elem<T>::from_f32(h[k0 + e] * rs * gain[k0 + e]));
+      z += Elem<T>::to_f32(lm_head[wi + e]) * x;
+    }
   }
   z = wave_sum(z);
   if (lane == 0) red[w] = z;
