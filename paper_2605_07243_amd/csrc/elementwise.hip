@@ -183,6 +183,14 @@ __global__ __launch_bounds__(1024) void residual_kernel(
   const int nv = d >> 2;
   float4 v[MAXV];
   float ss = 0.f;
+  // the norm gains are loaded with the partials (not after the reduction)
+  float4 gv[MAXV];
+#pragma unroll
+  for (int q = 0; q < MAXV; ++q) {
+    const int c = threadIdx.x + q * 1024;
+    gv[q] = (g != nullptr && c < nv) ? reinterpret_cast<const float4*>(g)[c]
+                                     : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
   if (nv > 1024) {
     // second column only where it exists (else a repeat of the first)
     const int c1 = threadIdx.x + 1024 < nv ? threadIdx.x + 1024 : threadIdx.x;
@@ -217,7 +225,7 @@ __global__ __launch_bounds__(1024) void residual_kernel(
   for (int q = 0; q < MAXV; ++q) {
     const int c = threadIdx.x + q * 1024;
     if (c < nv) {
-      const float4 gg = reinterpret_cast<const float4*>(g)[c];
+      const float4 gg = gv[q];
       store4<T>(o + 4 * c, make_float4(v[q].x * rs * gg.x, v[q].y * rs * gg.y,
                                        v[q].z * rs * gg.z, v[q].w * rs * gg.w));
     }

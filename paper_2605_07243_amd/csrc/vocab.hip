@@ -75,6 +75,24 @@ __device__ __forceinline__ void wave_topk(float (&tv)[KT], int (&ti)[KT],
   }
 }
 
+// One logit into the running (max, sum exp, sum exp * x) and the top-KT.
+template <int KT>
+__device__ __forceinline__ void vocab_step(float x, int j, float& m, float& s,
+                                           float& u, float (&tv)[KT],
+                                           int (&ti)[KT]) {
+  if (x > m) {
+    const float a = __expf(m - x);
+    s = s * a + 1.f;
+    u = u * a + x;
+    m = x;
+  } else {
+    const float ex = __expf(x - m);
+    s += ex;
+    u += ex * x;
+  }
+  topk_insert<KT>(tv, ti, x, j);
+}
+
 template <int KT>
 __global__ __launch_bounds__(256) void vocab_partial_kernel(
     const float* __restrict__ logits, const int* __restrict__ n, int V,
@@ -92,23 +110,33 @@ __global__ __launch_bounds__(256) void vocab_partial_kernel(
     ti[k] = 0x7FFFFFFF;
   }
   float m = -FLT_MAX, s = 0.f, u = 0.f;
-  // the next element's load is issued before the current one is processed
-  int j = v0 + threadIdx.x;
-  float xn = j < v1 ? z[j] : 0.f;
-  for (; j < v1; j += 256) {
-    const float x = xn;
-    if (j + 256 < v1) xn = z[j + 256];
-    if (x > m) {
-      const float a = __expf(m - x);
-      s = s * a + 1.f;
-      u = u * a + x;
-      m = x;
-    } else {
-      const float ex = __expf(x - m);
-      s += ex;
-      u += ex * x;
+  if constexpr (KT == 1) {
+    // the thread's elements j0, j0 + 256, ... in batches of eight whose
+    // loads are all issued before the batch is processed
+    for (int j0 = v0 + threadIdx.x; j0 < v1; j0 += 256 * 8) {
+      float xb[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int j = j0 + 256 * q;
+        xb[q] = j < v1 ? z[j] : 0.f;
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int j = j0 + 256 * q;
+        if (j >= v1) break;
+        vocab_step<KT>(xb[q], j, m, s, u, tv, ti);
+      }
     }
-    topk_insert<KT>(tv, ti, x, j);
+  } else {
+    // (eight unrolled top-10 insertions would not fit the registers): the
+    // next element's load is issued before the current one is processed
+    int j = v0 + threadIdx.x;
+    float xn = j < v1 ? z[j] : 0.f;
+    for (; j < v1; j += 256) {
+      const float x = xn;
+      if (j + 256 < v1) xn = z[j + 256];
+      vocab_step<KT>(x, j, m, s, u, tv, ti);
+    }
   }
   // block merge: stats via LDS, top-k wave by wave
   __shared__ float sm[4], ss[4], su[4];
@@ -214,12 +242,12 @@ __device__ __forceinline__ void merge_row(const float* __restrict__ part,
 // rank-head scores W_r [h^(L), psi] + b_r, bucket = argmax (ties low) or,
 // when forced buckets are given, the forced one; branch = map[bucket].
 // Also stores h^(L) into the tree's row cache.
-__global__ __launch_bounds__(256) void draft_finalize_kernel(
+__global__ __launch_bounds__(1024) void draft_finalize_kernel(
     const float* __restrict__ part, int n_chunks, CallPlan p,
     const float* __restrict__ x, const float* __restrict__ rank_w,
     const float* __restrict__ rank_b, int d, int4 bmap, DraftRowOut out) {
   __shared__ float psi_s[SB_PSI];
-  __shared__ float red[4][4];
+  __shared__ float red[16][4];
   const int i = blockIdx.x;
   if (i >= *p.n) return;
   const int o = p.out_row[i];
@@ -250,15 +278,31 @@ __global__ __launch_bounds__(256) void draft_finalize_kernel(
     }
   }
   __syncthreads();
+  // h^(L) part of the rank head: every load (the row and four rank-head
+  // rows, d <= 8192) issued before the row is stored into the tree's cache
+  constexpr int kMaxQ = 8;
   const float* xr = x + (size_t)i * d;
   float* hl = out.h_last + (size_t)o * d;
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
   const int ld = d + SB_PSI;
-  for (int j = threadIdx.x; j < d; j += blockDim.x) {
-    const float v = xr[j];
-    hl[j] = v;
+  float xv[kMaxQ];
+  float wv[4][kMaxQ];
 #pragma unroll
-    for (int b = 0; b < 4; ++b) acc[b] += rank_w[(size_t)b * ld + j] * v;
+  for (int q = 0; q < kMaxQ; ++q) {
+    const int j = threadIdx.x + 1024 * q;
+    const bool in = j < d;
+    xv[q] = in ? xr[j] : 0.f;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) wv[b][q] = in ? rank_w[(size_t)b * ld + j] : 0.f;
+  }
+#pragma unroll
+  for (int q = 0; q < kMaxQ; ++q)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[b] += wv[b][q] * xv[q];
+#pragma unroll
+  for (int q = 0; q < kMaxQ; ++q) {
+    const int j = threadIdx.x + 1024 * q;
+    if (j < d) hl[j] = xv[q];
   }
   if (threadIdx.x < SB_PSI) {
 #pragma unroll
@@ -276,7 +320,8 @@ __global__ __launch_bounds__(256) void draft_finalize_kernel(
     int best = 0;
     float bs = 0.f;
     for (int b = 0; b < 4; ++b) {
-      const float sc = red[0][b] + red[1][b] + red[2][b] + red[3][b] + rank_b[b];
+      float sc = rank_b[b];
+      for (int q = 0; q < 16; ++q) sc += red[q][b];
       if (b == 0 || sc > bs) {
         bs = sc;
         best = b;
@@ -293,7 +338,7 @@ void launch_draft_finalize(const float* part, int n_chunks, const CallPlan& p,
                            const float* x, const float* rank_w,
                            const float* rank_b, int d, int4 bmap,
                            DraftRowOut o, hipStream_t st) {
-  draft_finalize_kernel<<<p.cap, 256, 0, st>>>(part, n_chunks, p, x, rank_w,
+  draft_finalize_kernel<<<p.cap, 1024, 0, st>>>(part, n_chunks, p, x, rank_w,
                                                rank_b, d, bmap, o);
 }
 
