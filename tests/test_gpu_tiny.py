@@ -162,3 +162,48 @@ def test_lossless_loop(tiny):
         toks = host(rt.tree["token"][0])
         out += [int(toks[p]) for p in path] + [int(rt.aout["bonus"][0])]
     assert out[:24] == ref
+
+
+@pytest.mark.parametrize("temperature", [1.0, 0.25])
+def test_iteration_sampling(tiny, temperature):
+    """One whole iteration with stochastic verification on both sides (the
+    same float32 uniforms): drafting, verification logits, the walk, the
+    bonus draw and the commit.  The accepted path and bonus must be equal
+    where the oracle's decision margins exceed the float32 error (1e-4 for
+    the acceptance tests, 2e-6 of the residual mass for the draw); the
+    device state after the commit must then equal the oracle's."""
+    from oracle.sampling import accept_sample
+    w, tgt, dr, prompt, st0, rt = tiny
+    st = copy.deepcopy(st0)
+    inject(rt, 0, st)
+    rng = np.random.default_rng(int(temperature * 1000))
+    ua = rng.random((1, w.budget)).astype(np.float32)
+    ub = rng.random((1, w.budget)).astype(np.float32)
+    ref_state = copy.deepcopy(st)
+    rec = specdec.iteration(tgt, dr, ref_state, w,
+                            sampling=(temperature, ua[0].astype(np.float64),
+                                      ub[0].astype(np.float64)))
+    margins = accept_sample(rec["tree"], rec["verify_logits"], temperature,
+                            ua[0].astype(np.float64), ub[0].astype(np.float64))
+    assert margins["path"] == rec["path"] and margins["bonus"] == rec["bonus"]
+    for m in range(1, w.M + 1):
+        rt.expand(m)
+    rt.verify(want_logits=True)
+    rt.accept_sample(temperature, torch.as_tensor(ua).to(rt.dev),
+                     torch.as_tensor(ub).to(rt.dev))
+    torch.cuda.synchronize()
+    n = len(rec["tree"])
+    assert int(rt.tree["n_nodes"][0]) == n
+    assert list(host(rt.tree["token"][0, :n])) == \
+        [nd.token for nd in rec["tree"].nodes]
+    if margins["test_margin"] <= 1e-4 or margins["cdf_margin"] <= 2e-6:
+        pytest.skip(f"decision within float32 error (margins "
+                    f"{margins['test_margin']:.2e}, {margins['cdf_margin']:.2e})")
+    a = int(rt.aout["n_accepted"][0])
+    assert list(host(rt.aout["path"][0, :a])) == rec["path"]
+    assert int(rt.aout["bonus"][0]) == rec["bonus"]
+    rt.commit()
+    torch.cuda.synchronize()
+    assert int(rt.T[0]) == ref_state.T
+    assert int(rt.root[0]) == ref_state.root
+    assert rel_err(host(rt.cond_taps[0]), ref_state.cond_taps).max() < TOL
