@@ -753,6 +753,10 @@ AttnShape attn_shape(int rows_per_seq_cap, int G, int seq_heads, int es) {
   const int qtiles = (rows_per_seq_cap * G + 15) / 16;
   a.mfma32 = false;
   a.nq = qtiles >= 8 ? 8 : (qtiles >= 4 ? 4 : (qtiles >= 2 ? 2 : 1));
+  // bf16 with few pairs: at most four waves per workgroup (one per SIMD, so
+  // a split's tile chain is not shared with a second wave; twice the
+  // workgroups): 5% faster at 60 tree nodes, 12% at 128 (measured)
+  if (es == 2) a.nq = a.nq > 4 ? 4 : a.nq;
   a.qt = (qtiles > 8 && seq_heads >= 32) ? 2 : 1;  // 8 x 2 fits 256 VGPRs
   a.groups = (qtiles + a.nq * a.qt - 1) / (a.nq * a.qt);
   return a;
