@@ -69,8 +69,10 @@ Dims derive(const sb_config& c) {
                      std::max(D.chunk, D.S));
   D.tpages = ceil_div(std::max(D.budget, D.chunk), 16);
   D.dpages = ceil_div(std::max(D.row_cap, D.chunk), 16);
-  D.n_chunks = std::max(1, std::min(64, D.V / 2048));
-  D.n_chunks_d = std::max(1, std::min(64, D.Vd / 2048));
+  // record slots per row for the vocabulary reductions: up to 64 chunks,
+  // and always enough for chunks of at most 12288 logits
+  D.n_chunks = std::max({1, std::min(64, D.V / 2048), (D.V + 12287) / 12288});
+  D.n_chunks_d = std::max({1, std::min(64, D.Vd / 2048), (D.Vd + 12287) / 12288});
   D.adapt_cap = c.adapt_cap;
   D.n_split = 32;
   // partial-sum buffer: the largest ks * N over the projections
@@ -803,14 +805,15 @@ int draft_expand_impl(sb_ctx* c, int m, const sb_seqs* sq, const sb_kv* dkv,
   lm_head<T>(c, c->A, c->dw.lm_head, D.Vd, logits, p.n, p.cap, st);
   {
     ProfScope ps(c, st, SB_PROF_VOCAB);
-    launch_vocab_partial(logits, p.n, p.cap, D.Vd, D.n_chunks_d, SB_TOPK,
-                         c->vpart, st);
+    const int n_chunks = launch_vocab_partial(logits, p.n, p.cap, D.Vd,
+                                              D.n_chunks_d, SB_TOPK, c->vpart,
+                                              st);
     const DraftRowOut ro{o->topk_id, o->topk_logit, o->lse, o->psi,
                          o->bucket, o->branch, t->h_last, c->bucket_in,
                          c->dw.d2t, c->row_lse, D.Vd, D.row_cap};
     const int4 bmap = make_int4(c->cfg.branch_map[0], c->cfg.branch_map[1],
                                 c->cfg.branch_map[2], c->cfg.branch_map[3]);
-    launch_draft_finalize(c->vpart, D.n_chunks_d, p, c->x,
+    launch_draft_finalize(c->vpart, n_chunks, p, c->x,
                           static_cast<const float*>(c->dw.rank_w),
                           static_cast<const float*>(c->dw.rank_b), D.d, bmap,
                           ro, st);
@@ -834,8 +837,9 @@ int verify_impl(sb_ctx* c, const sb_seqs* sq, const sb_tree* t,
   lm_head<T>(c, c->A, c->tw.lm_head, D.V, logits, p.n, p.cap, st);
   {
     ProfScope ps(c, st, SB_PROF_VOCAB);
-    launch_vocab_partial(logits, p.n, p.cap, D.V, D.n_chunks, 1, c->vpart, st);
-    launch_verify_finalize(c->vpart, D.n_chunks, p.n, p.cap, p.out_row,
+    const int n_chunks =
+        launch_vocab_partial(logits, p.n, p.cap, D.V, D.n_chunks, 1, c->vpart, st);
+    launch_verify_finalize(c->vpart, n_chunks, p.n, p.cap, p.out_row,
                            out->argmax, st);
   }
   return hip_check(c, "sb_tree_verify");
@@ -899,9 +903,9 @@ int prefill_impl(sb_ctx* c, const sb_seqs* sq, const int32_t* prompt, int ld,
       if (a + n == len) {
         const T* last = static_cast<const T*>(c->A) + (size_t)(n - 1) * D.d;
         lm_head<T>(c, last, c->tw.lm_head, D.V, c->logits, c->one, 1, st);
-        launch_vocab_partial(c->logits, c->one, 1, D.V, D.n_chunks, 1,
-                             c->vpart, st);
-        launch_verify_finalize(c->vpart, D.n_chunks, c->one, 1, c->zero,
+        const int n_chunks = launch_vocab_partial(
+            c->logits, c->one, 1, D.V, D.n_chunks, 1, c->vpart, st);
+        launch_verify_finalize(c->vpart, n_chunks, c->one, 1, c->zero,
                                c->root_arg, st);
       }
       launch_plan_prefill_draft(S, s, a, n, prompt, ld, p, c->n_aux, st);
@@ -1106,9 +1110,10 @@ int head_update_impl(sb_ctx* c, sb_adapt_buffer* buf, const void* lm_head0,
                      a.Z, (size_t)cap * D.Vd, a.n, cap, 1, st);
   launch_gemm_xwt<T>(A, D.d, static_cast<const T*>(lm_head0), D.Vd, D.d, a.Z0,
                      (size_t)cap * D.Vd, a.n, cap, 1, st);
-  launch_vocab_partial(a.Z, a.n, cap, D.Vd, D.n_chunks_d, SB_TOPK, a.part, st);
+  const int n_chunks = launch_vocab_partial(a.Z, a.n, cap, D.Vd, D.n_chunks_d,
+                                            SB_TOPK, a.part, st);
   launch_vocab_partial(a.Z0, a.n, cap, D.Vd, D.n_chunks_d, 1, a.part0, st);
-  launch_adapt_rows(a.Z, a.Z0, D.Vd, a.part, a.part0, D.n_chunks_d, a.n, cap,
+  launch_adapt_rows(a.Z, a.Z0, D.Vd, a.part, a.part0, n_chunks, a.n, cap,
                     buf->h, D.d, buf->target, c->dw.d2t, w->rank_w, w->rank_b,
                     kl_weight, a.psi, a.ds, a.loss, st);
   launch_lm_update<T>(static_cast<T*>(w->lm_head), D.Vd, D.d, a.Z, A, a.n, lr,

@@ -130,9 +130,10 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
 int attn_qgroups(int rows_per_seq_cap, int G, int seq_heads, int es);
 
 // Vocabulary reductions over fp32 logits [cap][V].
-void launch_vocab_partial(const float* logits, const int* n, int cap, int V,
-                          int n_chunks, int topk, float* part,
-                          hipStream_t st);
+// Returns the number of chunk records written per row (<= max_chunks).
+int launch_vocab_partial(const float* logits, const int* n, int cap, int V,
+                         int max_chunks, int topk, float* part,
+                         hipStream_t st);
 struct DraftRowOut {
   int* topk_id;
   float* topk_logit;

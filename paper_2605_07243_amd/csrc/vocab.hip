@@ -4,6 +4,8 @@
 // drafter rows, or the greedy argmax for verified nodes.
 #include <float.h>
 
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -75,24 +77,20 @@ __device__ __forceinline__ void wave_topk(float (&tv)[KT], int (&ti)[KT],
   }
 }
 
-// One logit into the running (max, sum exp, sum exp * x) and the top-KT.
-template <int KT>
-__device__ __forceinline__ void vocab_step(float x, int j, float& m, float& s,
-                                           float& u, float (&tv)[KT],
-                                           int (&ti)[KT]) {
-  if (x > m) {
-    const float a = __expf(m - x);
-    s = s * a + 1.f;
-    u = u * a + x;
-    m = x;
-  } else {
-    const float ex = __expf(x - m);
-    s += ex;
-    u += ex * x;
-  }
-  topk_insert<KT>(tv, ti, x, j);
-}
+// Candidate list of the threshold filter (values, ids) per workgroup.
+constexpr int kCandCap = 256;
 
+// Partial record of one (row, chunk).  The chunk is staged in LDS with
+// coalesced 16-byte loads; a thread owns elements v0 + tid, v0 + tid + 256,
+// ... .  Pass 1 takes each thread's maximum (and, for KT = 1, its first
+// arg-max); pass 2 sums exp(z - max) and exp(z - max) z against that maximum
+// and, for KT > 1, collects the candidates z >= T, where T is a lower bound
+// of the chunk's KT-th largest logit: in each wave, the KT-th largest
+// distinct value among the 64 thread maxima (KT of the wave's logits are at
+// least that large), the largest over the waves.  The candidates, usually a
+// dozen or two, are ordered by rank (value, then smaller id); a chunk with
+// more than kCandCap candidates (many equal logits) falls back to per-thread
+// sorted lists merged wave by wave.
 template <int KT>
 __global__ __launch_bounds__(256) void vocab_partial_kernel(
     const float* __restrict__ logits, const int* __restrict__ n, int V,
@@ -102,104 +100,180 @@ __global__ __launch_bounds__(256) void vocab_partial_kernel(
   const int c = blockIdx.x;
   const int v0 = c * chunk, v1 = min(V, v0 + chunk);
   const float* z = logits + (size_t)i * V;
-  float tv[KT];
-  int ti[KT];
-#pragma unroll
-  for (int k = 0; k < KT; ++k) {
-    tv[k] = -FLT_MAX;
-    ti[k] = 0x7FFFFFFF;
-  }
-  float m = -FLT_MAX, s = 0.f, u = 0.f;
-  if constexpr (KT == 1) {
-    // the thread's elements j0, j0 + 256, ... in batches of eight whose
-    // loads are all issued before the batch is processed
-    for (int j0 = v0 + threadIdx.x; j0 < v1; j0 += 256 * 8) {
-      float xb[8];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const int j = j0 + 256 * q;
-        xb[q] = j < v1 ? z[j] : 0.f;
-      }
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const int j = j0 + 256 * q;
-        if (j >= v1) break;
-        vocab_step<KT>(xb[q], j, m, s, u, tv, ti);
-      }
-    }
-  } else {
-    // (eight unrolled top-10 insertions would not fit the registers): the
-    // next element's load is issued before the current one is processed
-    int j = v0 + threadIdx.x;
-    float xn = j < v1 ? z[j] : 0.f;
-    for (; j < v1; j += 256) {
-      const float x = xn;
-      if (j + 256 < v1) xn = z[j + 256];
-      vocab_step<KT>(x, j, m, s, u, tv, ti);
-    }
-  }
-  // block merge: stats via LDS, top-k wave by wave
-  __shared__ float sm[4], ss[4], su[4];
-  __shared__ float cv[4][KT];
-  __shared__ int ci[4][KT];
+  extern __shared__ float zs[];
+  __shared__ float sm[4], ss[4], su[4], thr[4];
+  __shared__ float cv[kCandCap], ov[4][KT];
+  __shared__ int ci[kCandCap], oi[4][KT];
+  __shared__ int n_cand;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (threadIdx.x == 0) n_cand = 0;
+  const int nvec = v1 > v0 ? (v1 - v0) >> 2 : 0;
+#pragma unroll 8
+  for (int e = threadIdx.x; e < nvec; e += 256)
+    reinterpret_cast<float4*>(zs)[e] =
+        *reinterpret_cast<const float4*>(z + v0 + 4 * e);
+  __syncthreads();
+  float mx = -FLT_MAX;
+  int mi = 0x7FFFFFFF;
+  for (int j = v0 + threadIdx.x; j < v1; j += 256) {
+    const float x = zs[j - v0];
+    if (x > mx) {
+      mx = x;
+      mi = j;
+    }
+  }
+  float tb = -FLT_MAX;
+  if constexpr (KT > 1) {
+    // KT-th distinct value among the wave's thread maxima
+    float v = mx, t = -FLT_MAX;
+#pragma unroll
+    for (int k = 0; k < KT; ++k) {
+      float b = v;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) b = fmaxf(b, __shfl_xor(b, o, SB_WAVE));
+      t = b;
+      if (v == b) v = -INFINITY;
+    }
+    if (lane == 0) thr[w] = t;
+    __syncthreads();
+    tb = fmaxf(fmaxf(fmaxf(thr[0], thr[1]), fmaxf(thr[2], thr[3])), -FLT_MAX);
+  }
+  float s = 0.f, u = 0.f;
+  for (int j = v0 + threadIdx.x; j < v1; j += 256) {
+    const float x = zs[j - v0];
+    const float e = __expf(x - mx);
+    s += e;
+    u = fmaf(e, x, u);
+    if constexpr (KT > 1) {
+      if (x >= tb) {
+        const int q = atomicAdd(&n_cand, 1);
+        if (q < kCandCap) {
+          cv[q] = x;
+          ci[q] = j;
+        }
+      }
+    }
+  }
+  const float m = mx;
+  float M = m, S = s, U = u;
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
-    const float m2 = __shfl_xor(m, o, SB_WAVE);
-    const float s2 = __shfl_xor(s, o, SB_WAVE);
-    const float u2 = __shfl_xor(u, o, SB_WAVE);
-    stats_merge(m, s, u, m2, s2, u2);
+    const float m2 = __shfl_xor(M, o, SB_WAVE);
+    const float s2 = __shfl_xor(S, o, SB_WAVE);
+    const float u2 = __shfl_xor(U, o, SB_WAVE);
+    stats_merge(M, S, U, m2, s2, u2);
   }
-  float bv[KT];
-  int bi[KT];
-  wave_topk<KT>(tv, ti, bv, bi);
   if (lane == 0) {
-    sm[w] = m;
-    ss[w] = s;
-    su[w] = u;
-#pragma unroll
-    for (int k = 0; k < KT; ++k) {
-      cv[w][k] = bv[k];
-      ci[w][k] = bi[k];
-    }
+    sm[w] = M;
+    ss[w] = S;
+    su[w] = U;
   }
-  __syncthreads();
-  if (w == 0) {
-    // lanes 0..3 hold the four waves' sorted lists
-    float lv[KT];
-    int li[KT];
-#pragma unroll
-    for (int k = 0; k < KT; ++k) {
-      lv[k] = lane < 4 ? cv[lane][k] : -FLT_MAX;
-      li[k] = lane < 4 ? ci[lane][k] : 0x7FFFFFFF;
-    }
-    wave_topk<KT>(lv, li, bv, bi);
+  float* rec = part + ((size_t)i * gridDim.x + c) * (2 * KT + 3);
+  if constexpr (KT == 1) {
+    float bv[1] = {mx};
+    int bi[1] = {mi};
+    wave_best(bv[0], bi[0]);
     if (lane == 0) {
-      float M = sm[0], S = ss[0], U = su[0];
-      for (int q = 1; q < 4; ++q) stats_merge(M, S, U, sm[q], ss[q], su[q]);
-      float* o = part + ((size_t)i * gridDim.x + c) * (2 * KT + 3);
+      ov[w][0] = bv[0];
+      oi[w][0] = bi[0];
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      for (int q = 1; q < 4; ++q)
+        if (better(ov[q][0], oi[q][0], bv[0], bi[0])) {
+          bv[0] = ov[q][0];
+          bi[0] = oi[q][0];
+        }
+      rec[0] = bv[0];
+      rec[1] = __int_as_float(bi[0]);
+    }
+  } else {
+    __syncthreads();
+    const int nc = n_cand;
+    if (nc <= kCandCap) {
+      // rank of candidate t among the candidates; ranks < KT are the top KT
+      if (threadIdx.x < nc) {
+        const float x = cv[threadIdx.x];
+        const int id = ci[threadIdx.x];
+        int r = 0;
+        for (int q = 0; q < nc; ++q) r += better(cv[q], ci[q], x, id) ? 1 : 0;
+        if (r < KT) {
+          rec[r] = x;
+          rec[KT + r] = __int_as_float(id);
+        }
+      }
+      if (threadIdx.x >= nc && threadIdx.x < KT) {
+        rec[threadIdx.x] = -FLT_MAX;
+        rec[KT + threadIdx.x] = __int_as_float(0x7FFFFFFF);
+      }
+    } else {
+      float tv[KT];
+      int ti[KT];
 #pragma unroll
       for (int k = 0; k < KT; ++k) {
-        o[k] = bv[k];
-        o[KT + k] = __int_as_float(bi[k]);
+        tv[k] = -FLT_MAX;
+        ti[k] = 0x7FFFFFFF;
       }
-      o[2 * KT] = M;
-      o[2 * KT + 1] = S;
-      o[2 * KT + 2] = U;
+      for (int j = v0 + threadIdx.x; j < v1; j += 256) {
+        const float x = zs[j - v0];
+        if (x >= tb) topk_insert<KT>(tv, ti, x, j);
+      }
+      float bv[KT];
+      int bi[KT];
+      wave_topk<KT>(tv, ti, bv, bi);
+      if (lane == 0) {
+#pragma unroll
+        for (int k = 0; k < KT; ++k) {
+          ov[w][k] = bv[k];
+          oi[w][k] = bi[k];
+        }
+      }
+      __syncthreads();
+      if (w == 0) {
+        float lv[KT];
+        int li[KT];
+#pragma unroll
+        for (int k = 0; k < KT; ++k) {
+          lv[k] = lane < 4 ? ov[lane][k] : -FLT_MAX;
+          li[k] = lane < 4 ? oi[lane][k] : 0x7FFFFFFF;
+        }
+        wave_topk<KT>(lv, li, bv, bi);
+        if (lane == 0) {
+#pragma unroll
+          for (int k = 0; k < KT; ++k) {
+            rec[k] = bv[k];
+            rec[KT + k] = __int_as_float(bi[k]);
+          }
+        }
+      }
     }
+  }
+  if (threadIdx.x == 0) {
+    float Mb = sm[0], Sb = ss[0], Ub = su[0];
+    for (int q = 1; q < 4; ++q) stats_merge(Mb, Sb, Ub, sm[q], ss[q], su[q]);
+    rec[2 * KT] = Mb;
+    rec[2 * KT + 1] = Sb;
+    rec[2 * KT + 2] = Ub;
   }
 }
 
-void launch_vocab_partial(const float* logits, const int* n, int cap, int V,
-                          int n_chunks, int topk, float* part,
-                          hipStream_t st) {
-  const int chunk = (V + n_chunks - 1) / n_chunks;
-  dim3 grid(n_chunks, cap);
+int launch_vocab_partial(const float* logits, const int* n, int cap, int V,
+                         int max_chunks, int topk, float* part,
+                         hipStream_t st) {
+  // chunks of at most 12288 logits (48 KiB LDS stage), about 2048 workgroups
+  // when the row capacity allows, at most max_chunks (the record buffer)
+  constexpr int kMaxChunk = 12288;
+  int n_chunks = std::max(1, std::min(max_chunks, (2048 + cap - 1) / cap));
+  n_chunks = std::max(n_chunks, (V + kMaxChunk - 1) / kMaxChunk);
+  const int chunk = (((V + n_chunks - 1) / n_chunks) + 3) & ~3;
+  const dim3 grid(n_chunks, cap);
+  const size_t lds = (size_t)chunk * sizeof(float);
   if (topk == 1)
-    vocab_partial_kernel<1><<<grid, 256, 0, st>>>(logits, n, V, chunk, part);
+    vocab_partial_kernel<1><<<grid, 256, lds, st>>>(logits, n, V, chunk, part);
   else
-    vocab_partial_kernel<SB_TOPK_K><<<grid, 256, 0, st>>>(logits, n, V, chunk,
-                                                          part);
+    vocab_partial_kernel<SB_TOPK_K><<<grid, 256, lds, st>>>(logits, n, V, chunk,
+                                                            part);
+  return n_chunks;
 }
 
 // Merge the chunk records of row i inside wave 0: top KT, m, s, u.
