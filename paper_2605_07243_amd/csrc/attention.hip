@@ -335,6 +335,73 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
 // registers.  K [64][HD] and V^T [HD][64] tiles are staged once per
 // workgroup in LDS (double buffered, padded rows: conflict-free 16-byte K
 // reads and 8-byte V^T reads), global loads run DEPTH tiles ahead.
+// Balanced splits (one 8-wave workgroup of the 32x32 kernel fills a CU, so
+// a launch runs in one round only with at most kAttnSlots workgroups): the
+// prefix of every sequence with rows is cut into splits of sp tiles of 64
+// keys, sp the smallest value for which all (sequence, split, KV head,
+// query group) items fit the slots (and no sequence needs more than
+// max_split splits); workgroup b takes item b, items ordered by sequence,
+// then split, then KV head and query group.  Every wave works this out on
+// its own from the prefix lengths (binary search over sp, then a wave scan
+// of the items per sequence); the host guarantees at most 64 sequences,
+// prefixes of at most 256 tiles and sequences x items per split <= slots,
+// so sp = 256 always fits.
+constexpr int kAttnSlots = 256;
+
+struct SplitItem {
+  bool live;
+  int s, z, nz, sp, item;
+};
+
+__device__ __forceinline__ int n_splits_of(int tiles, int sp) {
+  return tiles > 0 ? (tiles + sp - 1) / sp : 1;
+}
+
+__device__ SplitItem balanced_split(const CallPlan& p, int max_pages, int gx,
+                                    int max_split) {
+  const int lane = threadIdx.x & 63;
+  bool act = false;
+  int t = 0;
+  if (lane < p.n_seqs) {
+    act = p.seq_off[lane + 1] > p.seq_off[lane];
+    t = (min(p.prefix_len[lane], max_pages * 16) + 63) >> 6;
+  }
+  const int total = wave_sum_i(act ? t : 0);
+  int tmax = act ? t : 0;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) tmax = max(tmax, __shfl_xor(tmax, o, SB_WAVE));
+  int lo = max(1, max((total * gx + kAttnSlots - 1) / kAttnSlots,
+                      (tmax + max_split - 1) / max_split));
+  int hi = max(lo, 256);
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    const int used = wave_sum_i(act ? n_splits_of(t, mid) : 0);
+    if (used * gx <= kAttnSlots) hi = mid;
+    else lo = mid + 1;
+  }
+  const int nz = act ? n_splits_of(t, lo) : 0;
+  int inc = nz * gx;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int v = __shfl_up(inc, o, SB_WAVE);
+    if (lane >= o) inc += v;
+  }
+  const int exc = inc - nz * gx;
+  const int b = blockIdx.x;
+  const unsigned long long m = __ballot(act && exc <= b && b < inc);
+  SplitItem r{};
+  if (m == 0) return r;
+  const int sl = __builtin_ctzll(m);
+  const int local = b - __shfl(exc, sl, SB_WAVE);
+  r.live = true;
+  r.s = sl;
+  r.sp = lo;
+  r.nz = __shfl(nz, sl, SB_WAVE);
+  r.z = local / gx;
+  r.item = local % gx;
+  return r;
+}
+
 typedef float attn_f32x16_t __attribute__((ext_vector_type(16)));
 typedef unsigned int attn_u32x4_t __attribute__((ext_vector_type(4)));
 
@@ -345,11 +412,16 @@ __device__ __forceinline__ attn_f32x16_t mma32_attn(attn_u32x4_t a, attn_u32x4_t
       0, 0);
 }
 
+// split_rows == nullptr: grid (query groups, sequences x KV heads, splits)
+// with fixed splits of split_tokens keys; else a grid of kAttnSlots
+// balanced items (above), and the split count of every row's sequence is
+// written to split_rows for the merge.
 template <int HD, int NW>
 __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
     const bf16_t* __restrict__ q, CallPlan p, KVView kv, int H, int Hkv,
     int split_tokens, float scale, float* __restrict__ o_part,
-    float* __restrict__ ml, bf16_t* __restrict__ out) {
+    float* __restrict__ ml, bf16_t* __restrict__ out, int n_groups,
+    int max_split, int* __restrict__ split_rows) {
   constexpr int KT = 64;                    // keys per tile
   constexpr int LDK = HD + 8;               // K row: 16 B mod 256 B
   constexpr int LDV = KT + 4;               // V^T row: 136 B, 8-byte reads
@@ -364,11 +436,30 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
   __shared__ __attribute__((aligned(16))) bf16_t vsh[2][HD][LDV];
   constexpr int MAXP = 1024;
   __shared__ int pg_sh[MAXP];
-  const int s = blockIdx.y / Hkv, kh = blockIdx.y % Hkv;
+  int s, kh, qg, zs, nzs, split_tok;
+  if (split_rows != nullptr) {
+    const SplitItem it = balanced_split(p, kv.max_pages, Hkv * n_groups, max_split);
+    if (!it.live) return;                   // uniform: every wave agrees
+    s = it.s;
+    kh = it.item / n_groups;
+    qg = it.item % n_groups;
+    zs = it.z;
+    nzs = it.nz;
+    split_tok = it.sp * 64;
+  } else {
+    s = blockIdx.y / Hkv;
+    kh = blockIdx.y % Hkv;
+    qg = blockIdx.x;
+    zs = blockIdx.z;
+    nzs = gridDim.z;
+    split_tok = split_tokens;
+  }
   const int G = H / Hkv;
   const int row0 = p.seq_off[s];
   const int nq = (p.seq_off[s + 1] - row0) * G;
-  const int qg = blockIdx.x;
+  if (split_rows != nullptr && zs == 0 && kh == 0 && qg == 0)
+    for (int r = row0 + (int)threadIdx.x; r < p.seq_off[s + 1]; r += NW * 64)
+      split_rows[r] = nzs;
   if (qg * NW * 32 >= nq) return;           // uniform for the group
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int lq = lane & 31, h = lane >> 5;
@@ -397,9 +488,9 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
   const bf16_t* svp = static_cast<const bf16_t*>(kv.seg_v);
   const int* ptab = kv.page_table + (size_t)s * kv.max_pages;
   const int Tp = min(p.prefix_len[s], kv.max_pages * 16);
-  const int t0 = blockIdx.z * split_tokens;
-  const int t1 = min(Tp, t0 + split_tokens);
-  const bool last_split = blockIdx.z == gridDim.z - 1;
+  const int t0 = zs * split_tok;
+  const int t1 = min(Tp, t0 + split_tok);
+  const bool last_split = zs == nzs - 1;
   const int L = last_split ? min(p.seg_len[s], kv.seg_pages * 16) : 0;
   const int n_pre = t1 > t0 ? (t1 - t0 + KT - 1) / KT : 0;
   const int n_tiles = n_pre + (L + KT - 1) / KT;
@@ -602,8 +693,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
   if (!qvalid) return;
   // lane register r of head_dim block hb is element 32 hb + 8 (r / 4) +
   // 4 h + r % 4 of this lane's query
-  const int n_split = gridDim.z;
-  if (n_split == 1) {
+  if (split_rows == nullptr && gridDim.z == 1) {
     const float il = l_run > 0.f ? 1.0f / l_run : 0.f;
     bf16_t* o = out + ((size_t)qrow * H + qh) * HD;
 #pragma unroll
@@ -615,7 +705,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
                        pack_bf16x2(acc[hb][4 * g4 + 2] * il, acc[hb][4 * g4 + 3] * il));
     return;
   }
-  float* o = o_part + (((size_t)blockIdx.z * p.cap + qrow) * H + qh) * HD;
+  float* o = o_part + (((size_t)zs * p.cap + qrow) * H + qh) * HD;
 #pragma unroll
   for (int hb = 0; hb < HB; ++hb)
 #pragma unroll
@@ -624,7 +714,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
           make_float4(acc[hb][4 * g4], acc[hb][4 * g4 + 1], acc[hb][4 * g4 + 2],
                       acc[hb][4 * g4 + 3]);
   if (h == 0) {
-    float* mlp = ml + (((size_t)blockIdx.z * p.cap + qrow) * H + qh) * 2;
+    float* mlp = ml + (((size_t)zs * p.cap + qrow) * H + qh) * 2;
     mlp[0] = m_run * 0.69314718055994531f;   // natural-log units
     mlp[1] = l_run;
   }
@@ -644,12 +734,15 @@ template <int NS>
 __global__ __launch_bounds__(merge_threads<NS>()) void attn_merge_kernel_t(
     const float* __restrict__ o_part, const float* __restrict__ ml,
     const int* __restrict__ n, int cap, int H, int hd, int n_split,
-    void* out_v, int es) {
+    void* out_v, int es, const int* __restrict__ split_rows) {
   constexpr int BT = merge_threads<NS>();
   __shared__ float wgt[64][NS];
   __shared__ float inv_l[64];
   const int i = blockIdx.x;
   if (i >= *n) return;
+  // splits written for this row (balanced launches: its sequence's count;
+  // the other slots hold stale data and are never read)
+  if (split_rows != nullptr) n_split = min(n_split, split_rows[i]);
   const size_t zs = (size_t)cap * H * hd;
   const int ncol = (H * hd) >> 2;
   const float* row = o_part + (size_t)i * H * hd;
@@ -719,7 +812,8 @@ __global__ __launch_bounds__(merge_threads<NS>()) void attn_merge_kernel_t(
 template <typename T>
 void launch_attn_merge(const CallPlan& p, int H, int hd, int n_split,
                        const float* o_part, const float* ml, T* out,
-                       hipStream_t st, hipEvent_t stop);
+                       hipStream_t st, hipEvent_t stop,
+                       const int* split_rows = nullptr);
 
 namespace {
 
@@ -783,7 +877,7 @@ template <typename T>
 void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
                       int rows_per_seq_cap, int H, int Hkv, int hd,
                       int n_split, int max_prefix, float* o_part, float* ml,
-                      T* out, hipStream_t st) {
+                      T* out, int max_split, int* split_rows, hipStream_t st) {
   hipEvent_t ea = g_attn_start, eb = g_attn_stop;
   g_attn_start = g_attn_stop = nullptr;
   // with a merge, the kernel carries the start event and the merge the stop
@@ -799,13 +893,31 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
   const float scale = 1.0f / sqrtf((float)hd);
   if constexpr (sizeof(T) == 2) {
     if (a.mfma32) {
+      // balanced splits (see balanced_split) when the fixed plan would take
+      // more than two rounds of workgroups and the split can be worked out
+      // on the device: the grid is kAttnSlots items, each sequence's splits
+      // at most ms (the partial slots, and what the other sequences leave
+      // of the slots).  Measured: 4 sequences of equal prefixes (fixed plan
+      // 576 workgroups) +12%; 16 ragged prefixes (512) 7% slower than the
+      // fixed plan, whose second round fills in behind the short sequences
+      const int gx = a.groups * Hkv;
+      const bool bal = split_rows != nullptr && p.n_seqs <= 64 &&
+                       p.n_seqs * gx <= kAttnSlots && max_prefix <= 256 * 64 &&
+                       (long)p.n_seqs * gx * n_split > 2 * kAttnSlots;
+      const int ms = bal ? std::max(1, std::min(max_split,
+                                                kAttnSlots / gx - (p.n_seqs - 1)))
+                         : n_split;
+      const dim3 g32 = bal ? dim3(kAttnSlots) : grid;
+      int* sr = bal ? split_rows : nullptr;
+      const bool merge = bal || n_split > 1;
+      const hipEvent_t kb32 = merge ? nullptr : eb;
 #define SB_ATTN32(HD_, NW_)                                                    \
   if (hd == HD_ && a.nq == NW_) {                                             \
-    hipExtLaunchKernelGGL(tree_attn32_kernel<HD_, NW_>, grid, dim3(NW_ * 64), \
-                          0, st, ka, kb, 0, q, p, kv, H, Hkv, split_tokens,   \
-                          scale, o_part, ml, out);                            \
-    if (n_split > 1)                                                          \
-      launch_attn_merge<T>(p, H, hd, n_split, o_part, ml, out, st, eb);       \
+    hipExtLaunchKernelGGL(tree_attn32_kernel<HD_, NW_>, g32, dim3(NW_ * 64),  \
+                          0, st, ka, kb32, 0, q, p, kv, H, Hkv, split_tokens, \
+                          scale, o_part, ml, out, a.groups, ms, sr);          \
+    if (merge)                                                                \
+      launch_attn_merge<T>(p, H, hd, ms, o_part, ml, out, st, eb, sr);        \
     return;                                                                   \
   }
     SB_ATTN32(128, 8) SB_ATTN32(128, 4) SB_ATTN32(64, 8) SB_ATTN32(64, 4)
@@ -833,7 +945,8 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
 template <typename T>
 void launch_attn_merge(const CallPlan& p, int H, int hd, int n_split,
                        const float* o_part, const float* ml, T* out,
-                       hipStream_t st, hipEvent_t stop) {
+                       hipStream_t st, hipEvent_t stop,
+                       const int* split_rows) {
   // every split's (m, l) and partial row is loaded at once (no dependent
   // chain); the template size is n_split rounded up, extra slots read as
   // empty splits
@@ -842,7 +955,7 @@ void launch_attn_merge(const CallPlan& p, int H, int hd, int n_split,
     hipExtLaunchKernelGGL(attn_merge_kernel_t<NS_>, dim3(p.cap),              \
                           dim3(merge_threads<NS_>()), 0, st, nullptr, stop,   \
                           0, o_part, ml, p.n, p.cap, H, hd, n_split, out,     \
-                          (int)sizeof(T));                                    \
+                          (int)sizeof(T), split_rows);                        \
     return;                                                                   \
   }
   SB_MERGE(2) SB_MERGE(4) SB_MERGE(8) SB_MERGE(16) SB_MERGE(32)
@@ -855,11 +968,11 @@ int attn_qgroups(int rows_per_seq_cap, int G, int seq_heads, int es) {
 
 template void launch_tree_attn<float>(const float*, const CallPlan&,
                                       const KVView&, int, int, int, int, int,
-                                      int, float*, float*, float*,
+                                      int, float*, float*, float*, int, int*,
                                       hipStream_t);
 template void launch_tree_attn<bf16_t>(const bf16_t*, const CallPlan&,
                                        const KVView&, int, int, int, int, int,
-                                       int, float*, float*, bf16_t*,
+                                       int, float*, float*, bf16_t*, int, int*,
                                        hipStream_t);
 
 }  // namespace sb

@@ -121,6 +121,7 @@ struct sb_ctx {
   void* q = nullptr;
   float* o_part = nullptr;
   float* ml = nullptr;
+  int* split_rows = nullptr;     // [R] attention splits of each row's sequence
   float* logits = nullptr;
   float2* node_stats = nullptr;  // [S][budget][tiles] softmax stats of z / T
   float* row_lse = nullptr;      // [S][row_cap] drafter rows' log-sum-exp
@@ -183,6 +184,7 @@ static size_t layout(const Dims& D, void* base, sb_ctx* c) {
   void* q = cv.take<char>(R * D.H * D.hd * es);
   float* o_part = cv.take<float>((size_t)D.n_split * R * D.H * D.hd * 4);
   float* ml = cv.take<float>((size_t)D.n_split * R * D.H * 2 * 4);
+  int* split_rows = cv.take<int>(R * 4);
   float* logits = cv.take<float>(R * D.V * 4);
   float* row_lse = cv.take<float>((size_t)D.S * D.row_cap * 4);
   // head-update region (its own buffers: the update may run on another
@@ -247,6 +249,7 @@ static size_t layout(const Dims& D, void* base, sb_ctx* c) {
     c->q = q;
     c->o_part = o_part;
     c->ml = ml;
+    c->split_rows = split_rows;
     c->logits = logits;
     c->node_stats = node_stats;
     c->row_lse = row_lse;
@@ -680,7 +683,7 @@ void layer_body(sb_ctx* c, const sb_layer_weights& lw, int layer,
     ProfScope ps(c, st, SB_PROF_ATTN);
     launch_tree_attn<T>(static_cast<const T*>(c->q), p, kv, rows_per_seq, D.H,
                         D.Hkv, D.hd, n_split, max_prefix, c->o_part, c->ml, A,
-                        st);
+                        D.n_split, c->split_rows, st);
   }
   ks = gemm<T>(c, A, D.H * D.hd, lw.w_o, D.d, D.H * D.hd, p.n, R, st);
   launch_residual<T>(c->x, c->P, ks, (size_t)D.R_cap * D.d, p.n, R, D.d, true,

@@ -124,7 +124,7 @@ template <typename T>
 void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
                       int rows_per_seq_cap, int H, int Hkv, int hd,
                       int n_split, int max_prefix, float* o_part, float* ml,
-                      T* out, hipStream_t st);
+                      T* out, int max_split, int* split_rows, hipStream_t st);
 // Query groups (workgroups) per (sequence, KV head) of a launch (seq_heads
 // = the launch's sequences x KV heads, es = element bytes).
 int attn_qgroups(int rows_per_seq_cap, int G, int seq_heads, int es);
