@@ -253,7 +253,7 @@ int sb_bind(sb_ctx* ctx, const sb_target_weights* target,
  *     aligned).  Logical row r' of block rb = r' / 32 is source row r' when
  *     gate_up == 0; with gate_up != 0, logical row 32 rb + j is gate row
  *     16 rb + j (j < 16) or up row rows/2 + 16 rb + j - 16.  Element
- *       dst[((rb * (cols / 64) + kb) * 4 + i) * 512 + l * 8 + e]
+ *       dst[((kb * (rows / 32) + rb) * 4 + i) * 512 + l * 8 + e]
  *         = logical[32 rb + l % 32][64 kb + 32 (l / 32) + 8 i + e]
  *     for l = 0..63, i = 0..3, e = 0..7.
  * Enqueued on `stream`; errors: SB_EINVAL (NULL / misaligned / overlapping

@@ -73,7 +73,7 @@ __global__ __launch_bounds__(256) void lm_update_kernel(
       r = 32 * rbi + (l & 31);
       c = 64 * kbi + 32 * (l >> 5) + 8 * sub;
       const int rb = (r0 >> 5) + rbi, kb = (c0 >> 6) + kbi;
-      addr = ((((size_t)rb * (d >> 6) + kb) * 4 + sub) * 512) + (size_t)l * 8;
+      addr = ((((size_t)kb * (Vd >> 5) + rb) * 4 + sub) * 512) + (size_t)l * 8;
     } else {
       r = q / (CW / 8);
       c = 8 * (q % (CW / 8));

@@ -8,8 +8,10 @@
 // adds, which keeps results independent of scheduling order.
 //
 // bf16 (gemm_tile_kernel).  Weights are stored fragment-packed (the layout
-// sb_pack_weight writes): 32-row x 64-column blocks of 4 KiB, block
-// (rb, kb) at element offset (rb * K/64 + kb) * 2048, and inside a block
+// sb_pack_weight writes): 32-row x 64-column blocks of 4 KiB, K-block-major,
+// block (rb, kb) at element offset (kb * N/32 + rb) * 2048 (the waves that
+// stream neighbouring row blocks at the same K-stage read neighbouring
+// 4 KiB blocks), and inside a block
 // four 1 KiB sub-steps i, lane l holding the 8 elements
 //   W[32 rb + l % 32][64 kb + 32 (l / 32) + 8 i + e],  e = 0..7.
 // That is the A operand of v_mfma_f32_32x32x16_bf16 for sub-step i when the
@@ -87,12 +89,12 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(
   const bool wave_on = nb < N;                         // N % 32 == 0 tails
   const int kc0 = kc * k_chunk;
   const int nstage = k_chunk / 64;
-  const int kblocks = K / 64;
+  const size_t kstride = (size_t)(N / 32) * 2048;   // one K-block of all rows
   const bf16_t* wp[NF];
 #pragma unroll
   for (int f = 0; f < NF; ++f) {
     const int rb = min((nb >> 5) + f, N / 32 - 1);
-    wp[f] = W + ((size_t)rb * kblocks + kc0 / 64) * 2048 + lane * 8;
+    wp[f] = W + (size_t)(kc0 / 64) * kstride + (size_t)rb * 2048 + lane * 8;
   }
   // activation chunks of this thread: c = tid + 256 q is row c / 8,
   // 16-byte column chunk c % 8 of the stage; rows >= M repeat row M - 1
@@ -125,14 +127,14 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(
 #define SB_SCHED __builtin_amdgcn_sched_barrier(0);
 #define SB_ISSUE_W(p, s_)                                                     \
   {                                                                           \
-    const size_t so = (size_t)min((s_), nstage - 1) * 2048;                   \
+    const size_t so = (size_t)min((s_), nstage - 1) * kstride;                \
     _Pragma("unroll") for (int f = 0; f < NF; ++f)                            \
     _Pragma("unroll") for (int i = 0; i < 4; ++i) wq[p][f][i] =               \
         *reinterpret_cast<const u32x4_t*>(wp[f] + so + 512 * i);              \
   }
 #define SB_ISSUE_WI(p, s_, i)                                                 \
   {                                                                           \
-    const size_t so = (size_t)min((s_), nstage - 1) * 2048;                   \
+    const size_t so = (size_t)min((s_), nstage - 1) * kstride;                \
     _Pragma("unroll") for (int f = 0; f < NF; ++f) wq[p][f][i] =              \
         *reinterpret_cast<const u32x4_t*>(wp[f] + so + 512 * (i));            \
   }
@@ -332,10 +334,10 @@ __global__ void pack_kernel(const bf16_t* __restrict__ src,
                             bool gate_up, size_t chunks) {
   const size_t c = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (c >= chunks) return;
-  const int kblocks = cols / 64;
+  const int rblocks = rows / 32;
   const size_t blk = c >> 8;
   const int i = (int)((c >> 6) & 3), l = (int)(c & 63);
-  const int rb = (int)(blk / kblocks), kb = (int)(blk % kblocks);
+  const int kb = (int)(blk / rblocks), rb = (int)(blk % rblocks);
   const int j = l & 31;
   int row = 32 * rb + j;
   if (gate_up) row = j < 16 ? 16 * rb + j : rows / 2 + 16 * rb + (j - 16);

@@ -663,7 +663,7 @@ __global__ __launch_bounds__(256) void reject_signal_kernel(
       // fragment-packed LM head (32-row x 64-column blocks)
       const int c = k0 & 63;
       const int l = (id & 31) + 32 * (c >> 5);
-      wi = ((((size_t)(id >> 5) * (d >> 6) + (k0 >> 6)) * 4 + ((c & 31) >> 3)) *
+      wi = ((((size_t)(k0 >> 6) * (Vd >> 5) + (id >> 5)) * 4 + ((c & 31) >> 3)) *
             512) + (size_t)l * 8;
     } else {
       wi = (size_t)id * d + k0;

@@ -35,7 +35,7 @@ def unpack(packed: np.ndarray, rows: int, cols: int) -> np.ndarray:
     lane = (idx // 8) % 64
     i = (idx // 512) % 4
     blk = idx // 2048
-    rb, kb = blk // (cols // 64), blk % (cols // 64)
+    kb, rb = blk // (rows // 32), blk % (rows // 32)
     row = 32 * rb + lane % 32
     col = 64 * kb + 32 * (lane // 32) + 8 * i + e
     out = np.empty((rows, cols), packed.dtype)

@@ -20,7 +20,7 @@ def expected_packed(src: np.ndarray, gate_up: bool) -> np.ndarray:
     lane = (idx // 8) % 64
     i = (idx // 512) % 4
     blk = idx // 2048
-    rb, kb = blk // (cols // 64), blk % (cols // 64)
+    kb, rb = blk // (rows // 32), blk % (rows // 32)
     j = lane % 32
     if gate_up:
         row = np.where(j < 16, 16 * rb + j, rows // 2 + 16 * rb + j - 16)
