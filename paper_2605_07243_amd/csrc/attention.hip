@@ -830,13 +830,16 @@ struct AttnShape {
 };
 AttnShape attn_shape(int rows_per_seq_cap, int G, int seq_heads, int es) {
   AttnShape a{};
-  if (es == 2 && seq_heads >= 32) {
-    // many (sequence, KV head) pairs: the 32x32x16 kernel, waves of 32
-    // query vectors, 4 or 8 per workgroup (at least four waves share the
-    // tile loads; waves past the queries only load).  With few pairs the
-    // parallelism has to come from the splits and the 16-row q-tiles of
-    // the other kernel keep each split's chain shorter (measured faster for
-    // one sequence).
+  if (es == 2 && (seq_heads >= 32 || rows_per_seq_cap * G >= 512)) {
+    // many (sequence, KV head) pairs, or at least 512 query vectors per KV
+    // head: the 32x32x16 kernel, waves of 32 query vectors, 4 or 8 per
+    // workgroup (at least four waves share the tile loads; waves past the
+    // queries only load).  With few pairs and few queries the parallelism
+    // has to come from the splits and the 16-row q-tiles of the other
+    // kernel keep each split's chain shorter (measured faster for one
+    // sequence of 60 tree nodes; at 128 nodes x 4 query heads the 32x32
+    // kernel with balanced splits reads each K/V tile for 256 queries
+    // instead of 64: +12% attention throughput).
     const int qblocks = (rows_per_seq_cap * G + 31) / 32;
     a.mfma32 = true;
     a.nq = qblocks > 4 ? 8 : 4;
@@ -903,7 +906,8 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
       const int gx = a.groups * Hkv;
       const bool bal = split_rows != nullptr && p.n_seqs <= 64 &&
                        p.n_seqs * gx <= kAttnSlots && max_prefix <= 256 * 64 &&
-                       (long)p.n_seqs * gx * n_split > 2 * kAttnSlots;
+                       (p.n_seqs == 1 ||          // even splits, no rounding
+                        (long)p.n_seqs * gx * n_split > 2 * kAttnSlots);
       const int ms = bal ? std::max(1, std::min(max_split,
                                                 kAttnSlots / gx - (p.n_seqs - 1)))
                          : n_split;
