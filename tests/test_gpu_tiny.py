@@ -3,6 +3,7 @@ vocab 1024, K = 4, M = 3, budget 32, prompt 128): every C-ABI call against
 the oracle on identical inputs (the oracle's state is copied into the device
 caches before each call), tolerance 1e-4 relative for fp32."""
 import copy
+import dataclasses
 
 import numpy as np
 import pytest
@@ -70,6 +71,25 @@ def test_iteration_calls(tiny):
     """Block expansions, verification, acceptance and commit, each on the
     oracle's own inputs."""
     w, tgt, dr, prompt, st0, rt = tiny
+    _iteration_case(w, st0, rt)
+
+
+@pytest.mark.parametrize("budget", [2, 5, 9])
+def test_iteration_calls_small_budget(tiny, budget):
+    """Degenerate trees: a budget of 2, 5 or 9 nodes fills during block 1
+    (the last rows of the block are cut), so blocks 2 and 3 have no starts
+    and must add nothing; verify, accept and commit then run on the cut
+    tree (Alg. 2 with the tree budget of Sec. 3.2)."""
+    w0, tgt, dr, prompt, st0, _ = tiny
+    w = dataclasses.replace(w0, budget=budget)
+    weights, _, _ = models(w)
+    rt = runtime(w, weights, max_pages=32, adapt_cap=8)
+    _iteration_case(w, st0, rt, tgt, dr)
+
+
+def _iteration_case(w, st0, rt, tgt=None, dr=None):
+    if tgt is None:
+        weights, tgt, dr = models(w)
     st = copy.deepcopy(st0)
     inject(rt, 0, st)
     ref_state = copy.deepcopy(st)
@@ -80,6 +100,11 @@ def test_iteration_calls(tiny):
         rt.expand(m, want_logits=True)
         torch.cuda.synchronize()
         _check_block(rt, exp, rec["rows"], tree, m)
+    for m in range(len(rec["expansions"]) + 1, w.M + 1):
+        print("expand", m, "(no starts)", flush=True)
+        rt.expand(m, want_logits=True)
+        torch.cuda.synchronize()
+        assert int(rt.dout["n_call"][0]) == 0, m
     n = len(tree)
     assert int(rt.tree["n_nodes"][0]) == n
     t = rt.tree
