@@ -118,8 +118,12 @@ void launch_rows_to_elem(const float* src, const int* idx, const int* n,
                          int cap, int w, T* out, hipStream_t st);
 
 // Tree attention over paged prefix + masked segment.
-// o_part / ml: split partials [n_split][cap][H][hd] / [n_split][cap][H][2]
-// (used when n_split > 1, then merged by a second launch).
+// o_part / ml: split partials [max_split][cap][H][hd] / [max_split][cap][H][2]
+// (used when there is more than one split, then merged by a second launch).
+// n_split: splits of the fixed plan (split length max_prefix / n_split);
+// the bf16 32x32 kernel may instead size the splits on the device from the
+// prefix lengths (at most max_split per sequence) and then writes each
+// row's split count to split_rows [cap] for the merge.
 template <typename T>
 void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
                       int rows_per_seq_cap, int H, int Hkv, int hd,
