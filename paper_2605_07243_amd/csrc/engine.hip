@@ -70,9 +70,11 @@ Dims derive(const sb_config& c) {
   D.tpages = ceil_div(std::max(D.budget, D.chunk), 16);
   D.dpages = ceil_div(std::max(D.row_cap, D.chunk), 16);
   // record slots per row for the vocabulary reductions: up to 64 chunks,
-  // and always enough for chunks of at most 12288 logits
-  D.n_chunks = std::max({1, std::min(64, D.V / 2048), (D.V + 12287) / 12288});
-  D.n_chunks_d = std::max({1, std::min(64, D.Vd / 2048), (D.Vd + 12287) / 12288});
+  // and always enough for chunks of at most kVocabChunkMax logits
+  const int min_v = (D.V + kVocabChunkMax - 1) / kVocabChunkMax;
+  const int min_vd = (D.Vd + kVocabChunkMax - 1) / kVocabChunkMax;
+  D.n_chunks = std::max({1, std::min(64, D.V / 2048), min_v});
+  D.n_chunks_d = std::max({1, std::min(64, D.Vd / 2048), min_vd});
   D.adapt_cap = c.adapt_cap;
   D.n_split = 32;
   // partial-sum buffer: the largest ks * N over the projections

@@ -133,7 +133,10 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
 // = the launch's sequences x KV heads, es = element bytes).
 int attn_qgroups(int rows_per_seq_cap, int G, int seq_heads, int es);
 
-// Vocabulary reductions over fp32 logits [cap][V].
+// Vocabulary reductions over fp32 logits [cap][V], in chunks of at most
+// kVocabChunkMax logits (a chunk is staged in LDS); a row needs at least
+// ceil(V / kVocabChunkMax) record slots.
+constexpr int kVocabChunkMax = 12288;
 // Returns the number of chunk records written per row (<= max_chunks).
 int launch_vocab_partial(const float* logits, const int* n, int cap, int V,
                          int max_chunks, int topk, float* part,

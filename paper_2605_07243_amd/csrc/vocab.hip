@@ -260,11 +260,11 @@ __global__ __launch_bounds__(256) void vocab_partial_kernel(
 int launch_vocab_partial(const float* logits, const int* n, int cap, int V,
                          int max_chunks, int topk, float* part,
                          hipStream_t st) {
-  // chunks of at most 12288 logits (48 KiB LDS stage), about 2048 workgroups
-  // when the row capacity allows, at most max_chunks (the record buffer)
-  constexpr int kMaxChunk = 12288;
+  // chunks of at most kVocabChunkMax logits (48 KiB LDS stage), about 2048
+  // workgroups when the row capacity allows, at most max_chunks (the record
+  // buffer, sized for at least ceil(V / kVocabChunkMax))
   int n_chunks = std::max(1, std::min(max_chunks, (2048 + cap - 1) / cap));
-  n_chunks = std::max(n_chunks, (V + kMaxChunk - 1) / kMaxChunk);
+  n_chunks = std::max(n_chunks, (V + kVocabChunkMax - 1) / kVocabChunkMax);
   const int chunk = (((V + n_chunks - 1) / n_chunks) + 3) & ~3;
   const dim3 grid(n_chunks, cap);
   const size_t lds = (size_t)chunk * sizeof(float);
