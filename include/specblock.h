@@ -225,15 +225,30 @@ int32_t sb_row_capacity(const sb_config* cfg);
 /* Workspace bytes sb_bind needs for this configuration (0 if invalid). */
 size_t sb_workspace_bytes(const sb_config* cfg);
 
-/* Validate cfg (SB_EINVAL / SB_ESHAPE / SB_EDTYPE) and create a context. */
+/* Validate cfg (SB_EINVAL / SB_ESHAPE / SB_EDTYPE) and create a context.
+ * The configuration carries the inputs of one verifier iteration (Alg. 2:
+ * block depth K, block budget M, the bucket-to-branching map b(.) of the
+ * inference procedure, App. A.5), the drafter block's shape (Sec. 3.1: a
+ * Llama-style decoder of the target's width, App. A.1: L layers and an
+ * optional reduced vocabulary) and the target's, plus capacities.  Host
+ * only: nothing is allocated on the device.  *out is NULL on error. */
 int sb_create(const sb_config* cfg, sb_ctx** out);
 void sb_destroy(sb_ctx* ctx);
 /* Thread-unsafe description of the last error of ctx (or of the last failed
  * sb_create when ctx is NULL). */
 const char* sb_last_error(const sb_ctx* ctx);
 
-/* Attach weights and workspace.  Tables are copied (host arrays may be
+/* Attach weights and workspace.  The target tables hold the verifier
+ * (Alg. 2, M) and the drafter tables the drafter D_theta of Sec. 3.1:
+ * W_cond (Eq. 1), the three input norms, position queries and W_fuse
+ * (Eq. 2), per layer W_shift (Eq. 3) and the decoder weights, the LM head
+ * and the rank head g_phi (Eq. 4).  Tables are copied (host arrays may be
  * freed); the device memory they point to must outlive the context.
+ * workspace: device, 256-byte aligned, >= sb_workspace_bytes(cfg) bytes,
+ * owned by the caller and used as the library's scratch until the context
+ * is destroyed or bound again.  Errors: SB_EINVAL (NULL or misaligned
+ * pointers, a d2t that is not strictly increasing in [0, vocab)),
+ * SB_EBUDGET (workspace too small), SB_EHIP (reading d2t failed). */
  * SB_BF16: the projection matrices must have been packed by sb_pack_weight
  * (w_gate_up with gate_up = 1, the others with 0). */
 int sb_bind(sb_ctx* ctx, const sb_target_weights* target,
@@ -262,7 +277,12 @@ int sb_bind(sb_ctx* ctx, const sb_target_weights* target,
 int sb_pack_weight(const void* src, void* dst, int32_t rows, int32_t cols,
                    int32_t dtype, int32_t gate_up, void* stream);
 
-/* Prefill (setup, not the hot path): causal target forward over each prompt
+/* Prefill (setup, not the hot path).  It produces what one verifier
+ * iteration requires (Alg. 2): the last verified token, the target's
+ * multi-layer features of the preceding position, and the committed
+ * prefix's K/V for both models; the drafter's entries are the K/V each
+ * committed position produced in its own draft forward (App. A.2), here a
+ * one-position block per prompt position.  Causal target forward over each prompt
  * x_0..x_{n_s-1}, writing target K/V entries 0..n_s-1, the root x_{n_s}
  * (greedy), T = n_s and cond_taps; then drafter catch-up rows for positions
  * 1..n_s (a K = 1 block started at position p-1 conditioned on the target
@@ -334,13 +354,18 @@ int sb_accept_sample(sb_ctx* ctx, int32_t n_seqs, const sb_tree* tree,
                      const float* u_accept, const float* u_bonus,
                      sb_accept_out* out, void* stream);
 
-/* Commit: target K/V of the root and accepted nodes (from the last
+/* Commit (Alg. 2: the accepted prefix and the bonus are committed before
+ * the next iteration, App. A.5; committed positions keep the K/V of their
+ * own draft forward, App. A.2).  Target K/V of the root and accepted nodes (from the last
  * sb_tree_verify) become entries T..T+a; drafter entries for positions
  * T+1..T+a reuse the K/V of the rows that proposed the accepted nodes, and
  * position T+a+1 reuses the row continuing the last accepted node, or, when
  * the tree has none, a catch-up row (K = 1 block started at the last
  * accepted node, conditioned on the taps of its parent).  Then root = bonus,
  * T += a + 1, cond_taps = taps of the last accepted node. */
+/* Errors: SB_EINVAL (NULL or misaligned pointers), SB_ESHAPE (n_seqs,
+ * cache layer counts), SB_ESTATE (not bound).  Pages for the new entries
+ * must already be in both page tables. */
 int sb_commit(sb_ctx* ctx, sb_seqs* seqs, const sb_tree* tree,
               const sb_verify_out* verify, const sb_accept_out* acc,
               sb_kv* target_kv, sb_kv* draft_kv, void* stream);

@@ -107,3 +107,28 @@ def test_target_rank_brute_force():
         i = int(rng.integers(30))
         order = sorted(range(30), key=lambda j: (-z[j], j))
         assert target_rank(z, i) == order.index(i) + 1
+
+
+def test_drift_term_is_kl_of_training_head_from_pre_deployment_head():
+    """Sec. 3.4's drift penalty is lambda KL(p_theta || p_theta0): on three
+    tokens with p = (0.7, 0.2, 0.1) and p0 = (0.2, 0.3, 0.5) the two
+    directions differ (0.6349 vs 0.6758) and the loss must carry the first.
+    The cross-entropy terms are switched off (no target id) and the rank
+    head scores all zero, which leaves its cross-entropy at log 4."""
+    import scipy.stats
+    p = np.array([0.7, 0.2, 0.1])
+    p0 = np.array([0.2, 0.3, 0.5])
+    lm = np.log(p)[:, None]            # d = 1, operand a = 1: z = log p
+    lm0 = np.log(p0)[:, None]
+    A = np.ones((1, 1))
+    h = np.zeros((1, 1))
+    psis = np.zeros((1, 15))
+    rw, rb = np.zeros((4, 16)), np.zeros(4)
+    lam = 2.0
+    loss = head_loss(lm, rw, rb, lm0, A, h, [None], psis, np.array([0]), lam)
+    fwd = scipy.stats.entropy(p, p0)   # KL(p || p0)
+    rev = scipy.stats.entropy(p0, p)
+    assert abs(fwd - rev) > 0.04
+    assert fwd == pytest.approx(0.634897, abs=1e-6)
+    assert loss == pytest.approx(lam * fwd + np.log(4.0), rel=1e-12)
+    assert abs(loss - (lam * rev + np.log(4.0))) > 0.08

@@ -72,6 +72,13 @@ def _two_blocks(dr, st, w, second_start_depth):
 
 
 def test_attention_pattern_matches_paper_figure():
+    """The 8x8 block part of the App. A.2 figure (block rows against block
+    columns) and the block rows' position ids.  The figure's two prefix
+    columns (t1, t2) are deliberately left unpinned: the committed prefix
+    is fully visible to every block row by construction, and position 0
+    (t1) has no drafter K/V entry here, since no draft forward can have
+    produced it (prefix entries come from each committed position's own
+    draft forward, and position 0 precedes every draft)."""
     golden, pos = _read_golden()
     w = synth.Workload("fig", "f32", SHAPE, 1, K=4, M=2, B_max=1, budget=40,
                        n_seqs=1, prompt_len=(1, 1))

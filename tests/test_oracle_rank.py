@@ -90,3 +90,58 @@ def test_bucket_argmax_ties_low():
     assert bucket_of_scores([0.5, 2.0, 2.0, 1.0]) == 1
     assert bucket_of_scores([3.0, 3.0, 3.0, 3.0]) == 0
     assert bucket_of_scores([-1, -2, -0.5, -0.5]) == 2
+
+
+# --- rank head g_phi over [h^(L), psi] (Eq. 4) ---------------------------
+# Crafted heads that read one block of the input at a time: a swapped
+# concatenation [psi, h], a dropped block or a dropped bias each change the
+# winning bucket or the score value below.
+
+def _rank_case():
+    d = 8
+    h = np.array([0.5, -1.0, 2.0, 7.0, -3.0, 0.25, 1.5, -0.75])
+    # two-level logits: top token at 5, the other 999 at 0 (closed-form psi)
+    z = np.zeros(1000)
+    z[7] = 5.0
+    Z = np.exp(5.0) + 999.0
+    p1 = np.exp(5.0) / Z
+    return d, h, psi(z), p1
+
+
+def test_rank_head_reads_h_block_first():
+    from oracle.rank import rank_scores
+    d, h, ps, _ = _rank_case()
+    w = np.zeros((4, d + 15))
+    w[1, 3] = 1.0          # bucket b1 scores h^(L)[3] = 7
+    w[2, 4] = 1.0          # bucket b2 scores h^(L)[4] = -3
+    s = rank_scores(w, np.zeros(4), h, ps)
+    np.testing.assert_array_equal(s, [0.0, 7.0, -3.0, 0.0])
+    assert bucket_of_scores(s) == 1
+
+
+def test_rank_head_reads_psi_block_after_h():
+    from oracle.rank import rank_scores
+    d, h, ps, p1 = _rank_case()
+    w = np.zeros((4, d + 15))
+    w[2, d + 13] = 10.0    # psi[13] = top-1 probability
+    w[3, d + 10] = -1.0    # psi[10] = z1 - z2 = 5 (two-level logits)
+    s = rank_scores(w, np.zeros(4), h, ps)
+    assert s[0] == 0.0 and s[1] == 0.0
+    assert s[2] == pytest.approx(10.0 * p1, rel=1e-12)
+    assert s[3] == pytest.approx(-5.0, rel=1e-12)
+    assert bucket_of_scores(s) == 2
+
+
+def test_rank_head_adds_bias():
+    from oracle.rank import rank_scores
+    d, h, ps, _ = _rank_case()
+    b = np.array([0.0, -1.0, 0.5, 2.0])
+    s = rank_scores(np.zeros((4, d + 15)), b, h, ps)
+    np.testing.assert_array_equal(s, b)
+    assert bucket_of_scores(s) == 3
+    # bias and one weight together: b0 wins with 1 + h[0] = 1.5
+    w = np.zeros((4, d + 15))
+    w[0, 0] = 1.0
+    s = rank_scores(w, np.array([1.0, 0.0, 0.0, 1.4]), h, ps)
+    np.testing.assert_allclose(s, [1.5, 0.0, 0.0, 1.4], rtol=1e-15)
+    assert bucket_of_scores(s) == 0
