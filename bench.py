@@ -364,8 +364,32 @@ def main():
     n_nodes = int(rt.tree["n_nodes"].sum())
     gemm = prof["gemm"]
     gemm_gbps = gemm["bytes"] / (gemm["ms"] * 1e-3) / 1e9
-    flops = gemm_flops(w, verify_rows, rows_block, rt.S)
+    # bytes and flops over the rows each launch processed (the library
+    # captures every profiled launch's live row count); the host-side count
+    # of the same flops must agree
+    flops = gemm["flops"]
+    flops_host = gemm_flops(w, verify_rows, rows_block, rt.S)
+    if abs(flops - flops_host) > 1e-6 * flops_host:
+        log(f"note: library flops {flops:.4e} vs host count {flops_host:.4e} "
+            "(catch-up rows or rows past the budget)")
     gemm_tflops = flops / (gemm["ms"] * 1e-3) / 1e12
+    groups = {}
+    for name, g in prof["gemm_groups"].items():
+        if g["launches"] == 0:
+            continue
+        sec = g["ms"] * 1e-3
+        gb = (g["bytes_read"] + g["bytes_written"]) / sec / 1e9
+        groups[name] = {
+            "launches_per_step": round(g["launches"] / args.steps, 2),
+            "launches_with_rows_per_step": round(
+                g["launches_with_rows"] / args.steps, 2),
+            "us_per_step": round(g["ms"] * 1e3 / args.steps, 1),
+            "read_bytes_per_step": round(g["bytes_read"] / args.steps),
+            "write_bytes_per_step": round(g["bytes_written"] / args.steps),
+            "hbm_gbps": round(gb, 1), "hbm_frac": round(gb / HBM_PEAK_GBPS, 4),
+            "mfma_tflops": round(g["flops"] / sec / 1e12, 1),
+            "mfma_frac": round(g["flops"] / sec / 1e12 /
+                               MFMA_BF16_PEAK_TFLOPS, 4)}
     # bound by arithmetic intensity against the ridge point of the chip
     ridge = MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBPS * 1e9)
     mfma_bound = flops / gemm["bytes"] > ridge
@@ -444,6 +468,13 @@ def main():
                      "traffic": traffic,
                      "algorithmic_bytes_per_launch": round(
                          gemm["bytes"] / max(gemm["launches"], 1)),
+                     "algorithmic_read_bytes_per_step": round(sum(
+                         g["bytes_read"] for g in prof["gemm_groups"].values())
+                         / args.steps),
+                     "algorithmic_write_bytes_per_step": round(sum(
+                         g["bytes_written"]
+                         for g in prof["gemm_groups"].values()) / args.steps),
+                     "groups": groups,
                      "algorithmic_flops_per_launch": round(
                          flops / max(gemm["launches"], 1)),
                      "hbm_gbps": round(gemm_gbps, 1),

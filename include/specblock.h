@@ -248,7 +248,7 @@ const char* sb_last_error(const sb_ctx* ctx);
  * owned by the caller and used as the library's scratch until the context
  * is destroyed or bound again.  Errors: SB_EINVAL (NULL or misaligned
  * pointers, a d2t that is not strictly increasing in [0, vocab)),
- * SB_EBUDGET (workspace too small), SB_EHIP (reading d2t failed). */
+ * SB_EBUDGET (workspace too small), SB_EHIP (reading d2t failed).
  * SB_BF16: the projection matrices must have been packed by sb_pack_weight
  * (w_gate_up with gate_up = 1, the others with 0). */
 int sb_bind(sb_ctx* ctx, const sb_target_weights* target,
@@ -443,14 +443,23 @@ int sb_head_update(sb_ctx* ctx, sb_adapt_buffer* buf, const void* lm_head0,
  * NULL restores the argmax.  Errors: SB_EINVAL (NULL ctx, misaligned). */
 int sb_set_bucket_override(sb_ctx* ctx, const int32_t* buckets);
 
-/* Kernel timing.  While enabled, the library brackets every launch of the
- * projection GEMM, the tree attention (split kernel + merge) and the
- * vocabulary reduction with HIP events on the call's stream and accumulates
- * per class: launches, event-measured milliseconds and, for the GEMM, the
- * algorithmic bytes (weights + activation rows in + fp32 rows out, counted
- * at the call's row capacity) and flops.  sb_profile(ctx, 1) resets and
- * starts, sb_profile(ctx, 0) stops; sb_profile_read waits for the recorded
- * events and fills out[SB_PROF_N]. */
+/* Kernel timing (the per-kernel measurements the hot path is judged by;
+ * not part of the method).  While enabled, the library brackets every
+ * launch of the projection GEMM, the tree attention (split kernel + merge)
+ * and the vocabulary reduction with HIP events on the call's stream and
+ * accumulates per class: launches, event-measured milliseconds and, for
+ * the GEMM, the algorithmic bytes and flops of the rows each launch
+ * actually processed (after every profiled GEMM launch a one-thread kernel
+ * copies its live row count into the workspace; a launch with no rows is
+ * credited no bytes, its duration still counts).  Algorithmic bytes of a
+ * launch with m > 0 rows: the N x K weights and the m x K activations read,
+ * m x N fp32 outputs written (the SwiGLU projection: m x N/2 bf16).
+ * sb_profile(ctx, 1) resets and starts, sb_profile(ctx, 0) stops;
+ * sb_profile_read waits for the recorded events and fills out[SB_PROF_N];
+ * sb_profile_read_gemm fills out[SB_GEMM_N] per group of projections.
+ * At most 32768 GEMM launches are recorded with their row counts per
+ * sb_profile(ctx, 1); later ones are credited at their row capacity.
+ * Errors: SB_EINVAL (NULL), SB_EHIP. */
 enum sb_prof_class { SB_PROF_GEMM = 0, SB_PROF_ATTN = 1, SB_PROF_VOCAB = 2,
                      SB_PROF_N = 3 };
 typedef struct sb_kernel_stat {
@@ -459,8 +468,23 @@ typedef struct sb_kernel_stat {
   double bytes;
   double flops;
 } sb_kernel_stat;
+/* GEMM groups: target projections (QKV, O, down of sb_tree_verify and
+ * sb_prefill), drafter projections (W_cond, W_fuse, W_shift and the
+ * drafter's QKV, O, down), the fused gate/up + SwiGLU projections of both
+ * models, and the two LM heads. */
+enum sb_gemm_group { SB_GEMM_TARGET = 0, SB_GEMM_DRAFTER = 1,
+                     SB_GEMM_SWIGLU = 2, SB_GEMM_LM_HEAD = 3, SB_GEMM_N = 4 };
+typedef struct sb_gemm_stat {
+  int64_t launches;
+  int64_t launches_with_rows;
+  double total_ms;
+  double bytes_read;       /* algorithmic: weights + activation rows        */
+  double bytes_written;    /* algorithmic: output rows                      */
+  double flops;            /* 2 per multiply-add over the processed rows    */
+} sb_gemm_stat;
 int sb_profile(sb_ctx* ctx, int32_t enable);
 int sb_profile_read(sb_ctx* ctx, sb_kernel_stat* out);
+int sb_profile_read_gemm(sb_ctx* ctx, sb_gemm_stat* out);
 
 #ifdef __cplusplus
 }

@@ -103,12 +103,20 @@ class KernelStat(C.Structure):
                 ("bytes", C.c_double), ("flops", C.c_double)]
 
 
+class GemmStat(C.Structure):
+    _fields_ = [("launches", C.c_int64), ("launches_with_rows", C.c_int64),
+                ("total_ms", C.c_double), ("bytes_read", C.c_double),
+                ("bytes_written", C.c_double), ("flops", C.c_double)]
+
+
 PROF_CLASSES = ("gemm", "tree_attn", "vocab")
+GEMM_GROUPS = ("target", "drafter", "swiglu", "lm_head")
 
 EXPORTS = ["sb_row_capacity", "sb_workspace_bytes", "sb_create", "sb_destroy",
            "sb_last_error", "sb_bind", "sb_prefill", "sb_draft_block_expand",
            "sb_tree_verify", "sb_accept", "sb_commit", "sb_set_length_bound",
-           "sb_profile", "sb_profile_read", "sb_pack_weight",
+           "sb_profile", "sb_profile_read", "sb_profile_read_gemm",
+           "sb_pack_weight",
            "sb_set_bucket_override", "sb_accept_sample", "sb_adapt_push",
            "sb_head_update"]
 
@@ -170,6 +178,8 @@ def load(path: str = LIB_PATH):
     lib.sb_profile.restype = C.c_int
     lib.sb_profile_read.argtypes = [vp, P(KernelStat)]
     lib.sb_profile_read.restype = C.c_int
+    lib.sb_profile_read_gemm.argtypes = [vp, P(GemmStat)]
+    lib.sb_profile_read_gemm.restype = C.c_int
     _lib = lib
     return lib
 

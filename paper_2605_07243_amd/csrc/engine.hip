@@ -17,6 +17,9 @@ namespace {
 
 constexpr size_t kAlign = 256;
 constexpr int kVocabRec10 = 2 * SB_TOPK + 3;
+// row counts captured for profiled GEMM launches (one int each); launches
+// past the last slot are credited at their row capacity
+constexpr int kProfSlots = 32768;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -137,6 +140,7 @@ struct sb_ctx {
   int* root_arg = nullptr;
   int* blk_row0 = nullptr;
   int* blk_nst = nullptr;
+  int* prof_rows = nullptr;      // [kProfSlots] rows of profiled GEMM launches
   CommitInfo ci{};
   CallPlan plan{};
   CallPlan fb{};
@@ -154,8 +158,14 @@ struct sb_ctx {
     int cls;
     hipEvent_t a, b;
     double bytes, flops;
+    // projection GEMMs: group, row-count slot (-1: none), row capacity and
+    // the per-launch / per-row algorithmic counts
+    int group = -1, slot = -1, m_cap = 0;
+    double w_bytes = 0, in_row = 0, out_row = 0, flops_row = 0;
   };
   bool prof = false;
+  int prof_group = SB_GEMM_TARGET;   // group of the projections being run
+  int prof_slots_used = 0;
   std::vector<hipEvent_t> ev_pool;
   size_t ev_used = 0;
   std::vector<ProfRec> recs;
@@ -213,6 +223,7 @@ static size_t layout(const Dims& D, void* base, sb_ctx* c) {
   int* zero = cv.take<int>(4);
   int* blk_row0 = cv.take<int>(D.S * 4);
   int* blk_nst = cv.take<int>(D.S * 4);
+  int* prof_rows = cv.take<int>((size_t)kProfSlots * 4);
   CommitInfo ci{cv.take<int>(D.S * 4), cv.take<int>(D.S * 4),
                 cv.take<int>(D.S * 4), cv.take<int>(D.S * 4)};
   auto make_plan = [&](int cap) {
@@ -267,6 +278,7 @@ static size_t layout(const Dims& D, void* base, sb_ctx* c) {
     c->zero = zero;
     c->blk_row0 = blk_row0;
     c->blk_nst = blk_nst;
+    c->prof_rows = prof_rows;
     c->ci = ci;
     c->plan = plan;
     c->fb = fb;
@@ -556,13 +568,18 @@ hipEvent_t next_event(sb_ctx* c) {
 // Times the launches of one class inside its scope.  The projection GEMM
 // (one launch per scope) and the tree attention (kernel + merge) take events
 // attached to their dispatches, which mark the kernels' own start and end;
-// other classes record stream events around their launches.
+// other classes record stream events around their launches.  A GEMM scope
+// also copies the launch's live row count (*n, read on the device) into a
+// profiler slot after the launch, so that its algorithmic bytes and flops
+// are credited for the rows it actually processed (none when it had none).
 struct ProfScope {
   sb_ctx* c;
   hipStream_t st;
   int cls;
   double bytes, flops;
   hipEvent_t a = nullptr, b = nullptr;
+  const int* rows = nullptr;
+  sb_ctx::ProfRec g{};
   ProfScope(sb_ctx* c_, hipStream_t st_, int cls_, double bytes_ = 0,
             double flops_ = 0)
       : c(c_), st(st_), cls(cls_), bytes(bytes_), flops(flops_) {
@@ -574,6 +591,24 @@ struct ProfScope {
     } else {
       (void)hipEventRecord(a, st);
     }
+  }
+  // GEMM launch shape: N x K weights of `es` bytes per element, `n` live
+  // rows of capacity m_cap, out_es bytes per output element (4: fp32 rows
+  // of N; the SwiGLU projection writes N / 2 bf16 values per row)
+  ProfScope(sb_ctx* c_, hipStream_t st_, const int* n, int m_cap, int N,
+            int K, double es, bool swiglu, int group)
+      : ProfScope(c_, st_, SB_PROF_GEMM,
+                  (double)N * K * es + (double)m_cap * K * es +
+                      (double)m_cap * (swiglu ? N / 2 * es : N * 4.0),
+                  2.0 * m_cap * N * K) {
+    if (!a) return;
+    rows = n;
+    g.group = group;
+    g.m_cap = m_cap;
+    g.w_bytes = (double)N * K * es;
+    g.in_row = (double)K * es;
+    g.out_row = swiglu ? N / 2 * es : N * 4.0;
+    g.flops_row = 2.0 * N * K;
   }
   ~ProfScope() {
     if (!a) return;
@@ -591,7 +626,17 @@ struct ProfScope {
       if ((b = next_event(c)) == nullptr) return;
       (void)hipEventRecord(b, st);
     }
-    c->recs.push_back({cls, a, b, bytes, flops});
+    sb_ctx::ProfRec r = g;
+    r.cls = cls;
+    r.a = a;
+    r.b = b;
+    r.bytes = bytes;
+    r.flops = flops;
+    if (rows != nullptr && c->prof_slots_used < kProfSlots) {
+      r.slot = c->prof_slots_used++;
+      launch_copy_int(c->prof_rows + r.slot, rows, st);
+    }
+    c->recs.push_back(r);
   }
 };
 
@@ -599,10 +644,7 @@ template <typename T>
 int gemm(sb_ctx* c, const void* X, int ldx, const void* W, int N, int K,
          const int* n, int m_cap, hipStream_t st) {
   const int ks = 0;   // the shape's own split
-  const double es = sizeof(T);
-  ProfScope ps(c, st, SB_PROF_GEMM,
-               (double)N * K * es + (double)m_cap * K * es + (double)m_cap * N * 4,
-               2.0 * m_cap * N * K);
+  ProfScope ps(c, st, n, m_cap, N, K, sizeof(T), false, c->prof_group);
   return launch_gemm_xwt<T>(static_cast<const T*>(X), ldx,
                             static_cast<const T*>(W), N, K, c->P,
                             (size_t)c->D.R_cap * N, n, m_cap, ks, st);
@@ -616,11 +658,8 @@ void gate_up_swiglu(sb_ctx* c, const void* X, const void* W, const int* n,
                     int m_cap, T* out, hipStream_t st) {
   const Dims& D = c->D;
   if constexpr (sizeof(T) == 2) {
-    const double es = sizeof(T);
-    ProfScope ps(c, st, SB_PROF_GEMM,
-                 2.0 * D.F * D.d * es + (double)m_cap * D.d * es +
-                     (double)m_cap * D.F * es,
-                 2.0 * m_cap * 2 * D.F * D.d);
+    ProfScope ps(c, st, n, m_cap, 2 * D.F, D.d, sizeof(T), true,
+                 SB_GEMM_SWIGLU);
     launch_gemm_swiglu(static_cast<const bf16_t*>(X), D.d,
                        static_cast<const bf16_t*>(W), D.F, D.d, out, n, m_cap,
                        st);
@@ -705,6 +744,7 @@ void target_forward(sb_ctx* c, const CallPlan& p, const Prefix& pf,
                     int rows_per_seq, float* taps, hipStream_t st) {
   const Dims& D = c->D;
   const float eps = c->cfg.target.norm_eps;
+  c->prof_group = SB_GEMM_TARGET;
   launch_embed<T>(p, static_cast<const T*>(c->tw.embed), D.d, c->x, st);
   launch_rmsnorm<T>(c->x, p.n, p.cap, D.d,
                     static_cast<const float*>(c->tw.layers[0].attn_norm), eps,
@@ -732,6 +772,7 @@ void drafter_forward(sb_ctx* c, const CallPlan& p, const float* cond_base,
   const float eps = c->cfg.target.norm_eps;
   const int R = p.cap;
   T* A = static_cast<T*>(c->A);
+  c->prof_group = SB_GEMM_DRAFTER;
   launch_fuse_prep<T>(cond_base, p, static_cast<const T*>(c->tw.embed),
                       static_cast<const T*>(c->dw.pos_query),
                       static_cast<const float*>(c->dw.norm_c),
@@ -760,6 +801,7 @@ void cond_rows(sb_ctx* c, const float* taps, const int* idx, const int* n,
                int cap, hipStream_t st) {
   const Dims& D = c->D;
   T* A = static_cast<T*>(c->A);
+  c->prof_group = SB_GEMM_DRAFTER;
   launch_rows_to_elem<T>(taps, idx, n, cap, 3 * D.d, A, st);
   const int ks = gemm<T>(c, A, 3 * D.d, c->dw.w_cond, D.d, 3 * D.d, n, cap, st);
   launch_residual<T>(c->cond_buf, c->P, ks, (size_t)D.R_cap * D.d, n, cap, D.d,
@@ -774,10 +816,7 @@ template <typename T>
 void lm_head(sb_ctx* c, const void* A, const void* W, int V, float* logits,
              const int* n, int cap, hipStream_t st) {
   const Dims& D = c->D;
-  const double es = sizeof(T);
-  ProfScope ps(c, st, SB_PROF_GEMM,
-               (double)V * D.d * es + (double)cap * D.d * es + (double)cap * V * 4,
-               2.0 * cap * V * D.d);
+  ProfScope ps(c, st, n, cap, V, D.d, sizeof(T), false, SB_GEMM_LM_HEAD);
   launch_gemm_xwt<T>(static_cast<const T*>(A), D.d, static_cast<const T*>(W),
                      V, D.d, logits, (size_t)cap * V, n, cap, 1, st);
 }
@@ -1220,27 +1259,79 @@ int sb_profile(sb_ctx* c, int32_t enable) {
   if (enable) {
     c->recs.clear();
     c->ev_used = 0;
+    c->prof_slots_used = 0;
   }
   c->prof = enable != 0;
   return SB_OK;
 }
 
-int sb_profile_read(sb_ctx* c, sb_kernel_stat* out) {
-  if (!c || !out) return SB_EINVAL;
-  for (int i = 0; i < SB_PROF_N; ++i) out[i] = sb_kernel_stat{0, 0.0, 0.0, 0.0};
-  for (const auto& r : c->recs) {
+}  // extern "C"
+
+namespace {
+
+// Waits for the recorded events and fills the per-class and per-GEMM-group
+// statistics (either output may be NULL).
+int profile_collect(sb_ctx* c, sb_kernel_stat* out, sb_gemm_stat* gout) {
+  if (out)
+    for (int i = 0; i < SB_PROF_N; ++i) out[i] = sb_kernel_stat{0, 0.0, 0.0, 0.0};
+  if (gout)
+    for (int i = 0; i < SB_GEMM_N; ++i)
+      gout[i] = sb_gemm_stat{0, 0, 0.0, 0.0, 0.0, 0.0};
+  for (const auto& r : c->recs)
     if (hipEventSynchronize(r.b) != hipSuccess)
       return fail(c, SB_EHIP, "hipEventSynchronize failed");
+  std::vector<int> rows(c->prof_slots_used);
+  if (!rows.empty() &&
+      hipMemcpy(rows.data(), c->prof_rows, rows.size() * sizeof(int),
+                hipMemcpyDeviceToHost) != hipSuccess)
+    return fail(c, SB_EHIP, "profiler row counts: hipMemcpy failed");
+  for (const auto& r : c->recs) {
     float ms = 0.f;
     if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess)
       return fail(c, SB_EHIP, "hipEventElapsedTime failed");
-    sb_kernel_stat& k = out[r.cls];
-    k.launches += 1;
-    k.total_ms += ms;
-    k.bytes += r.bytes;
-    k.flops += r.flops;
+    double bytes = r.bytes, flops = r.flops;
+    double rd = 0, wr = 0;
+    const bool counted = r.group >= 0;
+    if (counted) {
+      const int m = r.slot >= 0 ? std::min(std::max(rows[r.slot], 0), r.m_cap)
+                                : r.m_cap;
+      rd = m > 0 ? r.w_bytes + m * r.in_row : 0.0;
+      wr = m * r.out_row;
+      bytes = rd + wr;
+      flops = m * r.flops_row;
+      if (gout) {
+        sb_gemm_stat& g = gout[r.group];
+        g.launches += 1;
+        g.launches_with_rows += m > 0;
+        g.total_ms += ms;
+        g.bytes_read += rd;
+        g.bytes_written += wr;
+        g.flops += flops;
+      }
+    }
+    if (out) {
+      sb_kernel_stat& k = out[r.cls];
+      k.launches += 1;
+      k.total_ms += ms;
+      k.bytes += bytes;
+      k.flops += flops;
+    }
   }
   return SB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int sb_profile_read(sb_ctx* c, sb_kernel_stat* out) {
+  if (!c || !out) return SB_EINVAL;
+  return profile_collect(c, out, nullptr);
+}
+
+int sb_profile_read_gemm(sb_ctx* c, sb_gemm_stat* out) {
+  if (!c || !out) return SB_EINVAL;
+  return profile_collect(c, nullptr, out);
 }
 
 }  // extern "C"

@@ -266,6 +266,8 @@ void launch_prefill_finish(const sb_seqs& sq, int s, int len, int d,
                            const int* root_arg, hipStream_t st);
 void launch_copy_f32(float* dst, const float* src, int n, hipStream_t st);
 void launch_set_int(int* p, int v, hipStream_t st);
+// *dst = *src (one thread; e.g. a row count captured for the profiler)
+void launch_copy_int(int* dst, const int* src, hipStream_t st);
 void launch_export_rows(const CallPlan& p, int out_cap, int* call_seq,
                         int* call_row, int* n_call, hipStream_t st);
 

@@ -559,6 +559,11 @@ __global__ void copy_f32_kernel(float* __restrict__ dst, const float* __restrict
 
 __global__ void set_int_kernel(int* __restrict__ p, int v) { *p = v; }
 
+__global__ void copy_int_kernel(int* __restrict__ dst,
+                                const int* __restrict__ src) {
+  *dst = *src;
+}
+
 __global__ void export_rows_kernel(CallPlan p, int out_cap,
                                    int* __restrict__ call_seq,
                                    int* __restrict__ call_row,
@@ -795,6 +800,9 @@ void launch_copy_f32(float* dst, const float* src, int n, hipStream_t st) {
 }
 void launch_set_int(int* p, int v, hipStream_t st) {
   set_int_kernel<<<1, 1, 0, st>>>(p, v);
+}
+void launch_copy_int(int* dst, const int* src, hipStream_t st) {
+  copy_int_kernel<<<1, 1, 0, st>>>(dst, src);
 }
 void launch_export_rows(const CallPlan& p, int out_cap, int* call_seq,
                         int* call_row, int* n_call, hipStream_t st) {

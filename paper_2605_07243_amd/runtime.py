@@ -391,9 +391,18 @@ class Runtime:
     def profile_read(self) -> dict:
         arr = (B.KernelStat * 3)()
         self._check(self.lib.sb_profile_read(self.ctx, arr))
-        return {name: dict(launches=arr[i].launches, ms=arr[i].total_ms,
-                           bytes=arr[i].bytes, flops=arr[i].flops)
-                for i, name in enumerate(B.PROF_CLASSES)}
+        out = {name: dict(launches=arr[i].launches, ms=arr[i].total_ms,
+                          bytes=arr[i].bytes, flops=arr[i].flops)
+               for i, name in enumerate(B.PROF_CLASSES)}
+        g = (B.GemmStat * len(B.GEMM_GROUPS))()
+        self._check(self.lib.sb_profile_read_gemm(self.ctx, g))
+        out["gemm_groups"] = {
+            name: dict(launches=g[i].launches,
+                       launches_with_rows=g[i].launches_with_rows,
+                       ms=g[i].total_ms, bytes_read=g[i].bytes_read,
+                       bytes_written=g[i].bytes_written, flops=g[i].flops)
+            for i, name in enumerate(B.GEMM_GROUPS)}
+        return out
 
     # ------------------------------------------------------------------
     # cache access for tests (host <-> device copies of single entries)

@@ -261,7 +261,7 @@ def test_struct_layouts_match_header(tmp_path):
                "sb_drafter_weights": B.DrafterWeights, "sb_kv": B.KV,
                "sb_seqs": B.Seqs, "sb_tree": B.Tree, "sb_draft_out": B.DraftOut,
                "sb_verify_out": B.VerifyOut, "sb_accept_out": B.AcceptOut,
-               "sb_kernel_stat": B.KernelStat,
+               "sb_kernel_stat": B.KernelStat, "sb_gemm_stat": B.GemmStat,
                "sb_adapt_buffer": B.AdaptBuffer,
                "sb_head_weights": B.HeadWeights}
     lines = ['#include <stdio.h>', '#include <stddef.h>',
