@@ -354,6 +354,27 @@ int sb_accept_sample(sb_ctx* ctx, int32_t n_seqs, const sb_tree* tree,
                      const float* u_accept, const float* u_bonus,
                      sb_accept_out* out, void* stream);
 
+/* Allocation-free variant of sb_accept_sample, for callers that cannot
+ * allocate (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation): same arguments, same results, but the per-node
+ * softmax tile statistics live in a static device array of the library
+ * (65536 float2 entries, 512 KiB, one copy per GPU, held until the process
+ * ends) instead of the bound workspace, and the call allocates nothing.
+ * The context need not be bound unless out->r_reject is requested (the
+ * signal reads the drafter weights and the workspace); only its
+ * configuration (budget, vocab, K, M, B_max) is used otherwise.
+ * Requires n_seqs * budget * ceil(vocab / 16384) <= 65536 (else
+ * SB_EBUDGET).  Every call on a GPU shares that GPU's array, which keeps
+ * the last call's contents (each call writes every entry it reads, so
+ * nothing needs clearing): calls that overlap in time on one GPU, on any
+ * stream or context, race and must be ordered by the caller.
+ * Errors: as sb_accept_sample, plus SB_EBUDGET, SB_ESTATE (r_reject on an
+ * unbound context), SB_EHIP (the array's address could not be resolved). */
+int sb_accept_sample_noalloc(sb_ctx* ctx, int32_t n_seqs, const sb_tree* tree,
+                             const float* logits, float temperature,
+                             const float* u_accept, const float* u_bonus,
+                             sb_accept_out* out, void* stream);
+
 /* Commit (Alg. 2: the accepted prefix and the bonus are committed before
  * the next iteration, App. A.5; committed positions keep the K/V of their
  * own draft forward, App. A.2).  Target K/V of the root and accepted nodes (from the last

@@ -118,7 +118,7 @@ EXPORTS = ["sb_row_capacity", "sb_workspace_bytes", "sb_create", "sb_destroy",
            "sb_profile", "sb_profile_read", "sb_profile_read_gemm",
            "sb_pack_weight",
            "sb_set_bucket_override", "sb_accept_sample", "sb_adapt_push",
-           "sb_head_update"]
+           "sb_head_update", "sb_accept_sample_noalloc"]
 
 _lib = None
 
@@ -167,6 +167,9 @@ def load(path: str = LIB_PATH):
     lib.sb_accept_sample.argtypes = [vp, i32, vp, vp, C.c_float, vp, vp,
                                      vp, vp]
     lib.sb_accept_sample.restype = C.c_int
+    lib.sb_accept_sample_noalloc.argtypes = [vp, i32, vp, vp, C.c_float, vp,
+                                             vp, vp, vp]
+    lib.sb_accept_sample_noalloc.restype = C.c_int
     lib.sb_adapt_push.argtypes = [vp, i32, vp, vp, vp, vp]
     lib.sb_adapt_push.restype = C.c_int
     lib.sb_head_update.argtypes = [vp, vp, vp, vp, C.c_float, C.c_float, vp,

@@ -5,6 +5,7 @@
 #include <algorithm>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -1110,6 +1111,83 @@ int sb_accept_sample(sb_ctx* c, int32_t n_seqs, const sb_tree* tree,
                        c->node_stats, u_accept, u_bonus, *out, st);
   reject_signal(c, n_seqs, *tree, *out, st);
   return hip_check(c, "sb_accept_sample");
+}
+
+}  // extern "C"
+
+// Scratch of the allocation-free stochastic acceptance: the per-node
+// softmax tile statistics that sb_accept_sample keeps in the workspace.
+// Every GPU holds its own copy at its own address until the process ends.
+constexpr size_t kNoAllocStats = 65536;   // float2 entries, 512 KiB
+static __device__ __align__(256) float2 scratch[kNoAllocStats];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};   // device address of scratch per GPU
+
+// Device address of this GPU's scratch, resolved once per device with the
+// device current (host code never passes the array's own name).
+int scratch_for_current_device(sb_ctx* c, float2** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+    return fail(c, SB_EHIP, "sb_accept_sample_noalloc: hipGetDevice failed");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || ptr == nullptr)
+      return fail(c, SB_EHIP,
+                  std::string("sb_accept_sample_noalloc: hipGetSymbolAddress: ") +
+                      hipGetErrorString(e));
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = static_cast<float2*>(g_scratch_ptr[dev]);
+  return SB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int sb_accept_sample_noalloc(sb_ctx* c, int32_t n_seqs, const sb_tree* tree,
+                             const float* logits, float temperature,
+                             const float* u_accept, const float* u_bonus,
+                             sb_accept_out* out, void* stream) {
+  if (!c) return SB_EINVAL;
+  if (n_seqs < 1 || n_seqs > c->cfg.max_seqs)
+    return fail(c, SB_ESHAPE, "n_seqs must be in 1..max_seqs");
+  int rc = check_tree(c, tree);
+  if (rc) return rc;
+  if (!(temperature > 0.f) || !(temperature < 3.0e38f))
+    return fail(c, SB_EINVAL, "temperature must be positive and finite");
+  if (bad_ptr(logits, 4) || bad_ptr(u_accept, 4) || bad_ptr(u_bonus, 4) ||
+      !out || bad_ptr(out->path, 4) || bad_ptr(out->n_accepted, 4) ||
+      bad_ptr(out->bonus, 4) || (out->r_reject && bad_ptr(out->r_reject, 4)))
+    return fail(c, SB_EINVAL, "accept_sample pointer NULL or misaligned");
+  if (out->r_reject && !c->bound)
+    return fail(c, SB_ESTATE,
+                "r_reject needs a bound context (drafter weights)");
+  if (c->D.V > sample_max_vocab())
+    return fail(c, SB_ESHAPE, "sb_accept_sample_noalloc supports vocab <= " +
+                                  std::to_string(sample_max_vocab()));
+  const size_t need = (size_t)n_seqs * c->D.budget * sample_tiles(c->D.V);
+  if (need > kNoAllocStats)
+    return fail(c, SB_EBUDGET,
+                "sb_accept_sample_noalloc: n_seqs * budget * ceil(vocab / "
+                "16384) = " + std::to_string(need) + " exceeds its static "
+                "scratch of " + std::to_string(kNoAllocStats) + " entries");
+  float2* stats = nullptr;
+  if ((rc = scratch_for_current_device(c, &stats))) return rc;
+  const hipStream_t st = S_(stream);
+  const float inv_t = 1.0f / temperature;
+  launch_node_stats(logits, c->D.V, inv_t, tree->n_nodes, n_seqs, c->D.budget,
+                    stats, st);
+  launch_accept_sample(tree_dims(c, n_seqs), *tree, logits, c->D.V, inv_t,
+                       stats, u_accept, u_bonus, *out, st);
+  reject_signal(c, n_seqs, *tree, *out, st);
+  return hip_check(c, "sb_accept_sample_noalloc");
 }
 
 int sb_adapt_push(sb_ctx* c, int32_t n_seqs, const sb_tree* tree,

@@ -299,10 +299,13 @@ class Runtime:
             self.ctx, self.S, C.byref(self.tree_c),
             _ptr(self.vout["argmax"]), C.byref(self.aout_c), self.stream))
 
-    def accept_sample(self, temperature, u_accept, u_bonus):
+    def accept_sample(self, temperature, u_accept, u_bonus, *,
+                      noalloc=False, n_seqs=None):
         """Stochastic acceptance over the logits of the last
         verify(want_logits=True); u_accept, u_bonus: device float tensors
-        [n_seqs][budget] of uniforms in [0, 1)."""
+        [n_seqs][budget] of uniforms in [0, 1).  noalloc: the
+        allocation-free entry point (static scratch); n_seqs: the first
+        n_seqs sequences only (default all)."""
         if self.vout["logits"] is None:
             raise RuntimeError("accept_sample needs verify(want_logits=True)")
         for u in (u_accept, u_bonus):
@@ -312,10 +315,12 @@ class Runtime:
                 raise ValueError("uniforms must be contiguous float32 device "
                                  f"tensors of shape ({self.S}, "
                                  f"{self.w.budget})")
-        self._check(self.lib.sb_accept_sample(
-            self.ctx, self.S, C.byref(self.tree_c), _ptr(self.vout["logits"]),
-            float(temperature), _ptr(u_accept), _ptr(u_bonus),
-            C.byref(self.aout_c), self.stream))
+        fn = (self.lib.sb_accept_sample_noalloc if noalloc
+              else self.lib.sb_accept_sample)
+        self._check(fn(
+            self.ctx, n_seqs or self.S, C.byref(self.tree_c),
+            _ptr(self.vout["logits"]), float(temperature), _ptr(u_accept),
+            _ptr(u_bonus), C.byref(self.aout_c), self.stream))
 
     def commit(self):
         vc = B.VerifyOut(_ptr(self.vout["argmax"]), _ptr(self.vout["taps"]),

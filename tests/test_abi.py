@@ -351,3 +351,43 @@ def test_adaptation_argument_checks(lib):
     assert upd(B.HeadWeights(f.at(), f.at(), f.at())) == B.SB_EINVAL  # bound
     assert upd(B.HeadWeights(f.at(8), f.at(), f.at())) == B.SB_EINVAL
     lib.sb_destroy(ctx)
+
+
+def _fake_tree():
+    """A tree whose every pointer is non-NULL and aligned host memory: the
+    calls below must fail their host-side checks before touching it."""
+    buf = (C.c_int32 * 64)()
+    p = C.cast(buf, C.c_void_p)
+    t = B.Tree(*([p] * len(B.Tree._fields_)))
+    return t, buf
+
+
+def test_noalloc_accept_rejects_sizes_past_its_static_scratch(lib):
+    """sb_accept_sample_noalloc keeps n_seqs * budget * ceil(vocab / 16384)
+    tile statistics in a static array of 65536 entries: 8 x 512 x 16 fits
+    exactly, 9 sequences do not (SB_EBUDGET, before any device work); the
+    signal r needs a bound context (SB_ESTATE)."""
+    c = cfg(t_vocab=262144, budget=512, max_seqs=16)
+    ctx = C.c_void_p()
+    assert lib.sb_create(C.byref(c), C.byref(ctx)) == B.SB_OK
+    try:
+        t, keep = _fake_tree()
+        buf = (C.c_float * 64)()
+        fp = C.cast(buf, C.c_void_p)
+        out = B.AcceptOut(fp, fp, fp, None)
+        rc = lib.sb_accept_sample_noalloc(ctx, 9, C.byref(t), fp, 1.0, fp, fp,
+                                          C.byref(out), None)
+        assert rc == B.SB_EBUDGET
+        assert b"65536" in lib.sb_last_error(ctx)
+        out_r = B.AcceptOut(fp, fp, fp, fp)
+        rc = lib.sb_accept_sample_noalloc(ctx, 1, C.byref(t), fp, 1.0, fp, fp,
+                                          C.byref(out_r), None)
+        assert rc == B.SB_ESTATE
+        rc = lib.sb_accept_sample_noalloc(ctx, 1, C.byref(t), fp, 0.0, fp, fp,
+                                          C.byref(out), None)
+        assert rc == B.SB_EINVAL
+        rc = lib.sb_accept_sample_noalloc(ctx, 17, C.byref(t), fp, 1.0, fp,
+                                          fp, C.byref(out), None)
+        assert rc == B.SB_ESHAPE
+    finally:
+        lib.sb_destroy(ctx)
