@@ -46,7 +46,7 @@ class Runtime:
 
     def __init__(self, w, weights=None, *, n_seqs=None, max_pages=None,
                  prefill_chunk=128, device="cuda", page_seed=3, seed=0,
-                 adapt_cap=0):
+                 adapt_cap=0, share_layers=False):
         self.lib = B.load()
         self.w = w
         self.dev = torch.device(device)
@@ -79,6 +79,9 @@ class Runtime:
         self.ctx = ctx
         self.row_cap = self.lib.sb_row_capacity(C.byref(cfg))
         self.et = elem_dtype(w.dtype)
+        # share_layers: every target layer's table entry points at layer 0's
+        # device weights (full-depth tests whose oracle shares one layer)
+        self.share_layers = share_layers
         self._weights(weights, seed)
         nbytes = self.lib.sb_workspace_bytes(C.byref(cfg))
         self.workspace = torch.empty(nbytes, dtype=torch.uint8,
@@ -141,8 +144,12 @@ class Runtime:
                                     ("attn_norm", "w_qkv", "w_o", "mlp_norm",
                                      "w_gate_up", "w_down", "w_shift")])
 
-        tl = (B.LayerWeights * s.n_layers)(*[layer(f"layers.{i}.", False)
-                                             for i in range(s.n_layers)])
+        if self.share_layers:
+            first = layer("layers.0.", False)
+            tl = (B.LayerWeights * s.n_layers)(*([first] * s.n_layers))
+        else:
+            tl = (B.LayerWeights * s.n_layers)(*[layer(f"layers.{i}.", False)
+                                                 for i in range(s.n_layers)])
         embed = get("embed", (s.vocab, d))
         tfin = get("final_norm", (d,), "ones")
         tlm = pack(get("lm_head", (s.vocab, d)))

@@ -223,12 +223,15 @@ def check_tree_exact(rt, s, tree, rows, lo, hi, tol_cum):
 
 
 def run_and_compare(rt, seqs, w, tgt, dr, tol, tally, log=print,
-                    forced=None):
+                    forced=None, deep_tol=None):
     """Drive one device iteration over all sequences, comparing the sampled
     ones; ``seqs`` maps seq -> (state before, state after, record, drafted
     tree).  The device's state for those sequences must equal the 'before'
     state when called.  ``forced``: [n_seqs][row_cap] buckets both sides
-    were given, or None."""
+    were given, or None.  ``deep_tol`` (default ``tol``) bounds the outputs
+    that went through the target's decoder stack: verify logits, taps, the
+    next condition taps and the committed target K/V."""
+    deep_tol = tol if deep_tol is None else deep_tol
     bmap = tuple(w.branch_map)
     for m in range(1, w.M + 1):
         log(f"expand {m}")
@@ -286,7 +289,7 @@ def run_and_compare(rt, seqs, w, tgt, dr, tol, tally, log=print,
         vl = host(rt.vout["logits"][offs[s]:offs[s] + n]).astype(np.float64)
         e = rel_err(vl, rec["verify_logits"])
         tally.worst_verify = max(tally.worst_verify, float(e.max()))
-        assert e.max() < tol, (s, e.max())
+        assert e.max() < deep_tol, (s, e.max())
         g = host(rt.vout["argmax"][s, :n])
         for j in range(n):
             assert g[j] == int(np.argmax(vl[j])), (s, j)
@@ -294,7 +297,7 @@ def run_and_compare(rt, seqs, w, tgt, dr, tol, tally, log=print,
             E = np.abs(vl[j] - z).max()
             assert z.max() - z[g[j]] <= 2 * E + 1e-6, (s, j)
         tap = host(rt.vout["taps"][s, :n]).reshape(n * 3, -1)
-        assert rel_err(tap, rec["taps"].reshape(n * 3, -1)).max() < tol, s
+        assert rel_err(tap, rec["taps"].reshape(n * 3, -1)).max() < deep_tol, s
         rt.vout["argmax"][s, :n] = torch.as_tensor(
             np.asarray(rec["greedy"], np.int32))
     log("accept, commit")
@@ -314,12 +317,13 @@ def run_and_compare(rt, seqs, w, tgt, dr, tol, tally, log=print,
         else:
             assert abs(rg - rr) <= 5e-2 * rr + 1e-7, (s, rg, rr)
         assert int(rt.T[s]) == after.T and int(rt.root[s]) == after.root
-        assert rel_err(host(rt.cond_taps[s]), after.cond_taps).max() < tol
+        assert rel_err(host(rt.cond_taps[s]), after.cond_taps).max() < deep_tol
         T0, n = before.T, after.T - before.T
         for which, ref in (("target", after.tkv), ("drafter", after.dkv)):
             k, v = rt.read_cache(which, s, n, T0)
+            bound = deep_tol if which == "target" else tol
             for layer in range(len(ref.k)):
                 for got, want in ((k[layer], ref.k[layer][T0:]),
                                   (v[layer], ref.v[layer][T0:])):
                     assert rel_err(got.reshape(n, -1),
-                                   want.reshape(n, -1)).max() < tol, (s, which)
+                                   want.reshape(n, -1)).max() < bound, (s, which)

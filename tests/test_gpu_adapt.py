@@ -49,8 +49,8 @@ CASES = {
 }
 
 
-@pytest.mark.parametrize("name", list(CASES))
-def test_head_update_matches_oracle(name):
+def _setup(name):
+    """Runtime, buffered positions, training copy and the oracle's step."""
     wname, vd, cap, n, lr = CASES[name]
     w = synth.with_layers(synth.WORKLOADS[wname], 1)
     if vd:
@@ -96,15 +96,43 @@ def test_head_update_matches_oracle(name):
         train["lm_head"].copy_(torch.as_tensor(wtf))
     rw0 = host(train["rank_w"]).astype(np.float64)
     rb0 = host(train["rank_b"]).astype(np.float64)
-    loss = torch.zeros(1, dtype=torch.float32, device=rt.dev)
     kl = 0.5
+    g = np.asarray(weights["d.final_norm"], np.float64)
+    return dict(w=w, s=s, d=d, V=V, Vd=Vd, bf16=bf16, weights=weights,
+                tgt=tgt, dr=dr, rt=rt, h=h, targets=targets, n=n, buf=buf, train=train,
+                lm0=lm0, wtf=wtf, w0f=w0f, rw0=rw0, rb0=rb0, lr=lr, kl=kl,
+                g=g, name=name)
+
+
+def _fill(c):
+    c["buf"]["h"][:c["n"]] = torch.as_tensor(c["h"])
+    c["buf"]["target"][:c["n"]] = torch.as_tensor(c["targets"])
+    c["buf"]["count"][0] = c["n"]
+
+
+def _fresh_train(c):
+    """A new training copy with the same initial values as c["train"]."""
+    return {k: v.clone() for k, v in c["train"].items()}
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_head_update_matches_oracle(name):
+    c = _setup(name)
+    loss = torch.zeros(1, dtype=torch.float32, device=c["rt"].dev)
     torch.cuda.synchronize()
     print(f"[{name}] update", flush=True)
-    rt.head_update(buf, lm0, train, lr, kl, loss)
+    c["rt"].head_update(c["buf"], c["lm0"], c["train"], c["lr"], c["kl"], loss)
     torch.cuda.synchronize()
-    assert int(buf["count"][0]) == 0
+    assert int(c["buf"]["count"][0]) == 0
+    _check_against_oracle(c, c["train"], loss)
+
+
+def _check_against_oracle(c, train, loss):
+    s, d, Vd, bf16, dr = c["s"], c["d"], c["Vd"], c["bf16"], c["dr"]
+    h, targets, wtf, w0f = c["h"], c["targets"], c["wtf"], c["w0f"]
+    rw0, rb0, lr, kl, g, name = (c["rw0"], c["rb0"], c["lr"], c["kl"],
+                                 c["g"], c["name"])
     # oracle step on the same values
-    g = np.asarray(weights["d.final_norm"], np.float64)
     nl, nr, nb, ref_loss = head_update(
         wtf.astype(np.float64), rw0, rb0, w0f.astype(np.float64),
         h.astype(np.float64), targets, g, s.norm_eps,
@@ -142,13 +170,73 @@ def test_head_update_matches_oracle(name):
             bad = np.argwhere(err > bound)
             print(f"[{name}] {len(bad)} elements out of bound; rows "
                   f"{np.unique(bad[:, 0])[:20]}", flush=True)
-            for r, c in bad[np.argsort(-(err / bound)[err > bound])][:8]:
-                print(f"  ({r},{c}) got {got[r, c]:.6g} want {want[r, c]:.6g} "
-                      f"old {wtf[r, c]:.6g} ref step {nl[r, c] - wtf[r, c]:.3g} "
-                      f"bound {bound[r, c]:.3g}", flush=True)
+            for r, j in bad[np.argsort(-(err / bound)[err > bound])][:8]:
+                print(f"  ({r},{j}) got {got[r, j]:.6g} want {want[r, j]:.6g} "
+                      f"old {wtf[r, j]:.6g} ref step {nl[r, j] - wtf[r, j]:.3g} "
+                      f"bound {bound[r, j]:.3g}", flush=True)
         assert (err <= bound).all()
         assert moved > 0 and exact > 0.99
     else:
         gotw = host(train["lm_head"]).astype(np.float64)
         dg, dref = gotw - wtf, nl - wtf
         assert np.abs(dg - dref).max() <= 1e-3 * np.abs(dref).max() + 1e-9
+
+
+def test_head_update_on_second_stream_beside_inference():
+    """Sec. 3.4: the head update runs on its own stream so that drafting is
+    not blocked.  The update of the paper-shaped drafter's head (second
+    stream, default priority) is enqueued and overlaps two block expansions
+    and a verify of the same context on the first stream.  Both must give
+    what they give alone: the inference outputs bit-identical to a solo run
+    of the same calls on the same state (whose parity with the oracle is
+    checked at this shape in test_gpu_configs), the updated heads
+    bit-identical to a solo update and within the oracle-step bounds of
+    test_head_update_matches_oracle, the loss as well."""
+    from test_gpu_configs import synthetic_state
+    from gpu_harness import inject
+    c = _setup("8b-paper-drafter")
+    rt, w = c["rt"], c["w"]
+    # a committed state to draft and verify from (seeded random K/V)
+    st = synthetic_state(w, c["tgt"], c["dr"], 0, 1024, 5)
+    inject(rt, 0, st)
+
+    def infer():
+        for m in range(1, w.M + 1):
+            rt.expand(m, want_logits=True)
+        rt.verify(want_logits=True)
+
+    def snap():
+        out = {f"d.{k}": v.clone() for k, v in rt.dout.items()
+               if isinstance(v, torch.Tensor)}
+        out.update({f"t.{k}": v.clone() for k, v in rt.tree.items()})
+        out.update({f"v.{k}": v.clone() for k, v in rt.vout.items()
+                    if isinstance(v, torch.Tensor)})
+        return out
+
+    print("[stream] solo inference and solo update", flush=True)
+    infer()
+    torch.cuda.synchronize()
+    ref = snap()
+    solo = _fresh_train(c)
+    loss_solo = torch.zeros(1, dtype=torch.float32, device=rt.dev)
+    rt.head_update(c["buf"], c["lm0"], solo, c["lr"], c["kl"], loss_solo)
+    torch.cuda.synchronize()
+    print("[stream] concurrent", flush=True)
+    _fill(c)
+    conc = _fresh_train(c)
+    loss_conc = torch.zeros(1, dtype=torch.float32, device=rt.dev)
+    side = torch.cuda.Stream(device=rt.dev)   # default priority
+    side.wait_stream(torch.cuda.current_stream(rt.dev))
+    rt.head_update(c["buf"], c["lm0"], conc, c["lr"], c["kl"], loss_conc,
+                   stream=side)
+    infer()
+    torch.cuda.current_stream(rt.dev).wait_stream(side)
+    torch.cuda.synchronize()
+    got = snap()
+    for k in ref:
+        assert torch.equal(got[k], ref[k]), k
+    for k in solo:
+        assert torch.equal(conc[k], solo[k]), k
+    assert torch.equal(loss_conc, loss_solo)
+    assert int(c["buf"]["count"][0]) == 0
+    _check_against_oracle(c, conc, loss_conc)

@@ -64,19 +64,29 @@ def log(msg):
 
 @pytest.mark.parametrize("name", list(CASES))
 def test_iteration_full_layer_shape(name):
-    _iteration(name, paper_buckets=False)
+    _iteration(name, buckets="natural")
 
 
 @pytest.mark.parametrize("name", ["8b-k4", "8b-batch16-paged"])
 def test_iteration_paper_frequency_buckets(name):
     """The same comparison with every drafter row's bucket forced from the
     seeded paper-frequency draws (both sides read the same array)."""
-    _iteration(name, paper_buckets=True)
+    _iteration(name, buckets="paper")
 
 
-def _iteration(name, paper_buckets):
+@pytest.mark.parametrize("name", ["8b-k4"])
+def test_iteration_uniform_tree(name):
+    """The uniform fixed-3 tree at the same budget (the rank-guided
+    branching ablation, Sec. 4): every row forced into b1 with the
+    branching map (3, 3, 3, 3), on both sides."""
+    _iteration(name, buckets="uniform")
+
+
+def _iteration(name, buckets):
     wname, layers, sample = CASES[name]
     w = synth.with_layers(synth.WORKLOADS[wname], layers)
+    if buckets == "uniform":
+        w = synth.uniform_tree(w, 3)
     log(f"[{name}] weights")
     weights, tgt, dr = models(w)
     lens = synth.prompt_lengths(w)
@@ -89,8 +99,11 @@ def _iteration(name, paper_buckets):
     for s, st in enumerate(states):
         inject(rt, s, st)
     forced = None
-    if paper_buckets:
+    if buckets == "paper":
         forced = synth.paper_buckets(7, 0, w.n_seqs, rt.row_cap)
+    elif buckets == "uniform":
+        forced = synth.uniform_buckets(w.n_seqs, rt.row_cap)
+    if forced is not None:
         rt.set_buckets(torch.as_tensor(forced).to(rt.dev))
     seqs = {}
     for s in sample:
