@@ -250,7 +250,10 @@ const char* sb_last_error(const sb_ctx* ctx);
  * pointers, a d2t that is not strictly increasing in [0, vocab)),
  * SB_EBUDGET (workspace too small), SB_EHIP (reading d2t failed).
  * SB_BF16: the projection matrices must have been packed by sb_pack_weight
- * (w_gate_up with gate_up = 1, the others with 0). */
+ * (w_gate_up with gate_up = 1, the others with 0).  With SB_BF16 the first
+ * drafter forward after sb_bind caches W_fuse's q_k part (the last d columns
+ * of W_fuse applied to norm_q(q_k), k = 1..K; Eq. 2) in the workspace; bind
+ * again after changing w_fuse, norm_q or pos_query. */
 int sb_bind(sb_ctx* ctx, const sb_target_weights* target,
             const sb_drafter_weights* drafter, void* workspace,
             size_t workspace_bytes);

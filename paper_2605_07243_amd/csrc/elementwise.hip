@@ -166,17 +166,23 @@ __device__ __forceinline__ void sum_parts2(const float* __restrict__ P,
 
 // One workgroup of 1024 threads per row: thread t owns float4 columns
 // t, t + 1024 (d <= 8192), summed over the partials in one pass.
+// add_rows != nullptr adds row add_rows[add_idx[i] - 1] (fp32 [.][d]) to
+// the partial sum.
 template <typename T>
 __global__ __launch_bounds__(1024) void residual_kernel(
     float* __restrict__ x, const float* __restrict__ P, int ks,
     size_t part_stride, const int* __restrict__ n, int d, int accumulate,
     const float* __restrict__ g, float eps, T* __restrict__ out, int ldo,
-    float* __restrict__ taps, int tap_mask, const int* __restrict__ out_row) {
+    float* __restrict__ taps, int tap_mask, const int* __restrict__ out_row,
+    const float* __restrict__ add_rows, const int* __restrict__ add_idx) {
   constexpr int MAXV = 2;
   __shared__ float red[16];
   const int i = blockIdx.x;
   if (i >= *n) return;
   float* xr = x + (size_t)i * d;
+  const float4* ar = add_rows != nullptr
+      ? reinterpret_cast<const float4*>(add_rows + (size_t)(add_idx[i] - 1) * d)
+      : nullptr;
   float* tr = nullptr;
   if (taps != nullptr && tap_mask != 0 && out_row[i] >= 0)
     tr = taps + (size_t)out_row[i] * 3 * d;
@@ -206,6 +212,7 @@ __global__ __launch_bounds__(1024) void residual_kernel(
     const int c = threadIdx.x + q * 1024;
     if (c < nv) {
       float4 a = v[q];
+      if (ar != nullptr) a = add4(a, ar[c]);
       if (accumulate) a = add4(a, reinterpret_cast<const float4*>(xr)[c]);
       reinterpret_cast<float4*>(xr)[c] = a;
       if (tr) {
@@ -236,10 +243,12 @@ template <typename T>
 void launch_residual(float* x, const float* P, int ks, size_t part_stride,
                      const int* n, int cap, int d, bool accumulate,
                      const float* g, float eps, T* out, int ldo, float* taps,
-                     int tap_mask, const int* out_row, hipStream_t st) {
+                     int tap_mask, const int* out_row, hipStream_t st,
+                     const float* add_rows, const int* add_idx) {
   residual_kernel<T><<<cap, 1024, 0, st>>>(x, P, ks, part_stride, n, d,
                                            accumulate ? 1 : 0, g, eps, out, ldo,
-                                           taps, tap_mask, out_row);
+                                           taps, tap_mask, out_row, add_rows,
+                                           add_idx);
 }
 
 // RoPE (rotate-half pairs (j, j + hd/2), angle pos * theta^(-2j/hd)) on the
@@ -388,12 +397,15 @@ void launch_shift_prep(const float* h, const CallPlan& p, int d, T* out,
 // Drafter input fusion operand (Eq. 2): [norm_c(c), norm_e(embed(x)),
 // norm_q(q_k)], each an RMSNorm with its own gain; all three rows are
 // loaded at once and their sums of squares reduced together.
+// With parts == 2 only [norm_c(c), norm_e(embed(x))] is written (row stride
+// 2d): the norm_q(q_k) third is then applied through cached rows (Eq. 2's
+// split of W_fuse, see the engine).
 template <typename T>
 __global__ __launch_bounds__(kRowThreads) void fuse_prep_kernel(
     const float* __restrict__ cond, CallPlan p, const T* __restrict__ E,
     const T* __restrict__ Q, const float* __restrict__ gc,
     const float* __restrict__ ge, const float* __restrict__ gq, float eps,
-    int d, T* __restrict__ out) {
+    int d, T* __restrict__ out, int parts) {
   __shared__ float red[3][16];
   const int i = blockIdx.x;
   if (i >= *p.n) return;
@@ -428,7 +440,7 @@ __global__ __launch_bounds__(kRowThreads) void fuse_prep_kernel(
     for (int q = 0; q < (int)(blockDim.x >> 6); ++q) t += red[j][q];
     r[j] = 1.0f / sqrtf(t / (float)d + eps);
   }
-  T* o = out + (size_t)i * 3 * d;
+  T* o = out + (size_t)i * parts * d;
 #pragma unroll
   for (int q = 0; q < kRowVec; ++q) {
     const int c = threadIdx.x + q * kRowThreads;
@@ -436,18 +448,53 @@ __global__ __launch_bounds__(kRowThreads) void fuse_prep_kernel(
       // a zero condition stays zero (0 * finite scale)
       store4<T>(o + 4 * c, scale4(vc[q], r[0], reinterpret_cast<const float4*>(gc)[c]));
       store4<T>(o + d + 4 * c, scale4(ve[q], r[1], reinterpret_cast<const float4*>(ge)[c]));
-      store4<T>(o + 2 * d + 4 * c, scale4(vq[q], r[2], reinterpret_cast<const float4*>(gq)[c]));
+      if (parts == 3)
+        store4<T>(o + 2 * d + 4 * c, scale4(vq[q], r[2], reinterpret_cast<const float4*>(gq)[c]));
     }
   }
+}
+
+// out[k] = rmsnorm(src[k]) * g as T for the first n rows of src (T rows).
+template <typename T>
+__global__ __launch_bounds__(kRowThreads) void norm_rows_kernel(
+    const T* __restrict__ src, int d, const float* __restrict__ g, float eps,
+    T* __restrict__ out) {
+  __shared__ float red[16];
+  const int i = blockIdx.x;
+  const T* sr = src + (size_t)i * d;
+  float4 v[kRowVec];
+  float ss = 0.f;
+#pragma unroll
+  for (int q = 0; q < kRowVec; ++q) {
+    const int c = threadIdx.x + q * kRowThreads;
+    v[q] = c < d / 4 ? load4<T>(sr + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
+    ss += sumsq4(v[q]);
+  }
+  ss = block_sum(ss, red);
+  const float r = 1.0f / sqrtf(ss / (float)d + eps);
+  T* o = out + (size_t)i * d;
+#pragma unroll
+  for (int q = 0; q < kRowVec; ++q) {
+    const int c = threadIdx.x + q * kRowThreads;
+    if (c < d / 4)
+      store4<T>(o + 4 * c, scale4(v[q], r, reinterpret_cast<const float4*>(g)[c]));
+  }
+}
+
+template <typename T>
+void launch_norm_rows(const T* src, int n_rows, int d, const float* g,
+                      float eps, T* out, hipStream_t st) {
+  norm_rows_kernel<T><<<n_rows, kRowThreads, 0, st>>>(src, d, g, eps, out);
 }
 
 template <typename T>
 void launch_fuse_prep(const float* cond, const CallPlan& p, const T* embed,
                       const T* pos_query, const float* gc, const float* ge,
-                      const float* gq, float eps, int d, T* out,
+                      const float* gq, float eps, int d, T* out, int parts,
                       hipStream_t st) {
   fuse_prep_kernel<T><<<p.cap, kRowThreads, 0, st>>>(cond, p, embed, pos_query,
-                                                     gc, ge, gq, eps, d, out);
+                                                     gc, ge, gq, eps, d, out,
+                                                     parts);
 }
 
 // out[i] = T(src[idx[i]]) (idx null: identity), rows of w floats; one
@@ -479,7 +526,9 @@ void launch_rows_to_elem(const float* src, const int* idx, const int* n,
   template void launch_residual<T>(float*, const float*, int, size_t,          \
                                    const int*, int, int, bool, const float*,   \
                                    float, T*, int, float*, int, const int*,    \
-                                   hipStream_t);                               \
+                                   hipStream_t, const float*, const int*);     \
+  template void launch_norm_rows<T>(const T*, int, int, const float*, float,   \
+                                    T*, hipStream_t);                          \
   template void launch_qkv_post<T>(const float*, int, size_t, const CallPlan&, \
                                    int, int, int, float, T*, void*, void*,     \
                                    int, hipStream_t);                          \
@@ -489,7 +538,7 @@ void launch_rows_to_elem(const float* src, const int* idx, const int* n,
                                      hipStream_t);                             \
   template void launch_fuse_prep<T>(const float*, const CallPlan&, const T*,   \
                                     const T*, const float*, const float*,      \
-                                    const float*, float, int, T*,              \
+                                    const float*, float, int, T*, int,         \
                                     hipStream_t);                              \
   template void launch_rows_to_elem<T>(const float*, const int*, const int*,   \
                                        int, int, T*, hipStream_t);

@@ -92,6 +92,7 @@ Dims derive(const sb_config& c) {
   upd(D.d, D.F);
   upd(D.d, 3 * D.d);
   upd(D.d, 2 * D.d);
+  upd(D.d, D.d);
   D.part_elems = mx * D.R_cap;
   return D;
 }
@@ -142,6 +143,10 @@ struct sb_ctx {
   int* blk_row0 = nullptr;
   int* blk_nst = nullptr;
   int* prof_rows = nullptr;      // [kProfSlots] rows of profiled GEMM launches
+  // Eq. 2 split (bf16): vq[k] = W_f3 norm_q(q_{k+1}), cached per bind
+  float* vq = nullptr;           // [K][d]
+  int* vq_n = nullptr;           // [1] = K on the device
+  bool vq_ready = false;
   CommitInfo ci{};
   CallPlan plan{};
   CallPlan fb{};
@@ -225,6 +230,8 @@ static size_t layout(const Dims& D, void* base, sb_ctx* c) {
   int* blk_row0 = cv.take<int>(D.S * 4);
   int* blk_nst = cv.take<int>(D.S * 4);
   int* prof_rows = cv.take<int>((size_t)kProfSlots * 4);
+  float* vq = cv.take<float>((size_t)D.K * D.d * 4);
+  int* vq_n = cv.take<int>(4);
   CommitInfo ci{cv.take<int>(D.S * 4), cv.take<int>(D.S * 4),
                 cv.take<int>(D.S * 4), cv.take<int>(D.S * 4)};
   auto make_plan = [&](int cap) {
@@ -280,6 +287,8 @@ static size_t layout(const Dims& D, void* base, sb_ctx* c) {
     c->blk_row0 = blk_row0;
     c->blk_nst = blk_nst;
     c->prof_rows = prof_rows;
+    c->vq = vq;
+    c->vq_n = vq_n;
     c->ci = ci;
     c->plan = plan;
     c->fb = fb;
@@ -537,6 +546,7 @@ int sb_bind(sb_ctx* c, const sb_target_weights* tw,
   c->dl.assign(dw->layers, dw->layers + c->D.LD);
   c->dw.layers = c->dl.data();
   layout(c->D, ws, c);
+  c->vq_ready = false;
   c->bound = true;
   return SB_OK;
 }
@@ -774,14 +784,36 @@ void drafter_forward(sb_ctx* c, const CallPlan& p, const float* cond_base,
   const int R = p.cap;
   T* A = static_cast<T*>(c->A);
   c->prof_group = SB_GEMM_DRAFTER;
+  // Eq. 2: h0_k = W_f1 n_c(c) + W_f2 n_e(e) + W_f3 n_q(q_k).  With bf16 the
+  // packed W_fuse splits into its first 2d columns and its last d columns
+  // (both contiguous packed matrices, the packing being K-block-major), and
+  // the q_k part, which depends on the weights only, is computed once per
+  // bind and added by the residual kernel: each call streams 2d x d of
+  // W_fuse instead of 3d x d.
+  const bool split = sizeof(T) == 2;
+  if (split && !c->vq_ready) {
+    launch_set_int(c->vq_n, D.K, st);
+    launch_norm_rows<T>(static_cast<const T*>(c->dw.pos_query), D.K, D.d,
+                        static_cast<const float*>(c->dw.norm_q), eps, A, st);
+    const T* wf3 = static_cast<const T*>(c->dw.w_fuse) + (size_t)2 * D.d * D.d;
+    const int kq = gemm<T>(c, A, D.d, wf3, D.d, D.d, c->vq_n, D.K, st);
+    launch_residual<T>(c->vq, c->P, kq, (size_t)D.R_cap * D.d, c->vq_n, D.K,
+                       D.d, false, nullptr, eps, A, D.d, nullptr, 0, nullptr,
+                       st);
+    c->vq_ready = true;
+  }
+  const int parts = split ? 2 : 3;
   launch_fuse_prep<T>(cond_base, p, static_cast<const T*>(c->tw.embed),
                       static_cast<const T*>(c->dw.pos_query),
                       static_cast<const float*>(c->dw.norm_c),
                       static_cast<const float*>(c->dw.norm_e),
-                      static_cast<const float*>(c->dw.norm_q), eps, D.d, A, st);
-  int ks = gemm<T>(c, A, 3 * D.d, c->dw.w_fuse, D.d, 3 * D.d, p.n, R, st);
+                      static_cast<const float*>(c->dw.norm_q), eps, D.d, A,
+                      parts, st);
+  int ks = gemm<T>(c, A, parts * D.d, c->dw.w_fuse, D.d, parts * D.d, p.n, R,
+                   st);
   launch_residual<T>(c->x, c->P, ks, (size_t)D.R_cap * D.d, p.n, R, D.d, false,
-                     nullptr, eps, A, D.d, nullptr, 0, nullptr, st);
+                     nullptr, eps, A, D.d, nullptr, 0, nullptr, st,
+                     split ? c->vq : nullptr, split ? p.k : nullptr);
   for (int l = 0; l < D.LD; ++l) {
     const sb_layer_weights& lw = c->dw.layers[l];
     launch_shift_prep<T>(c->x, p, D.d, A, st);
@@ -841,9 +873,9 @@ int draft_expand_impl(sb_ctx* c, int m, const sb_seqs* sq, const sb_kv* dkv,
     cond_rows<T>(c, sq->cond_taps, nullptr, c->n_aux, D.S, st);
     cond_base = c->cond_buf;
   }
-  launch_plan_block(td, m, *t, sq->T, p, c->blk_row0, c->blk_nst, st);
-  launch_export_rows(p, D.S * D.B_max * D.K, o->call_seq, o->call_row,
-                     o->n_call, st);
+  launch_plan_block(td, m, *t, sq->T, p, c->blk_row0, c->blk_nst,
+                    D.S * D.B_max * D.K, o->call_seq, o->call_row, o->n_call,
+                    st);
   const Prefix pf{dkv, c->dseg_k, c->dseg_v, D.dpages};
   drafter_forward<T>(c, p, cond_base, pf, D.B_max * D.K, true, st);
   float* logits = o->logits ? o->logits : c->logits;

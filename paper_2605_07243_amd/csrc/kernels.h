@@ -91,11 +91,19 @@ void launch_rmsnorm(const float* x, const int* n, int cap, int d,
                     hipStream_t st);
 // x = (accumulate ? x : 0) + sum_ks P[ks]; then optionally out = rmsnorm(x)*g
 // and taps[out_row][j] = x for every bit j of tap_mask.
+// add_rows (optional, fp32 [.][d]): row add_rows[add_idx[i] - 1] is added
+// to row i's partial sum before the residual.
 template <typename T>
 void launch_residual(float* x, const float* P, int ks, size_t part_stride,
                      const int* n, int cap, int d, bool accumulate,
                      const float* g, float eps, T* out, int ldo, float* taps,
-                     int tap_mask, const int* out_row, hipStream_t st);
+                     int tap_mask, const int* out_row, hipStream_t st,
+                     const float* add_rows = nullptr,
+                     const int* add_idx = nullptr);
+// out[k] = rmsnorm(src[k]) * g for rows k < n_rows (T rows of width d).
+template <typename T>
+void launch_norm_rows(const T* src, int n_rows, int d, const float* g,
+                      float eps, T* out, hipStream_t st);
 template <typename T>
 void launch_qkv_post(const float* P, int ks, size_t part_stride,
                      const CallPlan& p, int H, int Hkv, int hd, float theta,
@@ -107,10 +115,12 @@ void launch_swiglu(const float* P, int ks, size_t part_stride, const int* n,
 template <typename T>
 void launch_shift_prep(const float* h, const CallPlan& p, int d, T* out,
                        hipStream_t st);
+// Eq. 2 operand rows [norm_c(c), norm_e(embed(x)), norm_q(q_k)] (parts 3,
+// row stride 3d) or without the q_k third (parts 2, row stride 2d).
 template <typename T>
 void launch_fuse_prep(const float* cond, const CallPlan& p, const T* embed,
                       const T* pos_query, const float* gc, const float* ge,
-                      const float* gq, float eps, int d, T* out,
+                      const float* gq, float eps, int d, T* out, int parts,
                       hipStream_t st);
 // out[i] = T(src[idx[i]]) rows of width w (idx == nullptr: identity).
 template <typename T>
@@ -191,9 +201,12 @@ struct KVPools {
 };
 void launch_block1_reset(const TreeDims& td, const sb_tree& t, const int* root,
                          int* n_aux, hipStream_t st);
+// Rows of one block expansion; also exports them (call_seq / call_row
+// [out_cap], -1 past the call's rows, n_call).
 void launch_plan_block(const TreeDims& td, int m, const sb_tree& t,
                        const int* T, const CallPlan& p, int* blk_row0,
-                       int* blk_nst, hipStream_t st);
+                       int* blk_nst, int out_cap, int* call_seq,
+                       int* call_row, int* n_call, hipStream_t st);
 void launch_attach(const TreeDims& td, const sb_tree& t, const sb_draft_out& o,
                    const int* blk_row0, const int* blk_nst, hipStream_t st);
 void launch_plan_verify(const TreeDims& td, const sb_tree& t, const int* T,
@@ -268,7 +281,5 @@ void launch_copy_f32(float* dst, const float* src, int n, hipStream_t st);
 void launch_set_int(int* p, int v, hipStream_t st);
 // *dst = *src (one thread; e.g. a row count captured for the profiler)
 void launch_copy_int(int* dst, const int* src, hipStream_t st);
-void launch_export_rows(const CallPlan& p, int out_cap, int* call_seq,
-                        int* call_row, int* n_call, hipStream_t st);
 
 }  // namespace sb

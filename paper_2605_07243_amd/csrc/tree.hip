@@ -49,10 +49,15 @@ __global__ void block1_reset_kernel(TreeDims td, sb_tree t,
 // Rows of one block expansion: start b of sequence s gets rows k = 1..K at
 // positions pos(start) + k; they see the rows visible to the row that
 // proposed the start plus their own block's rows <= k.
+// The call rows are also exported (call_seq / call_row [out_cap], -1 past
+// the rows, n_call).
 __global__ void plan_block_kernel(TreeDims td, int m, sb_tree t,
                                   const int* __restrict__ T, CallPlan p,
                                   int* __restrict__ blk_row0,
-                                  int* __restrict__ blk_nst) {
+                                  int* __restrict__ blk_nst, int out_cap,
+                                  int* __restrict__ call_seq,
+                                  int* __restrict__ call_row,
+                                  int* __restrict__ n_call) {
   __shared__ int cnt[SB_MAX_SEQS], old[SB_MAX_SEQS], off[SB_MAX_SEQS];
   const int K = td.K, rw = td.rw;
   if (threadIdx.x == 0) {
@@ -73,13 +78,21 @@ __global__ void plan_block_kernel(TreeDims td, int m, sb_tree t,
     }
     p.seq_off[td.S] = o;
     *p.n = o;
+    *n_call = o;
   }
   __syncthreads();
+  for (int i = off[td.S - 1] + cnt[td.S - 1] + threadIdx.x; i < out_cap;
+       i += blockDim.x) {
+    call_seq[i] = -1;
+    call_row[i] = -1;
+  }
   for (int s = 0; s < td.S; ++s) {
     for (int j = threadIdx.x; j < cnt[s]; j += blockDim.x) {
       const int b = j / K, k = j % K + 1;
       const int i = off[s] + j;
       const int lr = old[s] + j;
+      call_seq[i] = s;
+      call_row[i] = lr;
       const int sn = t.starts[(size_t)s * td.B_max + b];
       const size_t nidx = (size_t)s * td.budget + sn;
       const int srow = t.row[nidx];
@@ -564,19 +577,6 @@ __global__ void copy_int_kernel(int* __restrict__ dst,
   *dst = *src;
 }
 
-__global__ void export_rows_kernel(CallPlan p, int out_cap,
-                                   int* __restrict__ call_seq,
-                                   int* __restrict__ call_row,
-                                   int* __restrict__ n_call) {
-  const int n = *p.n;
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < out_cap;
-       i += gridDim.x * blockDim.x) {
-    call_seq[i] = i < n ? p.seq[i] : -1;
-    call_row[i] = i < n ? p.slot[i] : -1;
-  }
-  if (blockIdx.x == 0 && threadIdx.x == 0) *n_call = n;
-}
-
 // ---------------------------------------------------------------------------
 // launchers
 
@@ -586,8 +586,10 @@ void launch_block1_reset(const TreeDims& td, const sb_tree& t, const int* root,
 }
 void launch_plan_block(const TreeDims& td, int m, const sb_tree& t,
                        const int* T, const CallPlan& p, int* blk_row0,
-                       int* blk_nst, hipStream_t st) {
-  plan_block_kernel<<<1, 256, 0, st>>>(td, m, t, T, p, blk_row0, blk_nst);
+                       int* blk_nst, int out_cap, int* call_seq,
+                       int* call_row, int* n_call, hipStream_t st) {
+  plan_block_kernel<<<1, 256, 0, st>>>(td, m, t, T, p, blk_row0, blk_nst,
+                                       out_cap, call_seq, call_row, n_call);
 }
 void launch_attach(const TreeDims& td, const sb_tree& t, const sb_draft_out& o,
                    const int* blk_row0, const int* blk_nst, hipStream_t st) {
@@ -803,11 +805,6 @@ void launch_set_int(int* p, int v, hipStream_t st) {
 }
 void launch_copy_int(int* dst, const int* src, hipStream_t st) {
   copy_int_kernel<<<1, 1, 0, st>>>(dst, src);
-}
-void launch_export_rows(const CallPlan& p, int out_cap, int* call_seq,
-                        int* call_row, int* n_call, hipStream_t st) {
-  export_rows_kernel<<<(out_cap + 255) / 256, 256, 0, st>>>(
-      p, out_cap, call_seq, call_row, n_call);
 }
 
 template void launch_commit_copy<float>(const TreeDims&, const sb_tree&,
