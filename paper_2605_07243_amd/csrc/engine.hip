@@ -41,7 +41,7 @@ struct Carver {
 struct Dims {
   int S, d, H, Hkv, hd, F, V, Vd, L, LD, qkv_n, es;
   int K, M, B_max, budget, row_cap, rw, bw, vis_words, R_cap, chunk;
-  int tpages, dpages, n_chunks, n_chunks_d, n_split;
+  int tpages, dpages, n_chunks, n_chunks_d, n_chunks_f, n_split;
   int adapt_cap;
   size_t part_elems;
 };
@@ -80,6 +80,9 @@ Dims derive(const sb_config& c) {
   D.n_chunks = std::max({1, std::min(64, D.V / 2048), min_v});
   D.n_chunks_d = std::max({1, std::min(64, D.Vd / 2048), min_vd});
   D.adapt_cap = c.adapt_cap;
+  // column tiles of the LM heads' fused reduction (at most one per 128
+  // vocabulary ids)
+  D.n_chunks_f = (std::max(D.V, D.Vd) + 127) / 128;
   D.n_split = 32;
   // partial-sum buffer: the largest ks * N over the projections
   size_t mx = 0;
@@ -219,7 +222,8 @@ static size_t layout(const Dims& D, void* base, sb_ctx* c) {
   int* ad_n = cv.take<int>(4);
   float2* node_stats = cv.take<float2>((size_t)D.S * D.budget *
                                        sample_tiles(D.V) * 8);
-  float* vpart = cv.take<float>(R * D.n_chunks * kVocabRec10 * 4);
+  float* vpart = cv.take<float>(R * std::max(D.n_chunks, D.n_chunks_f) *
+                                 kVocabRec10 * 4);
   float* cond_buf = cv.take<float>(R * D.d * 4);
   float* taps_pf = cv.take<float>((size_t)(D.chunk + 1) * 3 * D.d * 4);
   int* taps_idx = cv.take<int>(R * 4);
@@ -606,11 +610,14 @@ struct ProfScope {
   // GEMM launch shape: N x K weights of `es` bytes per element, `n` live
   // rows of capacity m_cap, out_es bytes per output element (4: fp32 rows
   // of N; the SwiGLU projection writes N / 2 bf16 values per row)
+  // (out_row >= 0: bytes written per row, e.g. the vocabulary records of
+  // the fused LM heads)
   ProfScope(sb_ctx* c_, hipStream_t st_, const int* n, int m_cap, int N,
-            int K, double es, bool swiglu, int group)
+            int K, double es, bool swiglu, int group, double out_row = -1.0)
       : ProfScope(c_, st_, SB_PROF_GEMM,
                   (double)N * K * es + (double)m_cap * K * es +
-                      (double)m_cap * (swiglu ? N / 2 * es : N * 4.0),
+                      (double)m_cap * (out_row >= 0.0 ? out_row
+                                       : swiglu ? N / 2 * es : N * 4.0),
                   2.0 * m_cap * N * K) {
     if (!a) return;
     rows = n;
@@ -618,7 +625,7 @@ struct ProfScope {
     g.m_cap = m_cap;
     g.w_bytes = (double)N * K * es;
     g.in_row = (double)K * es;
-    g.out_row = swiglu ? N / 2 * es : N * 4.0;
+    g.out_row = out_row >= 0.0 ? out_row : swiglu ? N / 2 * es : N * 4.0;
     g.flops_row = 2.0 * N * K;
   }
   ~ProfScope() {
@@ -854,6 +861,36 @@ void lm_head(sb_ctx* c, const void* A, const void* W, int V, float* logits,
                      V, D.d, logits, (size_t)cap * V, n, cap, 1, st);
 }
 
+// LM head with the vocabulary reduction.  bf16 greedy verification (top-1)
+// runs it in the GEMM epilogue: chunk records straight from the
+// accumulators, logits written only when the caller asked for them.  The
+// drafter's top-10 (and f32) write the logits and reduce them in a second
+// pass: a top-10 merge in the epilogue measured slower than that pass at
+// the 8B shape (0.42 vs 0.40 ms per block).  Returns the chunk records per
+// row in c->vpart.
+template <typename T>
+int lm_head_reduce(sb_ctx* c, const void* W, int V, float* logits_out,
+                   const int* n, int cap, int topk, int max_chunks,
+                   hipStream_t st) {
+  const Dims& D = c->D;
+  if (sizeof(T) == 2 && topk == 1) {
+    const int nc = gemm_vocab_chunks(V, D.d, cap);
+    const double out_row = (double)nc * (2 * topk + 3) * 4 +
+                           (logits_out != nullptr ? (double)V * 4 : 0.0);
+    ProfScope ps(c, st, n, cap, V, D.d, sizeof(T), false, SB_GEMM_LM_HEAD,
+                 out_row);
+    return launch_gemm_vocab(static_cast<const bf16_t*>(c->A), D.d,
+                             static_cast<const bf16_t*>(W), V, D.d,
+                             logits_out, n, cap, topk, c->vpart, st);
+  } else {
+    float* logits = logits_out ? logits_out : c->logits;
+    lm_head<T>(c, c->A, W, V, logits, n, cap, st);
+    ProfScope ps(c, st, SB_PROF_VOCAB);
+    return launch_vocab_partial(logits, n, cap, V, max_chunks, topk, c->vpart,
+                                st);
+  }
+}
+
 TreeDims tree_dims(const sb_ctx* c, int n_seqs) {
   const Dims& D = c->D;
   return TreeDims{n_seqs, D.K, D.M, D.B_max, D.budget, D.bw, D.row_cap, D.rw, D.d};
@@ -878,13 +915,11 @@ int draft_expand_impl(sb_ctx* c, int m, const sb_seqs* sq, const sb_kv* dkv,
                     st);
   const Prefix pf{dkv, c->dseg_k, c->dseg_v, D.dpages};
   drafter_forward<T>(c, p, cond_base, pf, D.B_max * D.K, true, st);
-  float* logits = o->logits ? o->logits : c->logits;
-  lm_head<T>(c, c->A, c->dw.lm_head, D.Vd, logits, p.n, p.cap, st);
+  const int n_chunks = lm_head_reduce<T>(c, c->dw.lm_head, D.Vd, o->logits,
+                                         p.n, p.cap, SB_TOPK, D.n_chunks_d,
+                                         st);
   {
     ProfScope ps(c, st, SB_PROF_VOCAB);
-    const int n_chunks = launch_vocab_partial(logits, p.n, p.cap, D.Vd,
-                                              D.n_chunks_d, SB_TOPK, c->vpart,
-                                              st);
     const DraftRowOut ro{o->topk_id, o->topk_logit, o->lse, o->psi,
                          o->bucket, o->branch, t->h_last, c->bucket_in,
                          c->dw.d2t, c->row_lse, D.Vd, D.row_cap};
@@ -910,12 +945,10 @@ int verify_impl(sb_ctx* c, const sb_seqs* sq, const sb_tree* t,
   launch_plan_verify(td, *t, sq->T, p, st);
   const Prefix pf{tkv, c->tseg_k, c->tseg_v, D.tpages};
   target_forward<T>(c, p, pf, D.budget, out->taps, st);
-  float* logits = out->logits ? out->logits : c->logits;
-  lm_head<T>(c, c->A, c->tw.lm_head, D.V, logits, p.n, p.cap, st);
+  const int n_chunks = lm_head_reduce<T>(c, c->tw.lm_head, D.V, out->logits,
+                                         p.n, p.cap, 1, D.n_chunks, st);
   {
     ProfScope ps(c, st, SB_PROF_VOCAB);
-    const int n_chunks =
-        launch_vocab_partial(logits, p.n, p.cap, D.V, D.n_chunks, 1, c->vpart, st);
     launch_verify_finalize(c->vpart, n_chunks, p.n, p.cap, p.out_row,
                            out->argmax, st);
   }

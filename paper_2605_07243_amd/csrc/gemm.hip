@@ -37,6 +37,7 @@
 //
 // f32 (gemm_xwt_kernel): row-major weights, fragments load straight into
 // registers and eight v_mfma_f32_16x16x4_f32 per 32-wide step.
+#include <float.h>
 #include <hip/hip_ext.h>
 
 #include <algorithm>
@@ -61,14 +62,51 @@ __device__ __forceinline__ f32x16_t mma_32x32x16(u32x4_t a, u32x4_t b,
 
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
 
+// Vocabulary records of the LM-head epilogue (the same record the separate
+// reduction writes: KT values, KT ids as int bits, then m, s = sum exp(z - m)
+// and u = sum exp(z - m) z).  Top-KT keeps the larger value first, equal
+// values ordered by the smaller id.
+template <int KT>
+__device__ __forceinline__ void vr_insert(float (&tv)[KT], int (&ti)[KT],
+                                          float v, int id) {
+  if (!better(v, id, tv[KT - 1], ti[KT - 1])) return;
+  tv[KT - 1] = v;
+  ti[KT - 1] = id;
+#pragma unroll
+  for (int j = KT - 1; j > 0; --j) {
+    if (better(tv[j], ti[j], tv[j - 1], ti[j - 1])) {
+      const float a = tv[j];
+      tv[j] = tv[j - 1];
+      tv[j - 1] = a;
+      const int b = ti[j];
+      ti[j] = ti[j - 1];
+      ti[j - 1] = b;
+    }
+  }
+}
+
+__device__ __forceinline__ void vr_stats_merge(float& m, float& s, float& u,
+                                               float m2, float s2, float u2) {
+  const float M = fmaxf(m, m2);
+  const float a = (s > 0.f) ? __expf(m - M) : 0.f;
+  const float b = (s2 > 0.f) ? __expf(m2 - M) : 0.f;
+  s = s * a + s2 * b;
+  u = u * a + u2 * b;
+  m = M;
+}
+
 // MF: 32-row activation tiles per workgroup; NF: 32-row weight fragments
 // per wave; PF: K-stages (64 columns each) of weights in flight per wave.
-template <int MF, int NF, int PF, bool SWIGLU>
+// VR > 0 (LM heads, one K-chunk): besides (or, with P == nullptr, instead
+// of) the fp32 outputs, each workgroup writes for every row the vocabulary
+// record (top VR, m, s, u) of its 128 NF output columns to
+// rec[(row * n_nt + column tile) * (2 VR + 3)].
+template <int MF, int NF, int PF, bool SWIGLU, int VR>
 __global__ __launch_bounds__(256) void gemm_tile_kernel(
     const bf16_t* __restrict__ X, int ldx, const bf16_t* __restrict__ W,
     int K, float* __restrict__ P, int N, size_t part_stride,
     const int* __restrict__ m_count, int k_chunk, int n_mt, int n_nt,
-    bf16_t* __restrict__ act, int F) {
+    bf16_t* __restrict__ act, int F, float* __restrict__ rec) {
   static_assert(PF == 2 || PF == 4, "weight ring depth");
   constexpr int BM = 32 * MF;
   constexpr int LD = 64 + 8;
@@ -206,6 +244,108 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(
 #undef SB_ISSUE_W
 #undef SB_ISSUE_WI
 #undef SB_SCHED
+  if constexpr (VR > 0) {
+    constexpr int RL = 2 * VR + 3;
+    __shared__ float vrec[4][32 * MF][RL];
+#pragma unroll
+    for (int t = 0; t < MF; ++t) {
+      const int m = m_base + 32 * t + lr;
+      float tv[VR];
+      int ti[VR];
+#pragma unroll
+      for (int k = 0; k < VR; ++k) {
+        tv[k] = -FLT_MAX;
+        ti[k] = 0x7FFFFFFF;
+      }
+      float mx = -FLT_MAX, sm = 0.f, su = 0.f;
+      if (wave_on) {
+        // lane register r of fragment f is column nb + 32 f + 8 (r / 4) +
+        // 4 h + r % 4 of row m
+#pragma unroll
+        for (int f = 0; f < NF; ++f)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float v = acc[t][f][r];
+            mx = fmaxf(mx, v);
+            vr_insert<VR>(tv, ti, v, nb + 32 * f + 8 * (r >> 2) + 4 * h + (r & 3));
+          }
+#pragma unroll
+        for (int f = 0; f < NF; ++f)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float e = __expf(acc[t][f][r] - mx);
+            sm += e;
+            su = fmaf(e, acc[t][f][r], su);
+          }
+        if (P != nullptr && m < M) {
+#pragma unroll
+          for (int f = 0; f < NF; ++f)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              *reinterpret_cast<float4*>(P + (size_t)m * N + nb + 32 * f + 8 * q + 4 * h) =
+                  make_float4(acc[t][f][4 * q], acc[t][f][4 * q + 1],
+                              acc[t][f][4 * q + 2], acc[t][f][4 * q + 3]);
+        }
+      }
+      // the lane pair (h = 0, 1) holds the same row
+      {
+        float pv[VR];
+        int pi[VR];
+#pragma unroll
+        for (int k = 0; k < VR; ++k) {
+          pv[k] = __shfl_xor(tv[k], 32, 64);
+          pi[k] = __shfl_xor(ti[k], 32, 64);
+        }
+        const float m2 = __shfl_xor(mx, 32, 64);
+        const float s2 = __shfl_xor(sm, 32, 64);
+        const float u2 = __shfl_xor(su, 32, 64);
+#pragma unroll
+        for (int k = 0; k < VR; ++k) vr_insert<VR>(tv, ti, pv[k], pi[k]);
+        vr_stats_merge(mx, sm, su, m2, s2, u2);
+      }
+      if (h == 0) {
+        float* o = vrec[wave][32 * t + lr];
+#pragma unroll
+        for (int k = 0; k < VR; ++k) {
+          o[k] = tv[k];
+          o[VR + k] = __int_as_float(ti[k]);
+        }
+        o[2 * VR] = mx;
+        o[2 * VR + 1] = sm;
+        o[2 * VR + 2] = su;
+      }
+    }
+    __syncthreads();
+    // one thread per row merges the four waves' records
+    if (tid < 32 * MF && m_base + tid < M) {
+      float tv[VR];
+      int ti[VR];
+      const float* o0 = vrec[0][tid];
+#pragma unroll
+      for (int k = 0; k < VR; ++k) {
+        tv[k] = o0[k];
+        ti[k] = __float_as_int(o0[VR + k]);
+      }
+      float mx = o0[2 * VR], sm = o0[2 * VR + 1], su = o0[2 * VR + 2];
+#pragma unroll
+      for (int w = 1; w < 4; ++w) {
+        const float* ow = vrec[w][tid];
+#pragma unroll
+        for (int k = 0; k < VR; ++k) vr_insert<VR>(tv, ti, ow[k], __float_as_int(ow[VR + k]));
+        vr_stats_merge(mx, sm, su, ow[2 * VR], ow[2 * VR + 1], ow[2 * VR + 2]);
+      }
+      float* g = rec + ((size_t)(m_base + tid) * n_nt + nt) * RL;
+#pragma unroll
+      for (int k = 0; k < VR; ++k) {
+        g[k] = tv[k];
+        g[VR + k] = __int_as_float(ti[k]);
+      }
+      g[2 * VR] = mx;
+      g[2 * VR + 1] = sm;
+      g[2 * VR + 2] = su;
+    }
+    return;
+  }
   if (!wave_on) return;
   if constexpr (SWIGLU) {
     // fragment f covers gate/up features 16 (nb / 32 + f) .. + 15; lane
@@ -436,11 +576,11 @@ int gemm_ksplit(int N, int K, int elem_bytes) {
 
 namespace {
 
-template <bool SWIGLU>
+template <bool SWIGLU, int VR = 0>
 void launch_tile(const GemmPlan& g, const bf16_t* X, int ldx, const bf16_t* W,
                  int N, int K, float* P, size_t part_stride,
                  const int* m_count, int m_cap, int ks, bf16_t* act, int F,
-                 hipStream_t st) {
+                 hipStream_t st, float* rec = nullptr) {
   const int n_mt = (m_cap + 32 * g.mf - 1) / (32 * g.mf);
   const int n_nt = (N + 128 * g.nf - 1) / (128 * g.nf);
   const int k_chunk = K / ks;
@@ -449,9 +589,10 @@ void launch_tile(const GemmPlan& g, const bf16_t* X, int ldx, const bf16_t* W,
   if (g.mf == MF_ && g.nf == NF_ && g.pf == PF_) {                            \
     hipEvent_t ea, eb;                                                        \
     take_events(ea, eb);                                                      \
-    hipExtLaunchKernelGGL(gemm_tile_kernel<MF_, NF_, PF_, SWIGLU>, grid,      \
+    hipExtLaunchKernelGGL(gemm_tile_kernel<MF_, NF_, PF_, SWIGLU, VR>, grid,  \
                           dim3(256), 0, st, ea, eb, 0, X, ldx, W, K, P, N,    \
-                          part_stride, m_count, k_chunk, n_mt, n_nt, act, F); \
+                          part_stride, m_count, k_chunk, n_mt, n_nt, act, F,  \
+                          rec);                                               \
     return;                                                                   \
   }
   SB_LAUNCH(1, 1, 2)
@@ -510,6 +651,21 @@ template int launch_gemm_xwt<float>(const float*, int, const float*, int, int,
 template int launch_gemm_xwt<bf16_t>(const bf16_t*, int, const bf16_t*, int,
                                      int, float*, size_t, const int*, int, int,
                                      hipStream_t);
+
+int launch_gemm_vocab(const bf16_t* X, int ldx, const bf16_t* W, int N,
+                      int K, float* logits, const int* m_count, int m_cap,
+                      int topk, float* rec, hipStream_t st) {
+  const GemmPlan g = gemm_plan(N, K, m_cap, 2);
+  if (topk != 1) return 0;
+  launch_tile<false, 1>(g, X, ldx, W, N, K, logits, 0, m_count, m_cap, 1,
+                        nullptr, 0, st, rec);
+  return gemm_vocab_chunks(N, K, m_cap);
+}
+
+int gemm_vocab_chunks(int N, int K, int m_cap) {
+  const GemmPlan g = gemm_plan(N, K, m_cap, 2);
+  return (N + 128 * g.nf - 1) / (128 * g.nf);
+}
 
 void launch_gemm_swiglu(const bf16_t* X, int ldx, const bf16_t* W, int F,
                         int K, bf16_t* act, const int* m_count, int m_cap,

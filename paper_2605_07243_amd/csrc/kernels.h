@@ -78,6 +78,17 @@ int launch_gemm_xwt(const T* X, int ldx, const T* W, int N, int K, float* P,
 void launch_gemm_swiglu(const bf16_t* X, int ldx, const bf16_t* W, int F,
                         int K, bf16_t* act, const int* m_count, int m_cap,
                         hipStream_t st);
+// LM head (bf16, fragment-packed W [N][K], one K-chunk) with the vocabulary
+// reduction in the epilogue: for each of the first *m_count rows and each
+// column tile of the launch, the record (top-1 value and id, m, s, u) the
+// separate reduction would write, at rec[(row * n_chunks + tile) * 5]; the
+// fp32 logits [row][N] are written too unless logits is NULL.  topk must be
+// 1 (nothing is launched otherwise).  Returns n_chunks, the column tiles
+// per row (gemm_vocab_chunks).
+int launch_gemm_vocab(const bf16_t* X, int ldx, const bf16_t* W, int N,
+                      int K, float* logits, const int* m_count, int m_cap,
+                      int topk, float* rec, hipStream_t st);
+int gemm_vocab_chunks(int N, int K, int m_cap);
 // Row-major bf16 [rows][cols] -> fragment-packed (rows % 32, cols % 64).
 int launch_pack_weight(const bf16_t* src, bf16_t* dst, int rows, int cols,
                        bool gate_up, hipStream_t st);

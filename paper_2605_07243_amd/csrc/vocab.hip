@@ -310,6 +310,76 @@ __device__ __forceinline__ void merge_row(const float* __restrict__ part,
   U = u;
 }
 
+// Merge the chunk records of row i over the whole workgroup (for the ~1000
+// records per row of the LM head's fused reduction): every thread
+// folds records threadIdx.x, + blockDim.x, ..., each wave reduces its
+// threads' lists and statistics, and wave 0 merges the waves' (lds: one
+// record per wave, at most 16 waves).  Call with every thread; the result
+// is valid in wave 0.
+template <int KT>
+__device__ __forceinline__ void merge_row_block(const float* __restrict__ part,
+                                                int n_chunks, float (&bv)[KT],
+                                                int (&bi)[KT], float& M,
+                                                float& S, float& U,
+                                                float (*lds)[2 * KT + 3]) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int nw = blockDim.x >> 6;
+  float tv[KT];
+  int ti[KT];
+#pragma unroll
+  for (int k = 0; k < KT; ++k) {
+    tv[k] = -FLT_MAX;
+    ti[k] = 0x7FFFFFFF;
+  }
+  float m = -FLT_MAX, s = 0.f, u = 0.f;
+  for (int c = threadIdx.x; c < n_chunks; c += blockDim.x) {
+    const float* o = part + (size_t)c * (2 * KT + 3);
+#pragma unroll
+    for (int k = 0; k < KT; ++k) topk_insert<KT>(tv, ti, o[k], __float_as_int(o[KT + k]));
+    stats_merge(m, s, u, o[2 * KT], o[2 * KT + 1], o[2 * KT + 2]);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float m2 = __shfl_xor(m, o, SB_WAVE);
+    const float s2 = __shfl_xor(s, o, SB_WAVE);
+    const float u2 = __shfl_xor(u, o, SB_WAVE);
+    stats_merge(m, s, u, m2, s2, u2);
+  }
+  wave_topk<KT>(tv, ti, bv, bi);
+  if (lane == 0) {
+#pragma unroll
+    for (int k = 0; k < KT; ++k) {
+      lds[w][k] = bv[k];
+      lds[w][KT + k] = __int_as_float(bi[k]);
+    }
+    lds[w][2 * KT] = m;
+    lds[w][2 * KT + 1] = s;
+    lds[w][2 * KT + 2] = u;
+  }
+  __syncthreads();
+  if (w == 0) {
+#pragma unroll
+    for (int k = 0; k < KT; ++k) {
+      tv[k] = lane < nw ? lds[lane][k] : -FLT_MAX;
+      ti[k] = lane < nw ? __float_as_int(lds[lane][KT + k]) : 0x7FFFFFFF;
+    }
+    m = lane < nw ? lds[lane][2 * KT] : -FLT_MAX;
+    s = lane < nw ? lds[lane][2 * KT + 1] : 0.f;
+    u = lane < nw ? lds[lane][2 * KT + 2] : 0.f;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float m2 = __shfl_xor(m, o, SB_WAVE);
+      const float s2 = __shfl_xor(s, o, SB_WAVE);
+      const float u2 = __shfl_xor(u, o, SB_WAVE);
+      stats_merge(m, s, u, m2, s2, u2);
+    }
+    wave_topk<KT>(tv, ti, bv, bi);
+  }
+  M = m;
+  S = s;
+  U = u;
+}
+
 // Drafter rows: top-10 ids (drafter ids mapped to target ids when the
 // drafter has a reduced vocabulary), log-sum-exp,
 // psi = [log p of top-10, z1-z2, z1-z3, z1-z5, p1, entropy],
@@ -416,23 +486,25 @@ void launch_draft_finalize(const float* part, int n_chunks, const CallPlan& p,
                                                rank_b, d, bmap, o);
 }
 
-__global__ __launch_bounds__(64) void verify_finalize_kernel(
+__global__ __launch_bounds__(256) void verify_finalize_kernel(
     const float* __restrict__ part, int n_chunks, const int* __restrict__ n,
     const int* __restrict__ out_row, int* __restrict__ argmax) {
+  __shared__ float mrec[4][5];
   const int i = blockIdx.x;
   if (i >= *n) return;
   float bv[1];
   int bi[1];
   float M, S, U;
-  merge_row<1>(part + (size_t)i * n_chunks * 5, n_chunks, bv, bi, M, S, U);
+  merge_row_block<1>(part + (size_t)i * n_chunks * 5, n_chunks, bv, bi, M, S,
+                     U, mrec);
   if (threadIdx.x == 0 && out_row[i] >= 0) argmax[out_row[i]] = bi[0];
 }
 
 void launch_verify_finalize(const float* part, int n_chunks, const int* n,
                             int cap, const int* out_row, int* argmax,
                             hipStream_t st) {
-  verify_finalize_kernel<<<cap, 64, 0, st>>>(part, n_chunks, n, out_row,
-                                             argmax);
+  verify_finalize_kernel<<<cap, 256, 0, st>>>(part, n_chunks, n, out_row,
+                                              argmax);
 }
 
 // Head-only drafter update (Sec. 3.4), one workgroup per buffered position
