@@ -163,3 +163,78 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
 __device__ __forceinline__ bool better(float v, int id, float bv, int bid) {
   return v > bv || (v == bv && id < bid);
 }
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+__device__ __forceinline__ int2 swap16_i(int v) {
+  const auto r = __builtin_amdgcn_permlane16_swap((unsigned)v, (unsigned)v,
+                                                  false, false);
+  return make_int2((int)r[0], (int)r[1]);
+}
+__device__ __forceinline__ int2 swap32_i(int v) {
+  const auto r = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v,
+                                                  false, false);
+  return make_int2((int)r[0], (int)r[1]);
+}
+__device__ __forceinline__ void take_better(float& v, int& id, float v2,
+                                            int i2) {
+  if (better(v2, i2, v, id)) {
+    v = v2;
+    id = i2;
+  }
+}
+// Wave-wide best (larger value, then smaller id); every lane gets it.  The
+// same DPP / permlane pairing as wave_max (the combine is symmetric and
+// idempotent), a few VALU cycles per step instead of an LDS permute.
+__device__ __forceinline__ void wave_best_pair(float& v, int& id) {
+  take_better(v, id, dpp_f<0xB1>(v), dpp_i<0xB1>(id));
+  take_better(v, id, dpp_f<0x4E>(v), dpp_i<0x4E>(id));
+  take_better(v, id, dpp_f<0x141>(v), dpp_i<0x141>(id));
+  take_better(v, id, dpp_f<0x140>(v), dpp_i<0x140>(id));
+  {
+    const float2 a = swap16(v);
+    const int2 b = swap16_i(id);
+    v = a.x;
+    id = b.x;
+    take_better(v, id, a.y, b.y);
+  }
+  {
+    const float2 a = swap32(v);
+    const int2 b = swap32_i(id);
+    v = a.x;
+    id = b.x;
+    take_better(v, id, a.y, b.y);
+  }
+}
+
+// Wave-wide minimum of an int (DPP / permlane pairing as wave_max).
+__device__ __forceinline__ int wave_min_i(int v) {
+  v = min(v, dpp_i<0xB1>(v));
+  v = min(v, dpp_i<0x4E>(v));
+  v = min(v, dpp_i<0x141>(v));
+  v = min(v, dpp_i<0x140>(v));
+  const int2 a = swap16_i(v);
+  v = min(a.x, a.y);
+  const int2 b = swap32_i(v);
+  return min(b.x, b.y);
+}
+
+// Exclusive wave prefix sum of small non-negative values (v < 2^BITS) by
+// bit planes: one ballot and one masked bit count per bit; total in every
+// lane.
+template <int BITS>
+__device__ __forceinline__ int wave_excl_scan_small(int v, int& total) {
+  int excl = 0;
+  total = 0;
+#pragma unroll
+  for (int b = 0; b < BITS; ++b) {
+    const unsigned long long m = __ballot((v >> b) & 1);
+    const int below = (int)__builtin_amdgcn_mbcnt_hi(
+        (unsigned)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
+    excl += below << b;
+    total += __popcll(m) << b;
+  }
+  return excl;
+}

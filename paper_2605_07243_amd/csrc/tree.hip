@@ -10,18 +10,6 @@
 
 namespace sb {
 
-__device__ __forceinline__ int wave_excl_scan(int v, int& total) {
-  const int lane = threadIdx.x & 63;
-  int incl = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int t = __shfl_up(incl, o, SB_WAVE);
-    if (lane >= o) incl += t;
-  }
-  total = __shfl(incl, 63, SB_WAVE);
-  return incl - v;
-}
-
 // ---------------------------------------------------------------------------
 // Block 1: reset the tree to the root (node 0, one start) and count the
 // W_cond rows (one per sequence).
@@ -127,12 +115,24 @@ __global__ void plan_block_kernel(TreeDims td, int m, sb_tree t,
 
 // Sibling attachment of one block in (k, start, rank) order within the
 // budget, then the next block's starts.  One wave per sequence; lane b owns
-// start b of the block.
+// start b of the block.  The block's row results (branch, bucket, lse,
+// top-10 ids and logits: rows row0 .. row0 + nst K - 1, at most 512) are
+// staged in LDS with coalesced loads before the attachment loop, and the
+// cumulative log-probability of every new node that qualifies as a next
+// start is kept in LDS, so that the loop and the start selection read no
+// global memory.
+constexpr int kAttachRows = 512;
 __global__ __launch_bounds__(64) void attach_kernel(
     TreeDims td, sb_tree t, const int* __restrict__ topk_id,
     const float* __restrict__ topk_logit, const float* __restrict__ lse,
     const int* __restrict__ bucket, const int* __restrict__ branch,
     const int* __restrict__ blk_row0, const int* __restrict__ blk_nst) {
+  __shared__ int ids_s[kAttachRows * SB_TOPK_K];
+  __shared__ float lg_s[kAttachRows * SB_TOPK_K];
+  __shared__ float lse_s[kAttachRows];
+  __shared__ int br_s[kAttachRows];
+  __shared__ int bk_s[kAttachRows];
+  __shared__ float cand_s[kAttachRows];   // new node id - first_new
   const int s = blockIdx.x;
   const int lane = threadIdx.x;
   const int K = td.K, budget = td.budget, bw = td.bw;
@@ -140,7 +140,19 @@ __global__ __launch_bounds__(64) void attach_kernel(
   const int row0 = blk_row0[s];
   const size_t nb = (size_t)s * budget;
   const size_t rb = (size_t)s * td.row_cap;
+  const int nrows = min(nst * K, kAttachRows);
   const bool mine = lane < nst;
+  // independent loads first: the block's rows, the start nodes
+  for (int e = lane; e < nrows * SB_TOPK_K; e += 64) {
+    ids_s[e] = topk_id[(rb + row0) * SB_TOPK_K + e];
+    lg_s[e] = topk_logit[(rb + row0) * SB_TOPK_K + e];
+  }
+  for (int j = lane; j < nrows; j += 64) {
+    lse_s[j] = lse[rb + row0 + j];
+    br_s[j] = branch[rb + row0 + j];
+    bk_s[j] = bucket[rb + row0 + j];
+  }
+  for (int j = lane; j < budget; j += 64) cand_s[j] = -FLT_MAX;
   int chain = mine ? t.starts[(size_t)s * td.B_max + lane] : 0;
   bool alive = mine;
   int chain_depth = 0;
@@ -157,25 +169,32 @@ __global__ __launch_bounds__(64) void attach_kernel(
   }
   int nn = t.n_nodes[s];
   const int first_new = nn;
+  __syncthreads();
   for (int k = 1; k <= K; ++k) {
-    const int r = row0 + lane * K + (k - 1);
-    const int want = (mine && alive) ? branch[rb + r] : 0;
+    const int j = lane * K + (k - 1);          // block-local row
+    const int r = row0 + j;
+    const bool live = mine && alive && j < nrows;
+    const int want = live ? br_s[j] : 0;   // 0..10
     int total;
-    const int excl = wave_excl_scan(want, total);
+    const int excl = wave_excl_scan_small<4>(want, total);
     const int id0 = nn + excl;
-    if (mine && alive) {
+    if (live) {
+      const float l0 = lse_s[j];
+      const int bk = bk_s[j];
+      const bool cand_row = bk == 1 || bk == 2;
       for (int rank = 1; rank <= want; ++rank) {
         const int id = id0 + rank - 1;
         if (id >= budget) break;
-        const size_t o = (rb + r) * SB_TOPK_K + (rank - 1);
-        const float lp = topk_logit[o] - lse[rb + r];
-        t.token[nb + id] = topk_id[o];
+        const int q = j * SB_TOPK_K + (rank - 1);
+        const float lp = lg_s[q] - l0;
+        t.token[nb + id] = ids_s[q];
         t.parent[nb + id] = chain;
         t.depth[nb + id] = chain_depth + 1;
         t.row[nb + id] = r;
         t.rank[nb + id] = rank;
         t.logp[nb + id] = lp;
         t.cum_logp[nb + id] = chain_cum + lp;
+        if (rank >= 2 && cand_row) cand_s[id - first_new] = chain_cum + lp;
 #pragma unroll
         for (int w = 0; w < SB_MAX_ANC_WORDS; ++w)
           if (w < bw)
@@ -183,10 +202,9 @@ __global__ __launch_bounds__(64) void attach_kernel(
                 chain_anc[w] | ((id >> 5) == w ? (1u << (id & 31)) : 0u);
       }
       if (want >= 1 && id0 < budget) {
-        const size_t o = (rb + r) * SB_TOPK_K;
         chain = id0;
         chain_depth += 1;
-        chain_cum += topk_logit[o] - lse[rb + r];
+        chain_cum += lg_s[j * SB_TOPK_K] - l0;
 #pragma unroll
         for (int w = 0; w < SB_MAX_ANC_WORDS; ++w)
           if ((id0 >> 5) == w) chain_anc[w] |= 1u << (id0 & 31);
@@ -197,7 +215,7 @@ __global__ __launch_bounds__(64) void attach_kernel(
     nn = min(budget, nn + total);
   }
   if (lane == 0) t.n_nodes[s] = nn;
-  __syncthreads();   // node writes of all lanes visible below
+  __syncthreads();   // candidate values of all lanes visible below
   // next-block starts: chain ends first, then rank >= 2 siblings of b1/b2
   // rows by cumulative log-probability (ties: lower node id)
   int* out = t.starts + (size_t)s * td.B_max;
@@ -207,17 +225,14 @@ __global__ __launch_bounds__(64) void attach_kernel(
   }
   int n_ends;
   const int is_end = (mine && alive) ? 1 : 0;
-  const int e_excl = wave_excl_scan(is_end, n_ends);
+  const int e_excl = wave_excl_scan_small<1>(is_end, n_ends);
   if (is_end && e_excl < td.B_max) out[e_excl] = chain;
   int taken = min(n_ends, td.B_max);
   // candidate mask per lane: node first_new + lane + 64 q
   uint32_t cand = 0u;
   for (int q = 0; q < 8; ++q) {
     const int id = first_new + lane + 64 * q;
-    if (id < nn && t.rank[nb + id] >= 2) {
-      const int bk = bucket[rb + t.row[nb + id]];
-      if (bk == 1 || bk == 2) cand |= 1u << q;
-    }
+    if (id < nn && cand_s[id - first_new] > -FLT_MAX) cand |= 1u << q;
   }
   while (taken < td.B_max) {
     float bv = -FLT_MAX;
@@ -225,7 +240,7 @@ __global__ __launch_bounds__(64) void attach_kernel(
     for (int q = 0; q < 8; ++q) {
       if (cand & (1u << q)) {
         const int id = first_new + lane + 64 * q;
-        const float v = t.cum_logp[nb + id];
+        const float v = cand_s[id - first_new];
         if (better(v, id, bv, bi)) {
           bv = v;
           bi = id;
@@ -234,15 +249,7 @@ __global__ __launch_bounds__(64) void attach_kernel(
     }
     float v = bv;
     int id = bi;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float v2 = __shfl_xor(v, o, SB_WAVE);
-      const int i2 = __shfl_xor(id, o, SB_WAVE);
-      if (better(v2, i2, v, id)) {
-        v = v2;
-        id = i2;
-      }
-    }
+    wave_best_pair(v, id);
     if (id == 0x7FFFFFFF) break;
     if (lane == 0) out[taken] = id;
     if (((id - first_new) & 63) == lane) cand &= ~(1u << ((id - first_new) >> 6));
@@ -306,8 +313,7 @@ __global__ __launch_bounds__(64) void accept_kernel(TreeDims td, sb_tree t,
     int best = 0x7FFFFFFF;
     for (int j = 1 + lane; j < nn; j += 64)
       if (t.parent[nb + j] == cur && t.token[nb + j] == g) best = min(best, j);
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) best = min(best, __shfl_xor(best, o, SB_WAVE));
+    best = wave_min_i(best);
     if (best == 0x7FFFFFFF) break;
     if (lane == 0) out.path[(size_t)s * path_cap + a] = best;
     cur = best;

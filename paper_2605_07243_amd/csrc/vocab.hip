@@ -43,14 +43,32 @@ __device__ __forceinline__ void stats_merge(float& m, float& s, float& u,
 
 // Wave-wide best (value, smaller id); every lane gets the winner.
 __device__ __forceinline__ void wave_best(float& v, int& id) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float v2 = __shfl_xor(v, o, SB_WAVE);
-    const int i2 = __shfl_xor(id, o, SB_WAVE);
-    if (better(v2, i2, v, id)) {
-      v = v2;
-      id = i2;
-    }
+  wave_best_pair(v, id);
+}
+
+// Wave-wide merge of (m, s, u) statistics; every lane gets the result (the
+// pairwise merge is symmetric, so DPP / permlane partners agree).
+__device__ __forceinline__ void wave_stats(float& m, float& s, float& u) {
+#define SB_STATS_DPP(C)                                                       \
+  {                                                                           \
+    const float m2 = dpp_f<C>(m), s2 = dpp_f<C>(s), u2 = dpp_f<C>(u);        \
+    stats_merge(m, s, u, m2, s2, u2);                                         \
+  }
+  SB_STATS_DPP(0xB1) SB_STATS_DPP(0x4E) SB_STATS_DPP(0x141) SB_STATS_DPP(0x140)
+#undef SB_STATS_DPP
+  {
+    const float2 a = swap16(m), b = swap16(s), c = swap16(u);
+    m = a.x;
+    s = b.x;
+    u = c.x;
+    stats_merge(m, s, u, a.y, b.y, c.y);
+  }
+  {
+    const float2 a = swap32(m), b = swap32(s), c = swap32(u);
+    m = a.x;
+    s = b.x;
+    u = c.x;
+    stats_merge(m, s, u, a.y, b.y, c.y);
   }
 }
 
@@ -128,9 +146,7 @@ __global__ __launch_bounds__(256) void vocab_partial_kernel(
     float v = mx, t = -FLT_MAX;
 #pragma unroll
     for (int k = 0; k < KT; ++k) {
-      float b = v;
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) b = fmaxf(b, __shfl_xor(b, o, SB_WAVE));
+      const float b = wave_max(v);
       t = b;
       if (v == b) v = -INFINITY;
     }
@@ -156,13 +172,7 @@ __global__ __launch_bounds__(256) void vocab_partial_kernel(
   }
   const float m = mx;
   float M = m, S = s, U = u;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float m2 = __shfl_xor(M, o, SB_WAVE);
-    const float s2 = __shfl_xor(S, o, SB_WAVE);
-    const float u2 = __shfl_xor(U, o, SB_WAVE);
-    stats_merge(M, S, U, m2, s2, u2);
-  }
+  wave_stats(M, S, U);
   if (lane == 0) {
     sm[w] = M;
     ss[w] = S;
@@ -297,13 +307,7 @@ __device__ __forceinline__ void merge_row(const float* __restrict__ part,
     for (int k = 0; k < KT; ++k) topk_insert<KT>(tv, ti, o[k], __float_as_int(o[KT + k]));
     stats_merge(m, s, u, o[2 * KT], o[2 * KT + 1], o[2 * KT + 2]);
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float m2 = __shfl_xor(m, o, SB_WAVE);
-    const float s2 = __shfl_xor(s, o, SB_WAVE);
-    const float u2 = __shfl_xor(u, o, SB_WAVE);
-    stats_merge(m, s, u, m2, s2, u2);
-  }
+  wave_stats(m, s, u);
   wave_topk<KT>(tv, ti, bv, bi);
   M = m;
   S = s;
@@ -338,13 +342,7 @@ __device__ __forceinline__ void merge_row_block(const float* __restrict__ part,
     for (int k = 0; k < KT; ++k) topk_insert<KT>(tv, ti, o[k], __float_as_int(o[KT + k]));
     stats_merge(m, s, u, o[2 * KT], o[2 * KT + 1], o[2 * KT + 2]);
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float m2 = __shfl_xor(m, o, SB_WAVE);
-    const float s2 = __shfl_xor(s, o, SB_WAVE);
-    const float u2 = __shfl_xor(u, o, SB_WAVE);
-    stats_merge(m, s, u, m2, s2, u2);
-  }
+  wave_stats(m, s, u);
   wave_topk<KT>(tv, ti, bv, bi);
   if (lane == 0) {
 #pragma unroll
@@ -366,13 +364,7 @@ __device__ __forceinline__ void merge_row_block(const float* __restrict__ part,
     m = lane < nw ? lds[lane][2 * KT] : -FLT_MAX;
     s = lane < nw ? lds[lane][2 * KT + 1] : 0.f;
     u = lane < nw ? lds[lane][2 * KT + 2] : 0.f;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float m2 = __shfl_xor(m, o, SB_WAVE);
-      const float s2 = __shfl_xor(s, o, SB_WAVE);
-      const float u2 = __shfl_xor(u, o, SB_WAVE);
-      stats_merge(m, s, u, m2, s2, u2);
-    }
+    wave_stats(m, s, u);
     wave_topk<KT>(tv, ti, bv, bi);
   }
   M = m;
@@ -395,6 +387,27 @@ __global__ __launch_bounds__(1024) void draft_finalize_kernel(
   const int i = blockIdx.x;
   if (i >= *p.n) return;
   const int o = p.out_row[i];
+  // h^(L) part of the rank head: the row and four rank-head rows (d <=
+  // 8192) are loaded before the record merge (they do not depend on it)
+  constexpr int kMaxQ = 8;
+  const float* xr = x + (size_t)i * d;
+  float* hl = out.h_last + (size_t)o * d;
+  const int ld = d + SB_PSI;
+  float xv[kMaxQ];
+  float wv[4][kMaxQ];
+#pragma unroll
+  for (int q = 0; q < kMaxQ; ++q) {
+    const int j = threadIdx.x + 1024 * q;
+    const bool in = j < d;
+    xv[q] = in ? xr[j] : 0.f;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) wv[b][q] = in ? rank_w[(size_t)b * ld + j] : 0.f;
+  }
+  float wp[4] = {0.f, 0.f, 0.f, 0.f};
+  if (threadIdx.x < SB_PSI) {
+#pragma unroll
+    for (int b = 0; b < 4; ++b) wp[b] = rank_w[(size_t)b * ld + d + threadIdx.x];
+  }
   if (threadIdx.x < 64) {
     float bv[SB_TOPK_K];
     int bi[SB_TOPK_K];
@@ -421,24 +434,7 @@ __global__ __launch_bounds__(1024) void draft_finalize_kernel(
       for (int k = 0; k < SB_PSI; ++k) out.psi[(size_t)o * SB_PSI + k] = psi_s[k];
     }
   }
-  __syncthreads();
-  // h^(L) part of the rank head: every load (the row and four rank-head
-  // rows, d <= 8192) issued before the row is stored into the tree's cache
-  constexpr int kMaxQ = 8;
-  const float* xr = x + (size_t)i * d;
-  float* hl = out.h_last + (size_t)o * d;
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
-  const int ld = d + SB_PSI;
-  float xv[kMaxQ];
-  float wv[4][kMaxQ];
-#pragma unroll
-  for (int q = 0; q < kMaxQ; ++q) {
-    const int j = threadIdx.x + 1024 * q;
-    const bool in = j < d;
-    xv[q] = in ? xr[j] : 0.f;
-#pragma unroll
-    for (int b = 0; b < 4; ++b) wv[b][q] = in ? rank_w[(size_t)b * ld + j] : 0.f;
-  }
 #pragma unroll
   for (int q = 0; q < kMaxQ; ++q)
 #pragma unroll
@@ -448,10 +444,10 @@ __global__ __launch_bounds__(1024) void draft_finalize_kernel(
     const int j = threadIdx.x + 1024 * q;
     if (j < d) hl[j] = xv[q];
   }
+  __syncthreads();   // psi_s
   if (threadIdx.x < SB_PSI) {
 #pragma unroll
-    for (int b = 0; b < 4; ++b)
-      acc[b] += rank_w[(size_t)b * ld + d + threadIdx.x] * psi_s[threadIdx.x];
+    for (int b = 0; b < 4; ++b) acc[b] += wp[b] * psi_s[threadIdx.x];
   }
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
 #pragma unroll
