@@ -5,8 +5,11 @@
     python -m paper_2605_07243_amd.profile_summary --pmc COUNTERS.csv \
         --last-steps N --calib-bytes B [--json OUT.json]
 
-The window is the last N hot-path steps, delimited by the first kernel of
-each step (``--step-marker``).  With a kernel trace, every kernel family gets
+The window is the last N complete hot-path steps, delimited by the first
+kernel of each step (``--step-marker``), leaving out steps that contain a
+kernel named by ``--skip-steps-with`` (by default the one-thread row-count
+copy that only bench.py's profiled pass launches, so that the window holds
+the timed steps).  With a kernel trace, every kernel family gets
 its dispatches per step, total and mean duration, so the mean duration of a
 kernel can be compared with the HIP-event timing bench.py reports.  With a
 counter collection (``--pmc``), every family gets the mean value of each
@@ -31,14 +34,23 @@ def family(name: str) -> str:
     return name
 
 
-def summarise(path: str, last_steps: int, marker: str):
+def step_window(names, last_steps: int, marker: str, skip: str):
+    """Indices into `names` (kernel names in launch order) of the last
+    `last_steps` complete steps that launch no kernel containing `skip`."""
+    starts = [i for i, n in enumerate(names) if marker in n]
+    steps = [range(a, b) for a, b in zip(starts, starts[1:])]
+    if skip:
+        steps = [r for r in steps if not any(skip in names[i] for i in r)]
+    if len(steps) < last_steps:
+        raise SystemExit(f"only {len(steps)} complete steps found")
+    return [i for r in steps[len(steps) - last_steps:] for i in r]
+
+
+def summarise(path: str, last_steps: int, marker: str, skip: str = ""):
     rows = list(csv.DictReader(open(path)))
     rows.sort(key=lambda r: int(r["Start_Timestamp"]))
-    starts = [i for i, r in enumerate(rows) if marker in r["Kernel_Name"]]
-    if len(starts) < last_steps + 1:
-        raise SystemExit(f"only {len(starts)} steps found")
-    lo, hi = starts[-last_steps - 1], starts[-1]
-    win = rows[lo:hi]
+    win = [rows[i] for i in step_window([r["Kernel_Name"] for r in rows],
+                                        last_steps, marker, skip)]
     agg = collections.defaultdict(lambda: [0, 0.0])
     for r in win:
         d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
@@ -49,7 +61,8 @@ def summarise(path: str, last_steps: int, marker: str):
     return agg, busy, len(win)
 
 
-def summarise_pmc(path: str, last_steps: int, marker: str, calib: str):
+def summarise_pmc(path: str, last_steps: int, marker: str, calib: str,
+                  skip: str = ""):
     """Per family and counter: (dispatches in window, mean value); plus the
     calibration kernel's mean per counter (over all its dispatches)."""
     per = collections.defaultdict(dict)     # dispatch -> counter -> value
@@ -60,10 +73,8 @@ def summarise_pmc(path: str, last_steps: int, marker: str, calib: str):
         c = r["Counter_Name"]
         per[d][c] = per[d].get(c, 0.0) + float(r["Counter_Value"])
     order = sorted(per)
-    starts = [i for i, d in enumerate(order) if marker in names[d]]
-    if len(starts) < last_steps + 1:
-        raise SystemExit(f"only {len(starts)} steps found")
-    win = order[starts[-last_steps - 1]:starts[-1]]
+    win = [order[i] for i in step_window([names[d] for d in order],
+                                         last_steps, marker, skip)]
     agg = collections.defaultdict(lambda: collections.defaultdict(list))
     for d in win:
         for c, v in per[d].items():
@@ -78,7 +89,8 @@ def summarise_pmc(path: str, last_steps: int, marker: str, calib: str):
 
 def main_pmc(a):
     import json
-    agg, cal = summarise_pmc(a.pmc, a.last_steps, a.step_marker, a.calib)
+    agg, cal = summarise_pmc(a.pmc, a.last_steps, a.step_marker, a.calib,
+                             a.skip_steps_with)
     k = a.last_steps
     counters = sorted({c for f in agg.values() for c in f})
     kib = a.calib_bytes / 1024.0
@@ -176,13 +188,16 @@ def main(argv=None):
     ap.add_argument("--json")
     ap.add_argument("--last-steps", type=int, default=5)
     ap.add_argument("--step-marker", default="block1_reset_kernel")
+    ap.add_argument("--skip-steps-with", default="copy_int_kernel",
+                    help="leave out steps that launch this kernel ('' keeps all)")
     ap.add_argument("--top", type=int, default=24)
     a = ap.parse_args(argv)
     if a.combine:
         return combine(*a.combine)
     if a.pmc:
         return main_pmc(a)
-    agg, busy, n = summarise(a.trace, a.last_steps, a.step_marker)
+    agg, busy, n = summarise(a.trace, a.last_steps, a.step_marker,
+                             a.skip_steps_with)
     k = a.last_steps
     out = [f"Window: last {k} steps, {n} dispatches, kernel busy "
            f"{busy / k:.1f} us/step.", "",
