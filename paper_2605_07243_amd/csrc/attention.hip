@@ -897,17 +897,18 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
   if constexpr (sizeof(T) == 2) {
     if (a.mfma32) {
       // balanced splits (see balanced_split) when the fixed plan would take
-      // more than two rounds of workgroups and the split can be worked out
+      // more than one round of workgroups and the split can be worked out
       // on the device: the grid is kAttnSlots items, each sequence's splits
       // at most ms (the partial slots, and what the other sequences leave
-      // of the slots).  Measured: 4 sequences of equal prefixes (fixed plan
-      // 576 workgroups) +12%; 16 ragged prefixes (512) 7% slower than the
-      // fixed plan, whose second round fills in behind the short sequences
+      // of the slots).  Measured: 4 sequences of equal 2048-key prefixes
+      // with 96 rows (fixed plan 3 splits, 288 workgroups) 74 vs 90 us; 16
+      // ragged prefixes with 64 rows take the fixed plan's one round
+      // (balanced: 83 vs 66 us)
       const int gx = a.groups * Hkv;
       const bool bal = split_rows != nullptr && p.n_seqs <= 64 &&
                        p.n_seqs * gx <= kAttnSlots && max_prefix <= 256 * 64 &&
                        (p.n_seqs == 1 ||          // even splits, no rounding
-                        (long)p.n_seqs * gx * n_split > 2 * kAttnSlots);
+                        (long)p.n_seqs * gx * n_split > kAttnSlots);
       const int ms = bal ? std::max(1, std::min(max_split,
                                                 kAttnSlots / gx - (p.n_seqs - 1)))
                          : n_split;
@@ -968,6 +969,19 @@ void launch_attn_merge(const CallPlan& p, int H, int hd, int n_split,
 
 int attn_qgroups(int rows_per_seq_cap, int G, int seq_heads, int es) {
   return attn_shape(rows_per_seq_cap, G, seq_heads, es).groups;
+}
+
+// The 32x32 kernel: one round of kAttnSlots workgroups.  Every split adds a
+// full fp32 partial of its rows (written, then read by the merge), which at
+// 16 sequences x 64 rows is 16.8 MB per split: 2 splits (one round) measured
+// 66 us against 84 us for 4 splits (two rounds) at 16 prefixes of 512-2000
+// keys; a 128-row tree drafting block at the same shape 67 vs 78 us.  The
+// 16-row kernel: two rounds (its workgroups are smaller; at one sequence of
+// 60 nodes the splits stay at 128 keys or more, see the caller).
+int attn_workgroup_target(int rows_per_seq_cap, int G, int seq_heads, int es) {
+  return attn_shape(rows_per_seq_cap, G, seq_heads, es).mfma32
+             ? kAttnSlots
+             : 2 * kAttnSlots;
 }
 
 template void launch_tree_attn<float>(const float*, const CallPlan&,

@@ -728,12 +728,12 @@ void layer_body(sb_ctx* c, const sb_layer_weights& lw, int layer,
   const int cap_tokens = c->cfg.max_pages * 16;
   const int max_prefix = c->T_bound > 0 ? std::min(c->T_bound, cap_tokens)
                                         : cap_tokens;
-  const int groups =
-      attn_qgroups(rows_per_seq, D.H / D.Hkv, p.n_seqs * D.Hkv, D.es) *
-      p.n_seqs * D.Hkv;
+  const int G = D.H / D.Hkv, seq_heads = p.n_seqs * D.Hkv;
+  const int groups = attn_qgroups(rows_per_seq, G, seq_heads, D.es) * seq_heads;
   // enough workgroups for the chip, splits of at least 128 keys (the
   // kernel keeps four 32-key tiles in flight; shorter splits measured slower)
-  int n_split = std::max(1, ceil_div(512, groups));
+  int n_split = std::max(
+      1, ceil_div(attn_workgroup_target(rows_per_seq, G, seq_heads, D.es), groups));
   n_split = std::min(n_split, std::max(1, max_prefix / 128));
   // a split spans at most 1024 pages of 16 keys
   n_split = std::max(n_split, ceil_div(max_prefix, 1024 * 16));

@@ -153,6 +153,9 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
 // Query groups (workgroups) per (sequence, KV head) of a launch (seq_heads
 // = the launch's sequences x KV heads, es = element bytes).
 int attn_qgroups(int rows_per_seq_cap, int G, int seq_heads, int es);
+// Workgroups a launch of that shape should reach for one full round of the
+// chip (the split count is chosen to reach it).
+int attn_workgroup_target(int rows_per_seq_cap, int G, int seq_heads, int es);
 
 // Vocabulary reductions over fp32 logits [cap][V], in chunks of at most
 // kVocabChunkMax logits (a chunk is staged in LDS); a row needs at least
