@@ -70,11 +70,31 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
   constexpr int QPW = NQ * QT;                      // q-tiles per workgroup
   __shared__ __attribute__((aligned(16))) T ksh[2][32][LDK];
   __shared__ __attribute__((aligned(16))) T vsh[2][HD][LDV];
-  const int s = blockIdx.y / Hkv, kh = blockIdx.y % Hkv;
+  // XCD-grouped order: the dispatcher deals workgroups out round-robin over
+  // the 8 XCDs, so neighbouring ids would land on different XCDs and each
+  // fetch the same K/V or Q into its own L2.  Remapped, a run of consecutive
+  // logical ids shares an XCD, and the logical order is q-group, then split,
+  // then (sequence, KV head): the q-groups of a split share its K/V tiles,
+  // the splits of a q-group its Q (one sequence of 60 nodes: one KV head per
+  // XCD; fetched bytes per call 17.8 -> 7.9 MB with q-groups alone grouped)
+  int bx = blockIdx.x, by = blockIdx.y, bz = blockIdx.z;
+  {
+    const int gx = gridDim.x, gy = gridDim.y;
+    const int total = gx * gy * (int)gridDim.z;
+    if ((total & 7) == 0) {
+      const int b = bx + gx * (by + gy * bz);
+      const int l = (b & 7) * (total >> 3) + (b >> 3);
+      const int gz = (int)gridDim.z;
+      bx = l % gx;
+      bz = (l / gx) % gz;
+      by = l / (gx * gz);
+    }
+  }
+  const int s = by / Hkv, kh = by % Hkv;
   const int G = H / Hkv;
   const int row0 = p.seq_off[s];
   const int nq = (p.seq_off[s + 1] - row0) * G;
-  const int qg = blockIdx.x;
+  const int qg = bx;
   if (qg * QPW * 16 >= nq) return;                  // uniform for the group
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int r = lane & 15, g = lane >> 4;
@@ -111,9 +131,9 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
   const T* svp = static_cast<const T*>(kv.seg_v);
   const int* ptab = kv.page_table + (size_t)s * kv.max_pages;
   const int Tp = min(p.prefix_len[s], kv.max_pages * 16);
-  const int t0 = blockIdx.z * split_tokens;
+  const int t0 = bz * split_tokens;
   const int t1 = min(Tp, t0 + split_tokens);
-  const bool last_split = blockIdx.z == gridDim.z - 1;
+  const bool last_split = bz == gridDim.z - 1;
   const int L = last_split ? min(p.seg_len[s], kv.seg_pages * 16) : 0;
   const int n_pre = t1 > t0 ? (t1 - t0 + 31) / 32 : 0;
   const int n_tiles = n_pre + (L + 31) / 32;
@@ -308,13 +328,13 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
           o[16 * c + 4 * g + rr] = Elem<T>::from_f32(acc[j][c][rr] * il);
       continue;
     }
-    float* o = o_part + (((size_t)blockIdx.z * cap + qrow[j]) * H + qh[j]) * HD;
+    float* o = o_part + (((size_t)bz * cap + qrow[j]) * H + qh[j]) * HD;
 #pragma unroll
     for (int c = 0; c < HD / 16; ++c)
       *reinterpret_cast<float4*>(o + 16 * c + 4 * g) =
           make_float4(acc[j][c][0], acc[j][c][1], acc[j][c][2], acc[j][c][3]);
     if (g == 0) {
-      float* mlp = ml + (((size_t)blockIdx.z * cap + qrow[j]) * H + qh[j]) * 2;
+      float* mlp = ml + (((size_t)bz * cap + qrow[j]) * H + qh[j]) * 2;
       mlp[0] = m_run[j];
       mlp[1] = l_run[j];
     }
@@ -358,7 +378,7 @@ __device__ __forceinline__ int n_splits_of(int tiles, int sp) {
 }
 
 __device__ SplitItem balanced_split(const CallPlan& p, int max_pages, int gx,
-                                    int max_split) {
+                                    int max_split, int b) {
   const int lane = threadIdx.x & 63;
   bool act = false;
   int t = 0;
@@ -387,7 +407,6 @@ __device__ SplitItem balanced_split(const CallPlan& p, int max_pages, int gx,
     if (lane >= o) inc += v;
   }
   const int exc = inc - nz * gx;
-  const int b = blockIdx.x;
   const unsigned long long m = __ballot(act && exc <= b && b < inc);
   SplitItem r{};
   if (m == 0) return r;
@@ -436,9 +455,26 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
   __shared__ __attribute__((aligned(16))) bf16_t vsh[2][HD][LDV];
   constexpr int MAXP = 1024;
   __shared__ int pg_sh[MAXP];
+  // XCD-grouped order as in the 16-row kernel (fixed splits: q-group, split,
+  // then (sequence, KV head)); balanced items are ordered by sequence, split,
+  // KV head and q-group, so neighbouring items again share K/V or Q
+  int bx = blockIdx.x, by = blockIdx.y, bz = blockIdx.z;
+  {
+    const int gx = gridDim.x, gy = gridDim.y;
+    const int total = gx * gy * (int)gridDim.z;
+    if ((total & 7) == 0) {
+      const int b = bx + gx * (by + gy * bz);
+      const int l = (b & 7) * (total >> 3) + (b >> 3);
+      const int gz = (int)gridDim.z;
+      bx = l % gx;
+      bz = (l / gx) % gz;
+      by = l / (gx * gz);
+    }
+  }
   int s, kh, qg, zs, nzs, split_tok;
   if (split_rows != nullptr) {
-    const SplitItem it = balanced_split(p, kv.max_pages, Hkv * n_groups, max_split);
+    const SplitItem it =
+        balanced_split(p, kv.max_pages, Hkv * n_groups, max_split, bx);
     if (!it.live) return;                   // uniform: every wave agrees
     s = it.s;
     kh = it.item / n_groups;
@@ -447,10 +483,10 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
     nzs = it.nz;
     split_tok = it.sp * 64;
   } else {
-    s = blockIdx.y / Hkv;
-    kh = blockIdx.y % Hkv;
-    qg = blockIdx.x;
-    zs = blockIdx.z;
+    s = by / Hkv;
+    kh = by % Hkv;
+    qg = bx;
+    zs = bz;
     nzs = gridDim.z;
     split_tok = split_tokens;
   }

@@ -516,7 +516,29 @@ double round_fill(int wgs) {
 
 }  // namespace
 
-GemmPlan gemm_plan(int N, int K, int m_cap, int elem_bytes) {
+namespace {
+
+// Estimated duration (us) of a many-row bf16 plan: rounds of 256
+// workgroups, each streaming its 32 mf x 128 nf tile over K / ks at the
+// per-CU MFMA rate the kernel sustains (0.45 of 2.5 PFLOP/s / 256), scaled
+// by the tile's relative efficiency (measured: 128 x 512 tiles 1.12 and
+// 96 x 256 tiles 0.97 of 128 x 256), plus the consumer's read of the ks
+// fp32 partial slabs at 5 TB/s.  Fits the measured 8B and 70B projections
+// within ~10%.
+double many_row_us(int mf, int nf, int ks, int N, int K, int m_cap) {
+  const int n_mt = (m_cap + 32 * mf - 1) / (32 * mf);
+  const int n_nt = (N + 128 * nf - 1) / (128 * nf);
+  const long wgs = (long)n_mt * n_nt * ks;
+  const long rounds = (wgs + kTargetWorkgroups - 1) / kTargetWorkgroups;
+  const double eff = nf == 4 ? 1.12 : mf == 3 ? 0.97 : 1.0;
+  const double t_wg =
+      2.0 * 32 * mf * 128 * nf * ((double)K / ks) / (0.45 * 2.5e15 / 256) * 1e6;
+  return rounds * t_wg / eff + (double)ks * m_cap * N * 4 / 5e12 * 1e6;
+}
+
+}  // namespace
+
+GemmPlan gemm_plan(int N, int K, int m_cap, int elem_bytes, bool retile) {
   GemmPlan g{};
   if (elem_bytes == 4) {
     g.mf = m_cap <= 16 ? 1 : (m_cap <= 32 ? 2 : 4);  // 16-row tiles
@@ -544,6 +566,32 @@ GemmPlan gemm_plan(int N, int K, int m_cap, int elem_bytes) {
   g.pf = (g.mf == 4 && g.nf == 1 && (K / 64) % 4 == 0) ? 4 : 2;
   const int n_nt = (N + 128 * g.nf - 1) / (128 * g.nf);
   g.ks = pick_split(n_mt * n_nt, K, g.pf);
+  if (retile && g.mf == 4 && m_cap > 128) {
+    // plain projections (K-split partials summed by the consumer): tiles
+    // of 384 weight rows or of 96 activation rows when they fill the chip's
+    // rounds evenly enough to be clearly faster (estimate > 8% lower).
+    // Measured, weights cold: 1024 x 6144 x 4096 62 -> 51 us (384-row
+    // weight tiles, 2 K-chunks); 384 rows x 8192 x 8192 58 -> 54 us and
+    // x 28672 188 -> 178 us (96-row tiles); 96-row tiles at 192 rows made
+    // the 70B drafting block 7% slower, so they need 256 rows or more.  The
+    // K-split stays within the one-row plan's (the partial buffers are
+    // sized for it).
+    const int ks_cap = pick_split((N + 127) / 128, K, 2);
+    const double base = many_row_us(g.mf, g.nf, g.ks, N, K, m_cap);
+    double best = 0.92 * base;
+    const int cand[2][2] = {{4, 3}, {3, 2}};
+    for (const auto& c : cand) {
+      const int mf = c[0], nf = c[1];
+      if (N % (128 * nf) != 0 || (mf == 3 && m_cap < 256)) continue;
+      const int tiles = ((m_cap + 32 * mf - 1) / (32 * mf)) * (N / (128 * nf));
+      const int ks = std::min(pick_split(tiles, K, 2), ks_cap);
+      const double t = many_row_us(mf, nf, ks, N, K, m_cap);
+      if (t < best) {
+        best = t;
+        g = GemmPlan{mf, nf, 2, ks};
+      }
+    }
+  }
   return g;
 }
 
@@ -601,6 +649,10 @@ void launch_tile(const GemmPlan& g, const bf16_t* X, int ldx, const bf16_t* W,
   SB_LAUNCH(4, 1, 4)
   SB_LAUNCH(4, 2, 2)
   SB_LAUNCH(4, 4, 2)
+  if constexpr (!SWIGLU && VR == 0) {   // re-tiled plain projections only
+    SB_LAUNCH(4, 3, 2)
+    SB_LAUNCH(3, 2, 2)
+  }
 #undef SB_LAUNCH
 }
 
@@ -610,7 +662,7 @@ template <typename T>
 int launch_gemm_xwt(const T* X, int ldx, const T* W, int N, int K, float* P,
                     size_t part_stride, const int* m_count, int m_cap,
                     int ksplit, hipStream_t st) {
-  const GemmPlan g = gemm_plan(N, K, m_cap, sizeof(T));
+  const GemmPlan g = gemm_plan(N, K, m_cap, sizeof(T), true);
   if constexpr (sizeof(T) == 2) {
     int ks = g.ks;
     if (ksplit > 0)

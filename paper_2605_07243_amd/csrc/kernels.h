@@ -56,7 +56,10 @@ struct GemmPlan {
 // Shapes the GEMMs take: bf16 N % 32 == 0 and K % 128 == 0 (fragment-packed
 // weights); f32 N % 16 == 0 and K % 32 == 0.
 bool gemm_shape_ok(int N, int K, int elem_bytes);
-GemmPlan gemm_plan(int N, int K, int m_cap, int elem_bytes);
+// retile: the call sums K-split partials in its consumer (plain
+// projections); the many-row planner may then pick other tile shapes.
+GemmPlan gemm_plan(int N, int K, int m_cap, int elem_bytes,
+                   bool retile = false);
 // Largest K-split any call of this shape may use (partial-buffer sizing).
 // Kernel-attached timing of the next projection-GEMM launch (profiling).
 void gemm_time_next_launch(hipEvent_t start, hipEvent_t stop);
