@@ -46,71 +46,83 @@ __global__ void plan_block_kernel(TreeDims td, int m, sb_tree t,
                                   int* __restrict__ call_seq,
                                   int* __restrict__ call_row,
                                   int* __restrict__ n_call) {
-  __shared__ int cnt[SB_MAX_SEQS], old[SB_MAX_SEQS], off[SB_MAX_SEQS];
+  __shared__ int cnt[SB_MAX_SEQS], old[SB_MAX_SEQS], off[SB_MAX_SEQS + 1];
+  __shared__ int Ts[SB_MAX_SEQS];
   const int K = td.K, rw = td.rw;
-  if (threadIdx.x == 0) {
-    int o = 0;
-    for (int s = 0; s < td.S; ++s) {
-      const int n_old = t.n_rows[s];
-      int nst = min(t.n_starts[s], td.B_max);
-      nst = max(0, min(nst, (td.row_cap - n_old) / K));
-      cnt[s] = nst * K;
-      old[s] = n_old;
-      off[s] = o;
-      p.seq_off[s] = o;
-      p.prefix_len[s] = T[s];
-      p.seg_len[s] = n_old + nst * K;
-      blk_row0[s] = n_old;
-      blk_nst[s] = nst;
-      o += nst * K;
-    }
-    p.seq_off[td.S] = o;
-    *p.n = o;
-    *n_call = o;
+  const int tid = threadIdx.x;
+  // every sequence's counts loaded at once (one thread each), offsets by a
+  // scan in LDS, then one pass over all rows: no chain of dependent global
+  // round trips per sequence
+  if (tid < td.S) {
+    const int s = tid;
+    const int n_old = t.n_rows[s];
+    int nst = min(t.n_starts[s], td.B_max);
+    nst = max(0, min(nst, (td.row_cap - n_old) / K));
+    cnt[s] = nst * K;
+    old[s] = n_old;
+    Ts[s] = T[s];
+    p.prefix_len[s] = Ts[s];
+    p.seg_len[s] = n_old + nst * K;
+    blk_row0[s] = n_old;
+    blk_nst[s] = nst;
   }
   __syncthreads();
-  for (int i = off[td.S - 1] + cnt[td.S - 1] + threadIdx.x; i < out_cap;
-       i += blockDim.x) {
+  if (tid == 0) {
+    int o = 0;
+    for (int s = 0; s < td.S; ++s) {
+      off[s] = o;
+      o += cnt[s];
+    }
+    off[td.S] = o;
+  }
+  __syncthreads();
+  const int total = off[td.S];
+  if (tid <= td.S) p.seq_off[tid] = off[tid];
+  if (tid == 0) {
+    *p.n = total;
+    *n_call = total;
+  }
+  for (int i = total + tid; i < out_cap; i += blockDim.x) {
     call_seq[i] = -1;
     call_row[i] = -1;
   }
-  for (int s = 0; s < td.S; ++s) {
-    for (int j = threadIdx.x; j < cnt[s]; j += blockDim.x) {
-      const int b = j / K, k = j % K + 1;
-      const int i = off[s] + j;
-      const int lr = old[s] + j;
-      call_seq[i] = s;
-      call_row[i] = lr;
-      const int sn = t.starts[(size_t)s * td.B_max + b];
-      const size_t nidx = (size_t)s * td.budget + sn;
-      const int srow = t.row[nidx];
-      p.seq[i] = s;
-      p.slot[i] = lr;
-      p.pos[i] = T[s] + t.depth[nidx] + k;
-      p.token[i] = t.token[nidx];
-      p.k[i] = k;
-      p.pred[i] = k > 1 ? i - 1 : i;
-      p.cond[i] = (m == 1 || srow < 0) ? s : s * td.row_cap + srow;
-      p.out_row[i] = s * td.row_cap + lr;
-      p.kv_dst[i] = -1;
-      const size_t rbase = (size_t)s * td.row_cap;
-      for (int w = 0; w < rw; ++w) {
-        uint32_t bits = (m > 1 && srow >= 0) ? t.row_vis[(rbase + srow) * rw + w] : 0u;
-        // own block rows lr-k+1 .. lr
-        for (int q = lr - k + 1; q <= lr; ++q)
-          if ((q >> 5) == w) bits |= 1u << (q & 31);
-        t.row_vis[(rbase + lr) * rw + w] = bits;
-        p.vis[(size_t)i * p.vis_words + w] = bits;
-      }
-      t.row_block[rbase + lr] = m;
-      t.row_start[rbase + lr] = sn;
-      t.row_k[rbase + lr] = k;
-      t.row_pos[rbase + lr] = p.pos[i];
+  for (int i = tid; i < total; i += blockDim.x) {
+    int s = 0;
+    while (off[s + 1] <= i) ++s;
+    const int j = i - off[s];
+    const int b = j / K, k = j % K + 1;
+    const int lr = old[s] + j;
+    call_seq[i] = s;
+    call_row[i] = lr;
+    const int sn = t.starts[(size_t)s * td.B_max + b];
+    const size_t nidx = (size_t)s * td.budget + sn;
+    const int srow = t.row[nidx];
+    const int pos = Ts[s] + t.depth[nidx] + k;
+    p.seq[i] = s;
+    p.slot[i] = lr;
+    p.pos[i] = pos;
+    p.token[i] = t.token[nidx];
+    p.k[i] = k;
+    p.pred[i] = k > 1 ? i - 1 : i;
+    p.cond[i] = (m == 1 || srow < 0) ? s : s * td.row_cap + srow;
+    p.out_row[i] = s * td.row_cap + lr;
+    p.kv_dst[i] = -1;
+    const size_t rbase = (size_t)s * td.row_cap;
+    for (int w = 0; w < rw; ++w) {
+      uint32_t bits = (m > 1 && srow >= 0) ? t.row_vis[(rbase + srow) * rw + w] : 0u;
+      // own block rows lr-k+1 .. lr
+      for (int q = lr - k + 1; q <= lr; ++q)
+        if ((q >> 5) == w) bits |= 1u << (q & 31);
+      t.row_vis[(rbase + lr) * rw + w] = bits;
+      p.vis[(size_t)i * p.vis_words + w] = bits;
     }
+    t.row_block[rbase + lr] = m;
+    t.row_start[rbase + lr] = sn;
+    t.row_k[rbase + lr] = k;
+    t.row_pos[rbase + lr] = pos;
   }
   __syncthreads();
-  if (threadIdx.x == 0)
-    for (int s = 0; s < td.S; ++s) t.n_rows[s] = old[s] + cnt[s];
+  if (tid < td.S) t.n_rows[tid] = old[tid] + cnt[tid];
 }
 
 // Sibling attachment of one block in (k, start, rank) order within the
@@ -263,38 +275,42 @@ __global__ __launch_bounds__(64) void attach_kernel(
 __global__ void plan_verify_kernel(TreeDims td, sb_tree t,
                                    const int* __restrict__ T, CallPlan p) {
   __shared__ int off[SB_MAX_SEQS + 1];
-  if (threadIdx.x == 0) {
-    int o = 0;
-    for (int s = 0; s < td.S; ++s) {
-      off[s] = o;
-      p.seq_off[s] = o;
-      p.prefix_len[s] = T[s];
-      const int n = min(t.n_nodes[s], td.budget);
-      p.seg_len[s] = n;
-      o += n;
-    }
-    off[td.S] = o;
-    p.seq_off[td.S] = o;
-    *p.n = o;
+  __shared__ int Ts[SB_MAX_SEQS];
+  const int tid = threadIdx.x;
+  // counts loaded at once, offsets by a scan in LDS, one pass over all rows
+  if (tid < td.S) {
+    off[tid + 1] = min(t.n_nodes[tid], td.budget);
+    Ts[tid] = T[tid];
   }
   __syncthreads();
-  for (int s = 0; s < td.S; ++s) {
-    const int n = off[s + 1] - off[s];
-    for (int j = threadIdx.x; j < n; j += blockDim.x) {
-      const int i = off[s] + j;
-      const size_t nidx = (size_t)s * td.budget + j;
-      p.seq[i] = s;
-      p.slot[i] = j;
-      p.pos[i] = T[s] + t.depth[nidx];
-      p.token[i] = t.token[nidx];
-      p.k[i] = 1;
-      p.pred[i] = i;
-      p.cond[i] = -1;
-      p.out_row[i] = s * td.budget + j;
-      p.kv_dst[i] = -1;
-      for (int w = 0; w < p.vis_words; ++w)
-        p.vis[(size_t)i * p.vis_words + w] = w < td.bw ? t.anc[nidx * td.bw + w] : 0u;
-    }
+  if (tid == 0) {
+    off[0] = 0;
+    for (int s = 0; s < td.S; ++s) off[s + 1] += off[s];
+  }
+  __syncthreads();
+  const int total = off[td.S];
+  if (tid < td.S) {
+    p.prefix_len[tid] = Ts[tid];
+    p.seg_len[tid] = off[tid + 1] - off[tid];
+  }
+  if (tid <= td.S) p.seq_off[tid] = off[tid];
+  if (tid == 0) *p.n = total;
+  for (int i = tid; i < total; i += blockDim.x) {
+    int s = 0;
+    while (off[s + 1] <= i) ++s;
+    const int j = i - off[s];
+    const size_t nidx = (size_t)s * td.budget + j;
+    p.seq[i] = s;
+    p.slot[i] = j;
+    p.pos[i] = Ts[s] + t.depth[nidx];
+    p.token[i] = t.token[nidx];
+    p.k[i] = 1;
+    p.pred[i] = i;
+    p.cond[i] = -1;
+    p.out_row[i] = s * td.budget + j;
+    p.kv_dst[i] = -1;
+    for (int w = 0; w < p.vis_words; ++w)
+      p.vis[(size_t)i * p.vis_words + w] = w < td.bw ? t.anc[nidx * td.bw + w] : 0u;
   }
 }
 
