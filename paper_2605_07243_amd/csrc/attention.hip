@@ -81,14 +81,11 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
   {
     const int gx = gridDim.x, gy = gridDim.y;
     const int total = gx * gy * (int)gridDim.z;
-    if ((total & 7) == 0) {
-      const int b = bx + gx * (by + gy * bz);
-      const int l = (b & 7) * (total >> 3) + (b >> 3);
-      const int gz = (int)gridDim.z;
-      bx = l % gx;
-      bz = (l / gx) % gz;
-      by = l / (gx * gz);
-    }
+    const int l = xcd_grouped(bx + gx * (by + gy * bz), total);
+    const int gz = (int)gridDim.z;
+    bx = l % gx;
+    bz = (l / gx) % gz;
+    by = l / (gx * gz);
   }
   const int s = by / Hkv, kh = by % Hkv;
   const int G = H / Hkv;
@@ -462,14 +459,11 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
   {
     const int gx = gridDim.x, gy = gridDim.y;
     const int total = gx * gy * (int)gridDim.z;
-    if ((total & 7) == 0) {
-      const int b = bx + gx * (by + gy * bz);
-      const int l = (b & 7) * (total >> 3) + (b >> 3);
-      const int gz = (int)gridDim.z;
-      bx = l % gx;
-      bz = (l / gx) % gz;
-      by = l / (gx * gz);
-    }
+    const int l = xcd_grouped(bx + gx * (by + gy * bz), total);
+    const int gz = (int)gridDim.z;
+    bx = l % gx;
+    bz = (l / gx) % gz;
+    by = l / (gx * gz);
   }
   int s, kh, qg, zs, nzs, split_tok;
   if (split_rows != nullptr) {

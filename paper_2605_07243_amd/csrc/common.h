@@ -159,6 +159,17 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return t;
 }
 
+// Logical workgroup id for a launch of `total` workgroups whose neighbours
+// should share an XCD's L2.  The dispatcher deals workgroups out round-robin
+// over the 8 XCDs (id b to XCD b % 8); with total = 8 q + r, XCD x holds
+// q + (x < r) of them and is given the contiguous logical ids starting at
+// x q + min(x, r).  A bijection for every total (for r = 0 it is
+// (b % 8) q + b / 8).
+__device__ __forceinline__ int xcd_grouped(int b, int total) {
+  const int x = b & 7, q = total >> 3, r = total & 7;
+  return x * q + min(x, r) + (b >> 3);
+}
+
 // Larger (value, smaller id) first.
 __device__ __forceinline__ bool better(float v, int id, float bv, int bid) {
   return v > bv || (v == bv && id < bid);

@@ -113,7 +113,7 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(
   __shared__ __attribute__((aligned(16))) bf16_t xs[2][BM][LD];
   const int total = gridDim.x;
   int b = blockIdx.x;
-  if ((total & 7) == 0) b = (b & 7) * (total >> 3) + (b >> 3);
+  b = xcd_grouped(b, total);
   const int mt = b % n_mt;
   const int rest = b / n_mt;
   const int nt = rest % n_nt;
