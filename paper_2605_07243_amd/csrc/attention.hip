@@ -57,7 +57,7 @@ template <typename T, int HD, int NQ, int QT>
 __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
     const T* __restrict__ q, CallPlan p, KVView kv, int H, int Hkv,
     int split_tokens, float scale, float* __restrict__ o_part,
-    float* __restrict__ ml, T* __restrict__ out) {
+    float* __restrict__ ml, T* __restrict__ out, int key_cap) {
   constexpr int ES = sizeof(T);
   constexpr int LDK = HD + 16 / ES;                 // padded K row
   constexpr int LDV = 32 + 16 / ES;                 // padded V^T row
@@ -127,7 +127,9 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
   const T* skp = static_cast<const T*>(kv.seg_k);
   const T* svp = static_cast<const T*>(kv.seg_v);
   const int* ptab = kv.page_table + (size_t)s * kv.max_pages;
-  const int Tp = min(p.prefix_len[s], kv.max_pages * 16);
+  // committed keys: the prefix, within the page table and the length bound
+  // (a bound below a prefix skips the entries past it)
+  const int Tp = min(min(p.prefix_len[s], kv.max_pages * 16), key_cap);
   const int t0 = bz * split_tokens;
   const int t1 = min(Tp, t0 + split_tokens);
   const bool last_split = bz == gridDim.z - 1;
@@ -375,13 +377,13 @@ __device__ __forceinline__ int n_splits_of(int tiles, int sp) {
 }
 
 __device__ SplitItem balanced_split(const CallPlan& p, int max_pages, int gx,
-                                    int max_split, int b) {
+                                    int max_split, int b, int key_cap) {
   const int lane = threadIdx.x & 63;
   bool act = false;
   int t = 0;
   if (lane < p.n_seqs) {
     act = p.seq_off[lane + 1] > p.seq_off[lane];
-    t = (min(p.prefix_len[lane], max_pages * 16) + 63) >> 6;
+    t = (min(min(p.prefix_len[lane], max_pages * 16), key_cap) + 63) >> 6;
   }
   const int total = wave_sum_i(act ? t : 0);
   int tmax = act ? t : 0;
@@ -437,7 +439,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
     const bf16_t* __restrict__ q, CallPlan p, KVView kv, int H, int Hkv,
     int split_tokens, float scale, float* __restrict__ o_part,
     float* __restrict__ ml, bf16_t* __restrict__ out, int n_groups,
-    int max_split, int* __restrict__ split_rows) {
+    int max_split, int* __restrict__ split_rows, int key_cap) {
   constexpr int KT = 64;                    // keys per tile
   constexpr int LDK = HD + 8;               // K row: 16 B mod 256 B
   constexpr int LDV = KT + 4;               // V^T row: 136 B, 8-byte reads
@@ -468,7 +470,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
   int s, kh, qg, zs, nzs, split_tok;
   if (split_rows != nullptr) {
     const SplitItem it =
-        balanced_split(p, kv.max_pages, Hkv * n_groups, max_split, bx);
+        balanced_split(p, kv.max_pages, Hkv * n_groups, max_split, bx, key_cap);
     if (!it.live) return;                   // uniform: every wave agrees
     s = it.s;
     kh = it.item / n_groups;
@@ -517,7 +519,9 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
   const bf16_t* skp = static_cast<const bf16_t*>(kv.seg_k);
   const bf16_t* svp = static_cast<const bf16_t*>(kv.seg_v);
   const int* ptab = kv.page_table + (size_t)s * kv.max_pages;
-  const int Tp = min(p.prefix_len[s], kv.max_pages * 16);
+  // committed keys: the prefix, within the page table and the length bound
+  // (a bound below a prefix skips the entries past it)
+  const int Tp = min(min(p.prefix_len[s], kv.max_pages * 16), key_cap);
   const int t0 = zs * split_tok;
   const int t1 = min(Tp, t0 + split_tok);
   const bool last_split = zs == nzs - 1;
@@ -950,7 +954,8 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
   if (hd == HD_ && a.nq == NW_) {                                             \
     hipExtLaunchKernelGGL(tree_attn32_kernel<HD_, NW_>, g32, dim3(NW_ * 64),  \
                           0, st, ka, kb32, 0, q, p, kv, H, Hkv, split_tokens, \
-                          scale, o_part, ml, out, a.groups, ms, sr);          \
+                          scale, o_part, ml, out, a.groups, ms, sr,           \
+                          max_prefix);                                        \
     if (merge)                                                                \
       launch_attn_merge<T>(p, H, hd, ms, o_part, ml, out, st, eb, sr);        \
     return;                                                                   \
@@ -964,7 +969,7 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
   if (hd == HD_ && a.nq == NQ_ && a.qt == QT_) {                              \
     hipExtLaunchKernelGGL(tree_attn_kernel<T, HD_, NQ_, QT_>, grid,           \
                           dim3(NQ_ * 64), 0, st, ka, kb, 0, q, p, kv, H, Hkv, \
-                          split_tokens, scale, o_part, ml, out);              \
+                          split_tokens, scale, o_part, ml, out, max_prefix);  \
     if (n_split > 1)                                                          \
       launch_attn_merge<T>(p, H, hd, n_split, o_part, ml, out, st, eb);       \
     return;                                                                   \
