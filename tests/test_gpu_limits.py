@@ -12,7 +12,9 @@ target, d 256) so that the oracle recomputes every call:
   tree: ten tokens per row, the branching maximum, so block 1 puts exactly
   64 starts forward);
 * 64 sequences, the per-call maximum, with small trees; the oracle recomputes
-  four of them while the device runs all.
+  four of them while the device runs all;
+* the shortest prompts and page edges: prompts of 1, 2, 16, 17 and 33 tokens
+  through the device prefill (against the oracle's) and one iteration.
 
 The committed prefix is seeded random K/V (as at the benchmark shapes), one
 iteration is compared call by call with teacher forcing (see parity_checks),
@@ -24,8 +26,9 @@ import pytest
 import torch
 
 import synth
+from oracle import specdec
 
-from gpu_harness import inject, models, runtime
+from gpu_harness import host, inject, models, rel_err, runtime
 from parity_checks import Tally, oracle_iteration, run_and_compare
 from test_gpu_configs import synthetic_state
 
@@ -97,5 +100,49 @@ def test_iteration_at_limits(name):
     log(f"[{name}] {tally}")
     if forced is not None:
         rt.set_buckets(None)
+    assert tally.rows == sum(sum(e["R"] for e in seqs[s][2]["expansions"])
+                             for s in seqs)
+
+
+EDGE = synth.Workload("edge-prompts-fp32", "f32", synth.TINY, 1, K=4, M=3,
+                      B_max=4, budget=32, n_seqs=5, prompt_len=(1, 33))
+
+
+def test_short_and_page_edge_prompts():
+    """Prompts of 1, 2, 16, 17 and 33 tokens: a one-token prompt commits one
+    entry (its drafter entry conditioned on zero taps, reading R2) and the
+    root is the target's next token; 16 and 17 end on and just past a page
+    boundary.  Device prefill against the oracle's (caches, root, condition
+    taps), then one iteration compared call by call."""
+    w = EDGE
+    weights, tgt, dr = models(w)
+    lens = [1, 2, 16, 17, 33]
+    prompts = synth.prompts(w, lengths=lens)
+    states = [specdec.prefill(tgt, dr, pr) for pr in prompts]
+    rt = runtime(w, weights, max_pages=8)
+    log("[edge] prefill")
+    rt.prefill(prompts)
+    torch.cuda.synchronize()
+    for s, st in enumerate(states):
+        assert int(rt.T[s]) == st.T, s
+        assert int(rt.root[s]) == st.root, s
+        assert rel_err(host(rt.cond_taps[s]), st.cond_taps).max() < TOL, s
+        for which, kv, layers in (("target", st.tkv, w.target.n_layers),
+                                  ("drafter", st.dkv, w.drafter_layers)):
+            k, v = rt.read_cache(which, s, st.T)
+            for layer in range(layers):
+                for got, ref in ((k, kv.k), (v, kv.v)):
+                    assert rel_err(got[layer].reshape(st.T, -1),
+                                   ref[layer].reshape(st.T, -1)).max() < TOL, \
+                        (s, which, layer)
+    for s, st in enumerate(states):
+        inject(rt, s, st)
+    seqs = {}
+    for s, st in enumerate(states):
+        seqs[s] = (st,) + oracle_iteration(tgt, dr, st, w, 2 + s)
+    tally = Tally()
+    run_and_compare(rt, seqs, w, tgt, dr, TOL, tally,
+                    log=lambda m: log(f"[edge] {m}"))
+    log(f"[edge] {tally}")
     assert tally.rows == sum(sum(e["R"] for e in seqs[s][2]["expansions"])
                              for s in seqs)
