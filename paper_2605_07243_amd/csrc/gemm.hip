@@ -100,13 +100,15 @@ __device__ __forceinline__ void vr_stats_merge(float& m, float& s, float& u,
 // VR > 0 (LM heads, one K-chunk): besides (or, with P == nullptr, instead
 // of) the fp32 outputs, each workgroup writes for every row the vocabulary
 // record (top VR, m, s, u) of its 128 NF output columns to
-// rec[(row * n_nt + column tile) * (2 VR + 3)].
+// rec[(row * n_nt + column tile) * (2 VR + 3)].  n_first (a multiple of
+// 32 NF; 0 with VR > 0): the launch covers weight rows n_first .. N - 1, in
+// n_nt column tiles from there.
 template <int MF, int NF, int PF, bool SWIGLU, int VR>
 __global__ __launch_bounds__(256) void gemm_tile_kernel(
     const bf16_t* __restrict__ X, int ldx, const bf16_t* __restrict__ W,
     int K, float* __restrict__ P, int N, size_t part_stride,
     const int* __restrict__ m_count, int k_chunk, int n_mt, int n_nt,
-    bf16_t* __restrict__ act, int F, float* __restrict__ rec) {
+    bf16_t* __restrict__ act, int F, float* __restrict__ rec, int n_first) {
   static_assert(PF == 2 || PF == 4, "weight ring depth");
   constexpr int BM = 32 * MF;
   constexpr int LD = 64 + 8;
@@ -123,7 +125,7 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(
   if (m_base >= M) return;  // whole workgroup
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int lr = lane & 31, h = lane >> 5;
-  const int nb = nt * (128 * NF) + wave * (32 * NF);  // first weight row
+  const int nb = n_first + nt * (128 * NF) + wave * (32 * NF);  // first row
   const bool wave_on = nb < N;                         // N % 32 == 0 tails
   const int kc0 = kc * k_chunk;
   const int nstage = k_chunk / 64;
@@ -525,7 +527,7 @@ namespace {
 // 96 x 256 tiles 0.97 of 128 x 256), plus the consumer's read of the ks
 // fp32 partial slabs at 5 TB/s.  Fits the measured 8B and 70B projections
 // within ~10%.
-double many_row_us(int mf, int nf, int ks, int N, int K, int m_cap) {
+double tile_rounds_us(int mf, int nf, int ks, int N, int K, int m_cap) {
   const int n_mt = (m_cap + 32 * mf - 1) / (32 * mf);
   const int n_nt = (N + 128 * nf - 1) / (128 * nf);
   const long wgs = (long)n_mt * n_nt * ks;
@@ -533,7 +535,12 @@ double many_row_us(int mf, int nf, int ks, int N, int K, int m_cap) {
   const double eff = nf == 4 ? 1.12 : mf == 3 ? 0.97 : 1.0;
   const double t_wg =
       2.0 * 32 * mf * 128 * nf * ((double)K / ks) / (0.45 * 2.5e15 / 256) * 1e6;
-  return rounds * t_wg / eff + (double)ks * m_cap * N * 4 / 5e12 * 1e6;
+  return rounds * t_wg / eff;
+}
+
+double many_row_us(int mf, int nf, int ks, int N, int K, int m_cap) {
+  return tile_rounds_us(mf, nf, ks, N, K, m_cap) +
+         (double)ks * m_cap * N * 4 / 5e12 * 1e6;
 }
 
 }  // namespace
@@ -628,9 +635,13 @@ template <bool SWIGLU, int VR = 0>
 void launch_tile(const GemmPlan& g, const bf16_t* X, int ldx, const bf16_t* W,
                  int N, int K, float* P, size_t part_stride,
                  const int* m_count, int m_cap, int ks, bf16_t* act, int F,
-                 hipStream_t st, float* rec = nullptr) {
+                 hipStream_t st, float* rec = nullptr, int n_first = 0,
+                 int n_rows = -1) {
+  // weight rows n_first .. n_first + n_rows - 1 (n_first + n_rows is N or a
+  // multiple of 128 nf)
+  const int rows = n_rows < 0 ? N - n_first : n_rows;
   const int n_mt = (m_cap + 32 * g.mf - 1) / (32 * g.mf);
-  const int n_nt = (N + 128 * g.nf - 1) / (128 * g.nf);
+  const int n_nt = (rows + 128 * g.nf - 1) / (128 * g.nf);
   const int k_chunk = K / ks;
   const dim3 grid(n_mt * n_nt * ks);
 #define SB_LAUNCH(MF_, NF_, PF_)                                              \
@@ -640,7 +651,7 @@ void launch_tile(const GemmPlan& g, const bf16_t* X, int ldx, const bf16_t* W,
     hipExtLaunchKernelGGL(gemm_tile_kernel<MF_, NF_, PF_, SWIGLU, VR>, grid,  \
                           dim3(256), 0, st, ea, eb, 0, X, ldx, W, K, P, N,    \
                           part_stride, m_count, k_chunk, n_mt, n_nt, act, F,  \
-                          rec);                                               \
+                          rec, n_first);                                      \
     return;                                                                   \
   }
   SB_LAUNCH(1, 1, 2)
@@ -649,10 +660,8 @@ void launch_tile(const GemmPlan& g, const bf16_t* X, int ldx, const bf16_t* W,
   SB_LAUNCH(4, 1, 4)
   SB_LAUNCH(4, 2, 2)
   SB_LAUNCH(4, 4, 2)
-  if constexpr (!SWIGLU && VR == 0) {   // re-tiled plain projections only
-    SB_LAUNCH(4, 3, 2)
-    SB_LAUNCH(3, 2, 2)
-  }
+  if constexpr (VR == 0) SB_LAUNCH(4, 3, 2)   // re-tiled or split launches
+  if constexpr (!SWIGLU && VR == 0) SB_LAUNCH(3, 2, 2)
 #undef SB_LAUNCH
 }
 
@@ -719,12 +728,77 @@ int gemm_vocab_chunks(int N, int K, int m_cap) {
   return (N + 128 * g.nf - 1) / (128 * g.nf);
 }
 
+namespace {
+
+// One launch of a SwiGLU projection over weight rows n_first ..
+// n_first + rows - 1.
+struct SwigluPart {
+  GemmPlan g;
+  int n_first, rows;
+};
+
+int weight_stages(int nf, int K) { return nf == 1 && (K / 64) % 4 == 0 ? 4 : 2; }
+
+// The gate/up projection has no K-split (SiLU(g) u is not linear in the
+// K-chunks), so with many rows its last round of workgroups can run part
+// empty: 1024 rows x 28672 gate/up rows make 448 workgroups of 128 x 512,
+// 1.75 rounds of 256.  Two launches over consecutive weight-row ranges,
+// each with tiles that fill their rounds, finish sooner: one round of
+// 128 x 512 tiles, then one of 128 x 384 (estimate 7% less; 384 rows x
+// 57344: one round of 128 x 512 and 0.63 of 128 x 256, 6% less).  Taken
+// when the estimate, with the second launch's start, is > 5% lower.
+int swiglu_parts(int N, int K, int m_cap, SwigluPart part[2]) {
+  const GemmPlan g = gemm_plan(N, K, m_cap, 2);
+  part[0] = SwigluPart{g, 0, N};
+  const int n_mt = (m_cap + 127) / 128;
+  if (g.mf != 4 || m_cap <= 128 || n_mt > kTargetWorkgroups) return 1;
+  constexpr double kSecondLaunchUs = 3.0;
+  double best = 0.95 * tile_rounds_us(4, g.nf, 1, N, K, m_cap);
+  int parts = 1;
+  for (const int nfa : {4, 2}) {
+    for (int r = 1;; ++r) {
+      const int rows_a = kTargetWorkgroups * r / n_mt * 128 * nfa;
+      if (rows_a >= N) break;
+      const int rows_b = N - rows_a;
+      for (int nfb = 4; nfb >= 1; --nfb) {   // wider tiles on a tie
+        if (rows_b % (32 * nfb) != 0) continue;
+        const double t = tile_rounds_us(4, nfa, 1, rows_a, K, m_cap) +
+                         tile_rounds_us(4, nfb, 1, rows_b, K, m_cap) +
+                         kSecondLaunchUs;
+        if (t < best) {
+          best = t;
+          parts = 2;
+          part[0] = SwigluPart{{4, nfa, weight_stages(nfa, K), 1}, 0, rows_a};
+          part[1] = SwigluPart{{4, nfb, weight_stages(nfb, K), 1}, rows_a, rows_b};
+        }
+      }
+    }
+  }
+  return parts;
+}
+
+}  // namespace
+
 void launch_gemm_swiglu(const bf16_t* X, int ldx, const bf16_t* W, int F,
                         int K, bf16_t* act, const int* m_count, int m_cap,
                         hipStream_t st) {
-  const GemmPlan g = gemm_plan(2 * F, K, m_cap, 2);
-  launch_tile<true>(g, X, ldx, W, 2 * F, K, nullptr, 0, m_count, m_cap, 1,
-                    act, F, st);
+  SwigluPart part[2];
+  const int parts = swiglu_parts(2 * F, K, m_cap, part);
+  if (parts == 1) {
+    launch_tile<true>(part[0].g, X, ldx, W, 2 * F, K, nullptr, 0, m_count,
+                      m_cap, 1, act, F, st);
+    return;
+  }
+  // profiling events: the start on the first launch, the stop on the second
+  hipEvent_t ea, eb;
+  take_events(ea, eb);
+  for (int i = 0; i < 2; ++i) {
+    g_ev_start = i == 0 ? ea : nullptr;
+    g_ev_stop = i == 1 ? eb : nullptr;
+    launch_tile<true>(part[i].g, X, ldx, W, 2 * F, K, nullptr, 0, m_count,
+                      m_cap, 1, act, F, st, nullptr, part[i].n_first,
+                      part[i].rows);
+  }
 }
 
 int launch_pack_weight(const bf16_t* src, bf16_t* dst, int rows, int cols,
