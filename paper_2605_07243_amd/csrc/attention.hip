@@ -449,7 +449,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
   constexpr int PER = (CH + NT - 1) / NT;
   constexpr int HB = HD / 32;               // head_dim blocks of 32
   constexpr int QK = HD / 16;               // contraction steps of S^T
-  constexpr int DEPTH = NW >= 8 ? 2 : 3;     // staging registers: 16 PER each
+  constexpr int DEPTH = NW >= 8 ? 1 : 3;     // staging registers: 16 PER each
   __shared__ __attribute__((aligned(16))) bf16_t ksh[2][KT][LDK];
   __shared__ __attribute__((aligned(16))) bf16_t vsh[2][HD][LDV];
   constexpr int MAXP = 1024;
@@ -627,15 +627,23 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
     const int w = i - n_pre;
     attn_f32x16_t sc[2];
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < 2; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) sc[b][r] = 0.f;
+    // the two 32-key blocks' chains interleaved, each K fragment read one
+    // contraction step ahead of its MFMA
+    auto kfrag = [&](int b, int j) {
+      return *reinterpret_cast<const attn_u32x4_t*>(&ksh[buf][32 * b + lq][16 * j + 8 * h]);
+    };
+    attn_u32x4_t kf0 = kfrag(0, 0), kf1 = kfrag(1, 0);
 #pragma unroll
-      for (int j = 0; j < QK; ++j) {
-        const attn_u32x4_t kf =
-            *reinterpret_cast<const attn_u32x4_t*>(&ksh[buf][32 * b + lq][16 * j + 8 * h]);
-        sc[b] = mma32_attn(kf, qf[j], sc[b]);
-      }
+    for (int j = 0; j < QK; ++j) {
+      const attn_u32x4_t nx0 = kfrag(0, min(j + 1, QK - 1));
+      const attn_u32x4_t nx1 = kfrag(1, min(j + 1, QK - 1));
+      sc[0] = mma32_attn(kf0, qf[j], sc[0]);
+      sc[1] = mma32_attn(kf1, qf[j], sc[1]);
+      kf0 = nx0;
+      kf1 = nx1;
     }
     // lane register r of block b is key 32 b + 8 (r / 4) + 4 h + r % 4
     float mx = SB_NEG;
