@@ -645,6 +645,19 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
       kf0 = nx0;
       kf1 = nx1;
     }
+    // V^T fragment of PV step t = (2 b + u) HB + hb; each is read two steps
+    // ahead, the first two before the softmax (the barrier keeps the
+    // compiler from sinking them next to their MFMAs)
+    constexpr int NPV = 4 * HB;
+    auto vfrag = [&](int t) {
+      const int b = t / (2 * HB), u = (t / HB) % 2, hb = t % HB;
+      const bf16_t* vr = &vsh[buf][32 * hb + lq][32 * b + 16 * u + 4 * h];
+      const uint2 lo = *reinterpret_cast<const uint2*>(vr);
+      const uint2 hi = *reinterpret_cast<const uint2*>(vr + 8);
+      return attn_u32x4_t{lo.x, lo.y, hi.x, hi.y};
+    };
+    attn_u32x4_t vf0 = vfrag(0), vf1 = vfrag(1);
+    __builtin_amdgcn_sched_barrier(0);
     // lane register r of block b is key 32 b + 8 (r / 4) + 4 h + r % 4
     float mx = SB_NEG;
     if (full) {
@@ -702,18 +715,13 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
     l_run += sum_x32(ps);
     // O^T[hd][query] += V^T[hd][keys] P^T[keys][query], 16 keys per step
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int k0 = 32 * b + 16 * u + 4 * h;
-#pragma unroll
-        for (int hb = 0; hb < HB; ++hb) {
-          const bf16_t* vr = &vsh[buf][32 * hb + lq][k0];
-          const uint2 lo = *reinterpret_cast<const uint2*>(vr);
-          const uint2 hi = *reinterpret_cast<const uint2*>(vr + 8);
-          acc[hb] = mma32_attn(attn_u32x4_t{lo.x, lo.y, hi.x, hi.y}, pf[b][u], acc[hb]);
-        }
-      }
+    for (int t = 0; t < NPV; ++t) {
+      const attn_u32x4_t vf2 = vfrag(min(t + 2, NPV - 1));
+      const int b = t / (2 * HB), u = (t / HB) % 2, hb = t % HB;
+      acc[hb] = mma32_attn(vf0, pf[b][u], acc[hb]);
+      vf0 = vf1;
+      vf1 = vf2;
+    }
   };
   if (n_tiles > 0) {
 #pragma unroll
