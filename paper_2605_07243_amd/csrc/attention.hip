@@ -935,8 +935,17 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
   g_attn_start = g_attn_stop = nullptr;
   // with a merge, the kernel carries the start event and the merge the stop
   hipEvent_t ka = ea, kb = n_split > 1 ? nullptr : eb;
-  const AttnShape a =
+  AttnShape a =
       attn_shape(rows_per_seq_cap, H / Hkv, p.n_seqs * Hkv, (int)sizeof(T));
+  if (sizeof(T) == 4 && hd == 128) {
+    // fp32 with 128-wide heads: at least two waves and one q-tile each (a
+    // lone wave's registers spill, and so do two q-tiles per wave); waves
+    // past the queries only load
+    const int qtiles = (rows_per_seq_cap * (H / Hkv) + 15) / 16;
+    a.nq = std::max(a.nq, 2);
+    a.qt = 1;
+    a.groups = (qtiles + a.nq - 1) / a.nq;
+  }
   // the caller picks n_split so that a split spans at most 1024 pages (the
   // kernels' page-table stage): max_prefix <= 1024 * 16 * n_split
   int split_tokens = (max_prefix + n_split - 1) / n_split;
@@ -990,8 +999,9 @@ void launch_tree_attn(const T* q, const CallPlan& p, const KVView& kv,
       launch_attn_merge<T>(p, H, hd, n_split, o_part, ml, out, st, eb);       \
     return;                                                                   \
   }
-    SB_ATTN(128, 8, 2) SB_ATTN(128, 8, 1) SB_ATTN(128, 4, 1)
-    SB_ATTN(128, 2, 1) SB_ATTN(128, 1, 1)
+    if constexpr (sizeof(T) == 2) SB_ATTN(128, 8, 2)
+    SB_ATTN(128, 8, 1) SB_ATTN(128, 4, 1) SB_ATTN(128, 2, 1)
+    if constexpr (sizeof(T) == 2) SB_ATTN(128, 1, 1)
     SB_ATTN(64, 8, 2) SB_ATTN(64, 8, 1) SB_ATTN(64, 4, 1)
     SB_ATTN(64, 2, 1) SB_ATTN(64, 1, 1)
 #undef SB_ATTN

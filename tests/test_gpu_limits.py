@@ -14,7 +14,11 @@ target, d 256) so that the oracle recomputes every call:
 * 64 sequences, the per-call maximum, with small trees; the oracle recomputes
   four of them while the device runs all;
 * the shortest prompts and page edges: prompts of 1, 2, 16, 17 and 33 tokens
-  through the device prefill (against the oracle's) and one iteration.
+  through the device prefill (against the oracle's) and one iteration;
+* fp32 with 128-wide heads (two heads, d 256), where the attention launch
+  takes its fallback shapes: one q-tile of queries per KV head (two-wave
+  workgroups whose second wave has no queries) and, with 16 sequences x 2
+  KV heads and 144-node trees, one q-tile per wave where bf16 takes two.
 
 The committed prefix is seeded random K/V (as at the benchmark shapes), one
 iteration is compared call by call with teacher forcing (see parity_checks),
@@ -44,6 +48,14 @@ MANY_SEQS = synth.Workload("many-seqs-fp32", "f32", synth.TINY, 1, K=4, M=2,
                            B_max=4, budget=16, n_seqs=64,
                            prompt_len=(10, 200))
 
+HD128 = synth.ModelShape(2, 256, 2, 2, 128, 512, 1024)
+HD128_ONE_QTILE = synth.Workload("hd128-fp32", "f32", HD128, 1, K=4, M=2,
+                                 B_max=4, budget=16, n_seqs=2,
+                                 prompt_len=(40, 90))
+HD128_MANY = synth.Workload("hd128-16seq-fp32", "f32", HD128, 1, K=4, M=2,
+                            B_max=8, budget=144, n_seqs=16,
+                            prompt_len=(20, 120))
+
 CASES = {
     # name: (workload, uniform fixed-k tree (0: paper-frequency buckets; -1:
     # the rank head's own), sequences the oracle runs)
@@ -51,6 +63,8 @@ CASES = {
     "budget512-uniform8": (BIG_TREE, 8, None),
     "bmax64-uniform10": (WIDE, 10, None),
     "64-sequences": (MANY_SEQS, -1, (0, 21, 42, 63)),
+    "f32-head-dim-128-one-qtile": (HD128_ONE_QTILE, -1, None),
+    "f32-head-dim-128-16-sequences": (HD128_MANY, 0, (0, 7, 15)),
 }
 
 
