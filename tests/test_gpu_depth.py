@@ -23,6 +23,11 @@ random and different for every layer, so each layer's attention reads its
 own cache.  One iteration is compared call by call as in the per-layer-
 shape tests (teacher forcing oracle -> device, tie-aware discrete checks),
 with a planted greedy path that crosses a block boundary.
+
+The device loop itself (expansions, verification, acceptance and commit,
+iteration after iteration) is checked for losslessness at the same depth
+against an oracle that follows the device's committed stream, with and
+without the oracle's greedy continuation planted into the drafted trees.
 """
 import numpy as np
 import pytest
@@ -125,3 +130,121 @@ def test_iteration_full_depth(name):
     # the planted greedy path was accepted (run_and_compare checked that the
     # device's accepted path, bonus and committed K/V equal the oracle's)
     assert seqs[0][2]["tau"] >= 2
+
+
+
+class _Follower:
+    """The oracle target (and a copy with 1e-5 relative embedding noise)
+    fed the device's committed tokens one position at a time: after each
+    token, the logits it predicts the next one from."""
+
+    def __init__(self, tgt, st):
+        noisy = copy.copy(tgt)
+        noisy.embed = _PerturbedRows(tgt.embed, 1e-5, 17)
+        self.models = (tgt, noisy)
+        self.kv = [copy.deepcopy(st.tkv), copy.deepcopy(st.tkv)]
+        self.pos = st.T
+        self.z = self._feed(st.root)
+
+    def _feed(self, tok):
+        out = []
+        for m, kv in zip(self.models, self.kv):
+            seg = m.new_segment(1)
+            lg, _ = m.forward([tok], [self.pos], [0], [[0]], kv, seg)
+            for layer in range(len(kv.k)):
+                kv.append(layer, seg.k[layer][0], seg.v[layer][0])
+            out.append(lg[0])
+        self.pos += 1
+        return out
+
+    def check(self, tok):
+        """tok must be the greedy choice, or lose to it by no more than the
+        noise-derived bound; returns (greedy, margin, bound)."""
+        z, zn = self.z
+        g = specdec.argmax_low(z)
+        gap = float(z[g] - z[tok])
+        bound = max(TOL, 2 * float(rel_err(zn, z))) * float(np.abs(z).max())
+        self.z = self._feed(tok)
+        return g, gap, bound
+
+    def lookahead(self, n):
+        """The greedy continuation of n tokens from here (on a copy)."""
+        tgt = self.models[0]
+        kv = copy.deepcopy(self.kv[0])
+        z, out = self.z[0], []
+        for k in range(n):
+            out.append(specdec.argmax_low(z))
+            seg = tgt.new_segment(1)
+            lg, _ = tgt.forward([out[-1]], [self.pos + k], [0], [[0]], kv, seg)
+            for layer in range(len(kv.k)):
+                kv.append(layer, seg.k[layer][0], seg.v[layer][0])
+            z = lg[0]
+        return out
+
+
+@pytest.mark.parametrize("plant", [0, 3])
+def test_lossless_loop_full_depth(plant):
+    """The device's speculative loop at the 8B shape with all 32 target
+    layers (shared weights, random 1024-entry prefix): every committed token
+    must be the target's greedy choice after the tokens committed before it
+    (losslessness, Alg. 2 with the greedy acceptance walk).  The oracle
+    follows the device's committed stream; a token that differs from the
+    oracle's choice is allowed only at a near-tie, within the bound that the
+    oracle's own recomputation with 1e-5 relative input noise moves the
+    logits at that position (at least 2e-2 of max |z|).  With random
+    weights the drafter's own trees are never accepted past the root (one
+    token per iteration); with plant = 3 the oracle's greedy continuation
+    of the committed stream is written, before verification, onto the
+    tokens of the lowest-id depth-3 path of every drafted tree, so that
+    iterations accept several tokens and commit their K/V."""
+    w = synth.WORKLOADS["llama3-8b-k4"]
+    n_new = 8 if plant == 0 else 16
+    log("[lossless-32] weights (one shared target layer)")
+    weights, tgt, dr = shared_layer_models(w)
+    T = int(synth.prompt_lengths(w)[0])
+    st = synthetic_state(w, tgt, dr, 0, T, 7)
+    rt = runtime(w, weights,
+                 max_pages=(T + n_new * (w.M * w.K + 1) + 16) // 16 + 1,
+                 share_layers=True)
+    del weights
+    inject(rt, 0, st)
+    assert int(rt.root[0]) == st.root
+    fol = _Follower(tgt, st)
+    committed, accepted, ties, it = 0, [], 0, 0
+    while committed < n_new:
+        if plant:
+            look = fol.lookahead(plant)
+            for m in range(1, w.M + 1):
+                rt.expand(m)
+            n = int(rt.tree["n_nodes"][0])
+            depth = rt.tree["depth"][0, :n].cpu().numpy()
+            parent = rt.tree["parent"][0, :n].cpu().numpy()
+            node = int(np.nonzero(depth == min(plant, int(depth.max())))[0].min())
+            while node > 0:
+                rt.tree["token"][0, node] = look[int(depth[node]) - 1]
+                node = int(parent[node])
+            rt.verify()
+            rt.accept()
+            rt.commit()
+        else:
+            rt.iteration()
+        a = int(rt.aout["n_accepted"][0])
+        path = rt.aout["path"][0, :a].cpu().numpy()
+        toks = rt.tree["token"][0].cpu().numpy()
+        new = [int(toks[q]) for q in path] + [int(rt.aout["bonus"][0])]
+        for tok in new:
+            g, gap, bound = fol.check(tok)
+            if tok != g:
+                ties += 1
+                log(f"[lossless-32] token {committed}: device {tok}, oracle "
+                    f"{g}, margin {gap:.3e} (bound {bound:.3e})")
+                assert gap <= bound, (committed, gap, bound)
+            committed += 1
+        accepted.append(a)
+        it += 1
+        log(f"[lossless-32] iteration {it}: {a} accepted, {committed} "
+            f"tokens committed after the root")
+    log(f"[lossless-32] {committed} tokens in {it} iterations, accepted per "
+        f"iteration {accepted}, {ties} near-ties")
+    if plant:
+        assert sum(accepted) >= 2 and max(accepted) >= 2
