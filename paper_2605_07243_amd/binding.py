@@ -10,7 +10,10 @@ import ctypes as C
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libspecblock.so")
+# SPECBLOCK_LIB selects another build of the same library (the host
+# AddressSanitizer build of the ABI checks); the default is the in-tree one
+LIB_PATH = os.environ.get("SPECBLOCK_LIB") or os.path.join(HERE,
+                                                            "libspecblock.so")
 
 SB_OK, SB_EINVAL, SB_ESHAPE, SB_EBUDGET, SB_EDTYPE, SB_EHIP, SB_ESTATE = range(7)
 SB_F32, SB_BF16 = 0, 1

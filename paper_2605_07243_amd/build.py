@@ -5,6 +5,7 @@
 from __future__ import annotations
 
 import os
+import shlex
 import subprocess
 import sys
 from concurrent.futures import ThreadPoolExecutor
@@ -52,6 +53,35 @@ def build(verbose: bool = False) -> str:
           tmp])
     os.replace(tmp, LIB)
     return LIB
+
+
+ASAN_LIB = os.path.join(BUILD, "asan", "libspecblock_asan.so")
+
+
+def build_host_asan(verbose: bool = False) -> str:
+    """The same library with AddressSanitizer on its host code only (device
+    code is built as usual); loading it needs the clang ASan runtime
+    preloaded.  For the CPU checks of the host-side ABI paths."""
+    out = os.path.dirname(ASAN_LIB)
+    os.makedirs(out, exist_ok=True)
+    san = shlex.split("-Xarch_host -fsanitize=address "
+                      "-Xarch_host -fno-omit-frame-pointer")
+
+    def one(src):
+        obj = os.path.join(out, src + ".o")
+        cmd = [HIPCC, *FLAGS, *san, "-c", os.path.join(CSRC, src), "-o", obj]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        _run(cmd)
+        return obj
+
+    with ThreadPoolExecutor(max_workers=min(6, os.cpu_count() or 1)) as ex:
+        objs = list(ex.map(one, SOURCES))
+    tmp = ASAN_LIB + ".tmp"
+    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o",
+          tmp])
+    os.replace(tmp, ASAN_LIB)
+    return ASAN_LIB
 
 
 if __name__ == "__main__":
