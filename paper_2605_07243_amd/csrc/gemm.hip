@@ -661,7 +661,7 @@ void launch_tile(const GemmPlan& g, const bf16_t* X, int ldx, const bf16_t* W,
   SB_LAUNCH(4, 2, 2)
   SB_LAUNCH(4, 4, 2)
   if constexpr (VR == 0) SB_LAUNCH(4, 3, 2)   // re-tiled or split launches
-  if constexpr (!SWIGLU && VR == 0) SB_LAUNCH(3, 2, 2)
+  if constexpr (VR == 0) SB_LAUNCH(3, 2, 2)
 #undef SB_LAUNCH
 }
 
@@ -745,8 +745,9 @@ int weight_stages(int nf, int K) { return nf == 1 && (K / 64) % 4 == 0 ? 4 : 2; 
 // 1.75 rounds of 256.  Two launches over consecutive weight-row ranges,
 // each with tiles that fill their rounds, finish sooner: one round of
 // 128 x 512 tiles, then one of 128 x 384 (estimate 7% less; 384 rows x
-// 57344: one round of 128 x 512 and 0.63 of 128 x 256, 6% less).  Taken
-// when the estimate, with the second launch's start, is > 5% lower.
+// 57344: one round of 128 x 512, then the other 13824 rows in 216
+// workgroups of 96 x 256, 9% less).  Taken when the estimate, with the
+// second launch's start, is > 5% lower.
 int swiglu_parts(int N, int K, int m_cap, SwigluPart part[2]) {
   const GemmPlan g = gemm_plan(N, K, m_cap, 2);
   part[0] = SwigluPart{g, 0, N};
@@ -760,16 +761,22 @@ int swiglu_parts(int N, int K, int m_cap, SwigluPart part[2]) {
       const int rows_a = kTargetWorkgroups * r / n_mt * 128 * nfa;
       if (rows_a >= N) break;
       const int rows_b = N - rows_a;
-      for (int nfb = 4; nfb >= 1; --nfb) {   // wider tiles on a tie
-        if (rows_b % (32 * nfb) != 0) continue;
-        const double t = tile_rounds_us(4, nfa, 1, rows_a, K, m_cap) +
-                         tile_rounds_us(4, nfb, 1, rows_b, K, m_cap) +
-                         kSecondLaunchUs;
-        if (t < best) {
-          best = t;
-          parts = 2;
-          part[0] = SwigluPart{{4, nfa, weight_stages(nfa, K), 1}, 0, rows_a};
-          part[1] = SwigluPart{{4, nfb, weight_stages(nfb, K), 1}, rows_a, rows_b};
+      // the second launch also in 96 x 256 tiles from 256 rows (more
+      // workgroups for the leftover rows)
+      for (const int mfb : {4, 3}) {
+        for (int nfb = 4; nfb >= 1; --nfb) {   // wider tiles on a tie
+          if (rows_b % (32 * nfb) != 0) continue;
+          if (mfb == 3 && (nfb != 2 || m_cap < 256)) continue;
+          const double t = tile_rounds_us(4, nfa, 1, rows_a, K, m_cap) +
+                           tile_rounds_us(mfb, nfb, 1, rows_b, K, m_cap) +
+                           kSecondLaunchUs;
+          if (t < best) {
+            best = t;
+            parts = 2;
+            part[0] = SwigluPart{{4, nfa, weight_stages(nfa, K), 1}, 0, rows_a};
+            part[1] = SwigluPart{{mfb, nfb, mfb == 4 ? weight_stages(nfb, K) : 2, 1},
+                                 rows_a, rows_b};
+          }
         }
       }
     }
