@@ -71,13 +71,16 @@ def continuation(tgt, st, n):
 def planter(stream, depth, vocab, snap):
     """plant() for specdec.iteration: keeps a copy of the drafted tree in
     ``snap``, then rewrites the lowest-id path of the given depth (or the
-    deepest available) with the greedy continuation ``stream``."""
+    deepest available) with the greedy continuation ``stream``; a tree of
+    the root alone has no path to plant."""
     def plant(tree, rows):
         snap.append(copy.deepcopy(tree))
         if not depth:
             return
         dmax = max(nd.depth for nd in tree.nodes)
         want = min(depth, dmax)
+        if want == 0:
+            return
         leaf = min(i for i in range(1, len(tree)) if tree.nodes[i].depth == want)
         for j, nid in enumerate(tree.anc_or_self(leaf)[1:]):
             tok = stream[j]
