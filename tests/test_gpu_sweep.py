@@ -96,8 +96,8 @@ def sweep_workload_bf16(seed: int):
     """A random bf16 configuration at d 512 (grouped-query attention, four
     query heads per KV head, head_dim 128): up to 24 sequences (from 16 the
     32x32 attention kernel takes over), budgets up to 160, so that the
-    projections run every tile plan (1-, 2- and 4-fragment rows, re-tiled,
-    split gate/up) and the oracle samples up to three sequences."""
+    projections run few- and many-row tiles (1-, 2- and 4-fragment rows);
+    the oracle samples up to three sequences."""
     rng = np.random.default_rng([seed, 512])
     K = int(rng.integers(1, 9))
     M = int(rng.integers(1, 4))
