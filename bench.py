@@ -52,6 +52,18 @@ def attn_bytes(w, T_total, n_nodes, rows_block, es):
     return verify + draft
 
 
+def attn_flops(w, verify_nodes_T, draft_rows_T):
+    """Algorithmic flops of the tree-attention launches (2 per multiply-add:
+    the scores and the probability-weighted sum of the values) over the
+    committed prefix: every verified node and every drafter row attends to
+    the T entries of its sequence in every layer (the sums over nodes and
+    rows of T are the arguments); the at most M K + 1 tree keys per row are
+    left out."""
+    s = w.target
+    per = 4.0 * s.n_heads * s.head_dim
+    return per * (s.n_layers * verify_nodes_T + w.drafter_layers * draft_rows_T)
+
+
 def gemm_flops(w, verify_rows, rows_block, n_seqs):
     """Algorithmic flops (2 per multiply-add) of the projection GEMMs over
     the actual rows: verify rows through every target layer and the LM
@@ -231,6 +243,7 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
+    import numpy as np
     import torch
 
     import synth
@@ -347,13 +360,20 @@ def main():
     Tp0 = rt.T.clone()
     rows_block = []
     verify_rows = 0
+    verify_nodes_T = draft_rows_T = 0.0   # sums of the rows' prefix lengths
     rt.profile(True)
     for i in range(args.steps):
         next_iteration()
+        Ts = rt.T.cpu().numpy().astype(np.float64)
         for m in range(1, w.M + 1):
             rt.expand(m)
-            rows_block.append(int(rt.dout["n_call"][0]))
-        verify_rows += int(rt.tree["n_nodes"].sum())
+            n_call = int(rt.dout["n_call"][0])
+            rows_block.append(n_call)
+            cs = rt.dout["call_seq"][:n_call].cpu().numpy()
+            draft_rows_T += float(Ts[cs].sum())
+        nodes = rt.tree["n_nodes"].cpu().numpy()
+        verify_rows += int(nodes.sum())
+        verify_nodes_T += float((nodes * Ts).sum())
         verify_accept()
         rt.commit()
     torch.cuda.synchronize()
@@ -397,6 +417,8 @@ def main():
                         es) for i in range(args.steps))
     attn = prof["tree_attn"]
     attn_gbps = ab / (attn["ms"] * 1e-3) / 1e9
+    af = attn_flops(w, verify_nodes_T, draft_rows_T)
+    attn_tflops = af / (attn["ms"] * 1e-3) / 1e12
     log(f"gemm {gemm['launches']} launches {gemm['ms']:.2f} ms "
         f"{gemm_gbps:.0f} GB/s {gemm_tflops:.0f} TFLOP/s; tree-attn {attn['launches']} launches "
         f"{attn['ms']:.2f} ms {attn_gbps:.0f} GB/s; vocab "
@@ -449,6 +471,12 @@ def main():
         "drafter_rows_per_step": round(sum(rows_block) / args.steps, 2),
         "tree_attn_gbps": round(attn_gbps, 1),
         "tree_attn_frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
+        # the same launches against the MFMA peak (the bound where the
+        # arithmetic intensity, rows x query heads per KV head, passes the
+        # ridge: one sequence of 128 nodes, the 70B shape)
+        "tree_attn_tflops": round(attn_tflops, 1),
+        "tree_attn_mfma_frac": round(attn_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+        "tree_attn_flop_per_byte": round(af / ab, 1),
         "accepted_tokens_per_s": round(committed / dt, 3),
         "tau": round(committed / (args.steps * rt.S), 3),
         # labelled projection, not a measurement: the same iteration rate
