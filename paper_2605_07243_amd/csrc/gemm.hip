@@ -559,8 +559,9 @@ GemmPlan gemm_plan(int N, int K, int m_cap, int elem_bytes, bool retile) {
   // rows); 64 weight rows per wave above 128 rows, 128 per wave when the
   // weight tiles alone fill the chip at least as evenly (fewer activation
   // LDS reads per MFMA: +13% on the 28672- and 128256-wide projections at
-  // 1024 rows).  Four weight stages in flight only for the 32-row-per-wave
-  // shapes (measured best there, no gain with more rows per wave).
+  // 1024 rows).  Four weight stages in flight only for 128-row tiles of
+  // 32 weight rows per wave above 128 rows; at 128 rows (one sequence of
+  // 128 tree nodes) two are faster (step -1.5%).
   g.mf = m_cap <= 32 ? 1 : m_cap <= 64 ? 2 : 4;
   const int n_mt = (m_cap + 32 * g.mf - 1) / (32 * g.mf);
   g.nf = 1;
@@ -570,7 +571,7 @@ GemmPlan gemm_plan(int N, int K, int m_cap, int elem_bytes, bool retile) {
     if (N % 128 == 0 && t4 >= kTargetWorkgroups && round_fill(t4) >= round_fill(t2))
       g.nf = 4;
   }
-  g.pf = (g.mf == 4 && g.nf == 1 && (K / 64) % 4 == 0) ? 4 : 2;
+  g.pf = (g.mf == 4 && g.nf == 1 && m_cap > 128 && (K / 64) % 4 == 0) ? 4 : 2;
   const int n_nt = (N + 128 * g.nf - 1) / (128 * g.nf);
   g.ks = pick_split(n_mt * n_nt, K, g.pf);
   if (retile && g.mf == 4 && m_cap > 128) {
