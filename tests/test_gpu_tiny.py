@@ -172,7 +172,7 @@ def _iteration_case(w, st0, rt, tgt=None, dr=None):
 
 
 def test_lossless_loop(tiny):
-    """North-star (c) on the device: the committed stream of the HIP loop
+    """Losslessness on the device: the committed stream of the HIP loop
     equals the target's greedy decode."""
     w, tgt, dr, prompt, st0, rt = tiny
     ref = specdec.greedy_decode(tgt, prompt, 24)

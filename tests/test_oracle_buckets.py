@@ -9,7 +9,7 @@ class frequencies of the rank-head quality table (App. B).  Pins:
 * the tree shapes that the forced buckets imply (all b0: a chain plus one
   sibling per row; all b3 with b(b3) = 0: no drafted node at all);
 * out-of-range values clamp to 0..3;
-* greedy acceptance stays lossless under forced buckets (north-star (c));
+* greedy acceptance stays lossless under forced buckets;
 * the uniform fixed-k tree of the rank-guided-branching ablation (Sec. 4):
   all rows b1, every bucket branching k.
 """

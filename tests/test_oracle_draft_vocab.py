@@ -7,7 +7,7 @@ Pins:
   at those ids, and its top-10 tokens are the brute-force top-10 of the full
   logits restricted to the mapped ids (a transposed or inverted map fails);
 * every drafted token lies in the map's image;
-* greedy acceptance stays lossless (north-star (c));
+* greedy acceptance stays lossless;
 * the synthetic map is strictly increasing, in range and seeded.
 """
 import copy

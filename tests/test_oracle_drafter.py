@@ -5,7 +5,7 @@
 * block 1 on top of the catch-up prefix, and a block-2 expansion started
   from B_{1,1}, equal a causal run of transformers' Llama layer over the
   path's shifted inputs (brute force over the path; with K = 1 this is one
-  autoregressive drafter step, north-star check (b));
+  autoregressive drafter step);
 * invariants that follow from causal attention and the left-only shift:
   prefix consistency, causality in k, start-permutation invariance;
 * later blocks bypass W_cond and carry the cached h^(L).

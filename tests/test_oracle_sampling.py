@@ -7,7 +7,7 @@ the target probabilities within a few standard errors), including duplicate
 child tokens and nodes without children; and in the deterministic limit,
 where a one-hot target must reproduce greedy acceptance exactly, and a
 near-zero temperature speculative decode must reproduce the target's greedy
-decode (spec check (c)).
+decode (losslessness).
 """
 import numpy as np
 import pytest

@@ -4,7 +4,8 @@ r is the drafter's probability of the target's token at the rejected
 position, read from the drafter row that predicted that position.
 * When the root's position is rejected (nothing accepted), that row is the
   first row of block 1; a block's first row is one autoregressive drafter
-  step (spec check (b)), so r must equal the probability that a K = 1
+  step (the drafter forward reduces to one, see test_oracle_drafter), so r
+  must equal the probability that a K = 1
   block started at the root assigns to the bonus token.
 * r is None exactly when no drafter row continues the last accepted node
   (the commit then needs a catch-up row), and lies in [0, 1] otherwise.

@@ -1,7 +1,7 @@
 """Pins of the whole iteration: losslessness and cache bookkeeping.
 
-North-star check (c): greedy draft-then-verify is lossless, so the committed
-stream equals the target's own greedy decode, whatever the drafter proposes.
+Losslessness: greedy draft-then-verify commits exactly the target's own
+greedy decode, whatever the drafter proposes.
 Random-init drafters rarely match, so trees are also *planted*: after
 drafting, a root path is rewritten with the target's greedy continuation,
 which must then be accepted exactly (tau = planted depth + 1).

@@ -90,7 +90,7 @@ def _verify(tgt, prefix_toks, tree):
 
 
 def test_single_chain_tree_is_causal():
-    """North-star check (a): a chain tree is plain causal attention."""
+    """A tree that is a single chain is plain causal attention."""
     _, tgt = _target(SHAPE_GQA)
     rng = np.random.default_rng(7)
     toks = rng.integers(0, SHAPE_GQA.vocab, 15)
@@ -105,7 +105,7 @@ def test_single_chain_tree_is_causal():
 
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_tree_verify_equals_path_bruteforce(hf, seed):
-    """North-star check (d): each node's logits equal a causal forward of
+    """Tree verification: each node's logits equal a causal forward of
     the library model over prefix + the root-to-node path."""
     tw, tgt = _target(SHAPE_GQA, seed=seed)
     rng = np.random.default_rng(10 + seed)

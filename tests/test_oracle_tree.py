@@ -113,7 +113,7 @@ def _random_tree(rng, budget, vocab):
 @given(seed=st.integers(0, 10 ** 6), budget=st.integers(1, 40),
        vocab=st.integers(2, 6))
 def test_accept_equals_bruteforce_over_paths(seed, budget, vocab):
-    """North-star check (d): the walk returns the longest root path whose
+    """Greedy acceptance (Alg. 2): the walk returns the longest root path whose
     every token is the target's greedy choice at its parent."""
     rng = np.random.default_rng(seed)
     tree = _random_tree(rng, budget, vocab)
