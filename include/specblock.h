@@ -52,7 +52,8 @@ enum sb_status {
   SB_EBUDGET = 3,  /* tree, row, page or workspace capacity exceeded        */
   SB_EDTYPE = 4,   /* unknown storage type                                  */
   SB_EHIP = 5,     /* a HIP runtime call failed (message in sb_last_error)  */
-  SB_ESTATE = 6    /* call out of order (e.g. before sb_bind)               */
+  SB_ESTATE = 6,   /* call out of order (e.g. before sb_bind)               */
+  SB_EDEVICE = 7   /* sb_device_check: kernels clamped an out-of-range input */
 };
 
 enum sb_dtype { SB_F32 = 0, SB_BF16 = 1 };
@@ -401,6 +402,26 @@ int sb_commit(sb_ctx* ctx, sb_seqs* seqs, const sb_tree* tree,
  * the page-table capacity max_pages * 16 is assumed).  A bound below the
  * true T makes attention skip the entries beyond it. */
 int sb_set_length_bound(sb_ctx* ctx, int32_t max_T);
+
+/* Device-side range checks (a debugging aid, not part of the method).  Two
+ * kinds of caller-supplied index are read by kernels only: the entries of
+ * the KV page tables (sb_kv.page_table) and the token ids of the prompt and
+ * of sb_seqs.root.  Every such read is clamped into range (page to
+ * 0 .. n_pages - 1, token to 0 .. vocab - 1), so a bad value never reads or
+ * writes outside the pools or the embedding table; it silently computes on
+ * the clamped index instead.  sb_set_debug(ctx, 1) clears the context's
+ * device status word and makes the kernels of later calls set a bit in it
+ * for every clamp (one atomic per clamped read; nothing when inputs are in
+ * range); sb_set_debug(ctx, 0) stops reporting.  sb_device_check returns
+ * SB_OK at once if sb_set_debug has not been called since sb_bind (the
+ * word is not cleared at bind, which touches no device memory); otherwise
+ * it waits for `stream`, reads the word and, if it is not zero, clears it
+ * and returns SB_EDEVICE with sb_last_error() naming the kinds of input
+ * that were out of range (page-table entry, token id) since the last
+ * check.  The word is per context and shared by all its streams.
+ * Errors: SB_EINVAL (NULL), SB_ESTATE (not bound), SB_EHIP. */
+int sb_set_debug(sb_ctx* ctx, int32_t on);
+int sb_device_check(sb_ctx* ctx, void* stream);
 
 /* Serving-time adaptation, head-only action (Sec. 3.4; the per-query
  * adaptation procedure of App. A.3; the bandit that picks the action is the

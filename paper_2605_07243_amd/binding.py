@@ -15,7 +15,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("SPECBLOCK_LIB") or os.path.join(HERE,
                                                             "libspecblock.so")
 
-SB_OK, SB_EINVAL, SB_ESHAPE, SB_EBUDGET, SB_EDTYPE, SB_EHIP, SB_ESTATE = range(7)
+(SB_OK, SB_EINVAL, SB_ESHAPE, SB_EBUDGET, SB_EDTYPE, SB_EHIP, SB_ESTATE,
+ SB_EDEVICE) = range(8)
 SB_F32, SB_BF16 = 0, 1
 TOPK, PSI_DIM = 10, 15
 
@@ -121,7 +122,8 @@ EXPORTS = ["sb_row_capacity", "sb_workspace_bytes", "sb_create", "sb_destroy",
            "sb_profile", "sb_profile_read", "sb_profile_read_gemm",
            "sb_pack_weight",
            "sb_set_bucket_override", "sb_accept_sample", "sb_adapt_push",
-           "sb_head_update", "sb_accept_sample_noalloc"]
+           "sb_head_update", "sb_accept_sample_noalloc", "sb_set_debug",
+           "sb_device_check"]
 
 _lib = None
 
@@ -167,6 +169,10 @@ def load(path: str = LIB_PATH):
     lib.sb_commit.restype = C.c_int
     lib.sb_set_length_bound.argtypes = [vp, i32]
     lib.sb_set_length_bound.restype = C.c_int
+    lib.sb_set_debug.argtypes = [vp, i32]
+    lib.sb_set_debug.restype = C.c_int
+    lib.sb_device_check.argtypes = [vp, vp]
+    lib.sb_device_check.restype = C.c_int
     lib.sb_accept_sample.argtypes = [vp, i32, vp, vp, C.c_float, vp, vp,
                                      vp, vp]
     lib.sb_accept_sample.restype = C.c_int

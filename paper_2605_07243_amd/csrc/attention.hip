@@ -143,7 +143,7 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
   const int pg0 = t0 >> 4;
   const int n_pg = t1 > t0 ? ((t1 + 15) >> 4) - pg0 : 0;
   for (int j = tid; j < n_pg && j < MAXP; j += NT)
-    pg_sh[j] = min(max(ptab[pg0 + j], 0), kv.n_pages - 1);
+    pg_sh[j] = checked_index(ptab[pg0 + j], kv.n_pages, kv.err, kDevPage);
   __syncthreads();
 
   // page base (element offset) of half h of tile i, or -1 when empty.  The
@@ -531,7 +531,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
   const int pg0 = t0 >> 4;
   const int n_pg = t1 > t0 ? ((t1 + 15) >> 4) - pg0 : 0;
   for (int j = tid; j < n_pg && j < MAXP; j += NT)
-    pg_sh[j] = min(max(ptab[pg0 + j], 0), kv.n_pages - 1);
+    pg_sh[j] = checked_index(ptab[pg0 + j], kv.n_pages, kv.err, kDevPage);
   __syncthreads();
 
   // element offset of page pp (0..3) of tile i in its pool, or -1 (empty;

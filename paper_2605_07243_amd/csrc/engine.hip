@@ -158,6 +158,13 @@ struct sb_ctx {
   void* dseg_k = nullptr;
   void* dseg_v = nullptr;
   int* zero = nullptr;
+  // debug status word: bits of the range checks on caller-supplied indices
+  // (page-table entries, token ids), raised by the kernels while debug is
+  // set; read and cleared by sb_device_check
+  int* dev_status = nullptr;
+  bool debug = false;
+  bool status_live = false;   // cleared by sb_set_debug since the last bind
+  int* dbg() const { return debug ? dev_status : nullptr; }
   // running upper bound of every sequence's T (0: unknown)
   int T_bound = 0;
   // forced drafter-row buckets [max_seqs][row_cap] (NULL: rank-head argmax)
@@ -231,6 +238,7 @@ static size_t layout(const Dims& D, void* base, sb_ctx* c) {
   int* one = cv.take<int>(4);
   int* root_arg = cv.take<int>(4);
   int* zero = cv.take<int>(4);
+  int* dev_status = cv.take<int>(4);
   int* blk_row0 = cv.take<int>(D.S * 4);
   int* blk_nst = cv.take<int>(D.S * 4);
   int* prof_rows = cv.take<int>((size_t)kProfSlots * 4);
@@ -288,6 +296,7 @@ static size_t layout(const Dims& D, void* base, sb_ctx* c) {
     c->one = one;
     c->root_arg = root_arg;
     c->zero = zero;
+    c->dev_status = dev_status;
     c->blk_row0 = blk_row0;
     c->blk_nst = blk_nst;
     c->prof_rows = prof_rows;
@@ -550,6 +559,8 @@ int sb_bind(sb_ctx* c, const sb_target_weights* tw,
   c->dl.assign(dw->layers, dw->layers + c->D.LD);
   c->dw.layers = c->dl.data();
   layout(c->D, ws, c);
+  c->status_live = false;
+  c->debug = false;
   c->vq_ready = false;
   c->bound = true;
   return SB_OK;
@@ -720,6 +731,7 @@ void layer_body(sb_ctx* c, const sb_layer_weights& lw, int layer,
   kv.page_table = pf.kv->page_table;
   kv.max_pages = c->cfg.max_pages;
   kv.n_pages = pf.kv->n_pages;
+  kv.err = c->dbg();
   kv.seg_k = segk;
   kv.seg_v = segv;
   kv.seg_pages = pf.seg_pages;
@@ -893,7 +905,8 @@ int lm_head_reduce(sb_ctx* c, const void* W, int V, float* logits_out,
 
 TreeDims tree_dims(const sb_ctx* c, int n_seqs) {
   const Dims& D = c->D;
-  return TreeDims{n_seqs, D.K, D.M, D.B_max, D.budget, D.bw, D.row_cap, D.rw, D.d};
+  return TreeDims{n_seqs, D.K,  D.M,  D.B_max, D.budget, D.bw,
+                  D.row_cap, D.rw, D.d, D.V, c->dbg()};
 }
 
 template <typename T>
@@ -964,9 +977,9 @@ int commit_impl(sb_ctx* c, sb_seqs* sq, const sb_tree* t,
   launch_commit_plan(td, *t, *acc, sq->T, c->ci, c->fb, c->taps_idx, c->n_aux,
                      st);
   const KVPools tp{tkv->k, tkv->v, tkv->page_table, c->cfg.max_pages,
-                   tkv->n_pages, c->tseg_k, c->tseg_v, D.tpages};
+                   tkv->n_pages, c->tseg_k, c->tseg_v, D.tpages, c->dbg()};
   const KVPools dp{dkv->k, dkv->v, dkv->page_table, c->cfg.max_pages,
-                   dkv->n_pages, c->dseg_k, c->dseg_v, D.dpages};
+                   dkv->n_pages, c->dseg_k, c->dseg_v, D.dpages, c->dbg()};
   launch_commit_copy<T>(td, *t, *acc, c->ci, false, tp, D.S, D.L, D.Hkv, D.hd,
                         st);
   launch_commit_copy<T>(td, *t, *acc, c->ci, true, dp, D.S, D.LD, D.Hkv, D.hd,
@@ -994,9 +1007,9 @@ int prefill_impl(sb_ctx* c, const sb_seqs* sq, const int32_t* prompt, int ld,
   launch_set_int(c->one, 1, st);
   launch_set_int(c->zero, 0, st);
   const KVPools tp{tkv->k, tkv->v, tkv->page_table, c->cfg.max_pages,
-                   tkv->n_pages, c->tseg_k, c->tseg_v, D.tpages};
+                   tkv->n_pages, c->tseg_k, c->tseg_v, D.tpages, c->dbg()};
   const KVPools dp{dkv->k, dkv->v, dkv->page_table, c->cfg.max_pages,
-                   dkv->n_pages, c->dseg_k, c->dseg_v, D.dpages};
+                   dkv->n_pages, c->dseg_k, c->dseg_v, D.dpages, c->dbg()};
   const Prefix tpf{tkv, c->tseg_k, c->tseg_v, D.tpages};
   const Prefix dpf{dkv, c->dseg_k, c->dseg_v, D.dpages};
   const size_t tap_row = (size_t)3 * D.d;
@@ -1007,7 +1020,7 @@ int prefill_impl(sb_ctx* c, const sb_seqs* sq, const int32_t* prompt, int ld,
     const int len = lens[s];
     for (int a = 0; a < len; a += D.chunk) {
       const int n = std::min(D.chunk, len - a);
-      launch_plan_prefill_target(S, s, a, n, prompt, ld, p, st);
+      launch_plan_prefill_target(S, s, a, n, prompt, ld, p, D.V, c->dbg(), st);
       target_forward<T>(c, p, tpf, D.chunk, c->taps_pf, st);
       launch_seg_to_cache<T>(p, tp, S, D.L, D.Hkv, D.hd, st);
       if (a + n == len) {
@@ -1018,7 +1031,8 @@ int prefill_impl(sb_ctx* c, const sb_seqs* sq, const int32_t* prompt, int ld,
         launch_verify_finalize(c->vpart, n_chunks, c->one, 1, c->zero,
                                c->root_arg, st);
       }
-      launch_plan_prefill_draft(S, s, a, n, prompt, ld, p, c->n_aux, st);
+      launch_plan_prefill_draft(S, s, a, n, prompt, ld, p, c->n_aux, D.V,
+                                c->dbg(), st);
       cond_rows<T>(c, c->taps_pf, nullptr, c->n_aux, D.chunk, st);
       drafter_forward<T>(c, p, c->cond_buf, dpf, D.chunk, false, st);
       launch_seg_to_cache<T>(p, dp, S, D.LD, D.Hkv, D.hd, st);
@@ -1387,6 +1401,35 @@ int sb_set_length_bound(sb_ctx* c, int32_t max_T) {
   if (max_T < 0) return fail(c, SB_EINVAL, "max_T must be >= 0");
   c->T_bound = max_T;
   return SB_OK;
+}
+
+int sb_set_debug(sb_ctx* c, int32_t on) {
+  if (!c) return SB_EINVAL;
+  if (!c->bound) return fail(c, SB_ESTATE, "context not bound (call sb_bind)");
+  if (hipMemset(c->dev_status, 0, sizeof(int)) != hipSuccess)
+    return fail(c, SB_EHIP, "clearing the debug status word failed");
+  c->status_live = true;
+  c->debug = on != 0;
+  return SB_OK;
+}
+
+int sb_device_check(sb_ctx* c, void* stream) {
+  if (!c) return SB_EINVAL;
+  if (!c->bound) return fail(c, SB_ESTATE, "context not bound (call sb_bind)");
+  if (!c->status_live) return SB_OK;   // no kernel has had the word
+  int word = 0;
+  if (hipStreamSynchronize(S_(stream)) != hipSuccess ||
+      hipMemcpy(&word, c->dev_status, sizeof(int), hipMemcpyDeviceToHost) !=
+          hipSuccess)
+    return fail(c, SB_EHIP, "reading the debug status word failed");
+  if (word == 0) return SB_OK;
+  if (hipMemset(c->dev_status, 0, sizeof(int)) != hipSuccess)
+    return fail(c, SB_EHIP, "clearing the debug status word failed");
+  std::string msg = "out-of-range input clamped on the device:";
+  if (word & kDevPage) msg += " page-table entry outside [0, n_pages)";
+  if ((word & kDevPage) && (word & kDevToken)) msg += ";";
+  if (word & kDevToken) msg += " token id outside [0, vocab)";
+  return fail(c, SB_EDEVICE, msg);
 }
 
 int sb_set_bucket_override(sb_ctx* c, const int32_t* buckets) {

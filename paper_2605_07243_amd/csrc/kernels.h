@@ -45,6 +45,7 @@ struct KVView {
   const void* seg_k;        // layer base of the segment pool [S][seg_pages]
   const void* seg_v;
   int seg_pages;            // pages per sequence in the segment pool
+  int* err = nullptr;       // debug status word (out-of-range pages), or null
 };
 
 // Projection GEMM plan.  bf16: 32-row activation tiles per workgroup (mf),
@@ -191,12 +192,18 @@ void launch_verify_finalize(const float* part, int n_chunks, const int* n,
                             hipStream_t st);
 
 // Tree kernels.
+// Debug status bits (sb_device_check): a caller-supplied page-table entry
+// or token id was outside its range and was clamped into it.
+constexpr int kDevPage = 1, kDevToken = 2;
+
 struct TreeDims {
   int S, K, M, B_max, budget;
   int bw;        // ancestor words per node
   int row_cap;   // drafter rows per sequence per iteration
   int rw;        // visibility words per drafter row
   int d;
+  int V;         // target vocabulary (caller-supplied tokens are clamped to it)
+  int* err;      // debug status word, or null
 };
 struct CommitInfo {
   int* T_old;
@@ -215,6 +222,7 @@ struct KVPools {
   void* seg_k;
   void* seg_v;
   int seg_pages;
+  int* err;      // debug status word (out-of-range pages), or null
 };
 void launch_block1_reset(const TreeDims& td, const sb_tree& t, const int* root,
                          int* n_aux, hipStream_t st);
@@ -286,11 +294,14 @@ void launch_seg_to_cache(const CallPlan& p, const KVPools& kv, int S,
 void launch_commit_state(const TreeDims& td, const sb_seqs& sq,
                          const sb_accept_out& acc, const CommitInfo& ci,
                          const float* taps, hipStream_t st);
+// Prompt tokens outside 0 .. V - 1 are clamped into it (and recorded in the
+// debug status word err when it is not null).
 void launch_plan_prefill_target(int S, int s, int a, int n, const int* prompt,
-                                int ld, const CallPlan& p, hipStream_t st);
+                                int ld, const CallPlan& p, int V, int* err,
+                                hipStream_t st);
 void launch_plan_prefill_draft(int S, int s, int a, int n, const int* prompt,
-                               int ld, const CallPlan& p, int* n_aux,
-                               hipStream_t st);
+                               int ld, const CallPlan& p, int* n_aux, int V,
+                               int* err, hipStream_t st);
 void launch_prefill_finish(const sb_seqs& sq, int s, int len, int d,
                            const float* taps_pf, int n_last,
                            const int* root_arg, hipStream_t st);

@@ -19,7 +19,7 @@ __global__ void block1_reset_kernel(TreeDims td, sb_tree t,
   for (int s = threadIdx.x; s < td.S; s += blockDim.x) {
     const size_t b = (size_t)s * td.budget;
     t.n_nodes[s] = 1;
-    t.token[b] = root[s];
+    t.token[b] = checked_index(root[s], td.V, td.err, kDevToken);
     t.parent[b] = -1;
     t.depth[b] = 0;
     t.row[b] = -1;
@@ -441,10 +441,11 @@ __global__ void commit_copy_kernel(TreeDims td, sb_tree t, sb_accept_out acc,
       return;
     }
   }
+  // entries outside the page table (a negative T included) are not written
+  if (dst < 0 || (dst >> 4) >= kv.max_pages) return;
   const int page_i = dst >> 4;
-  if (page_i >= kv.max_pages) return;
-  const int page = min(max(kv.page_table[(size_t)s * kv.max_pages + page_i], 0),
-                       kv.n_pages - 1);
+  const int page = checked_index(kv.page_table[(size_t)s * kv.max_pages + page_i],
+                                 kv.n_pages, kv.err, kDevPage);
   const int sl = dst & 15;
   const int sp = src_slot >> 4, ss = src_slot & 15;
   if (sp >= kv.seg_pages) return;
@@ -473,8 +474,8 @@ __global__ void seg_to_cache_kernel(CallPlan p, KVPools kv, int S, int Hkv,
   const int s = p.seq[i], slot = p.slot[i];
   const int page_i = dst >> 4;
   if (page_i >= kv.max_pages) return;
-  const int page = min(max(kv.page_table[(size_t)s * kv.max_pages + page_i], 0),
-                       kv.n_pages - 1);
+  const int page = checked_index(kv.page_table[(size_t)s * kv.max_pages + page_i],
+                                 kv.n_pages, kv.err, kDevPage);
   const int sl = dst & 15;
   const int sp = slot >> 4, ss = slot & 15;
   if (sp >= kv.seg_pages) return;
@@ -511,7 +512,8 @@ __global__ void commit_state_kernel(TreeDims td, sb_seqs sq, sb_accept_out acc,
 // Prefill of sequence s, chunk [a, a + n): target rows (causal chain).
 __global__ void plan_prefill_target_kernel(int S, int s, int a, int n,
                                            const int* __restrict__ prompt,
-                                           int ld, CallPlan p) {
+                                           int ld, CallPlan p, int V,
+                                           int* __restrict__ err) {
   if (threadIdx.x == 0) {
     for (int q = 0; q <= S; ++q) p.seq_off[q] = q <= s ? 0 : n;
     for (int q = 0; q < S; ++q) {
@@ -524,7 +526,7 @@ __global__ void plan_prefill_target_kernel(int S, int s, int a, int n,
     p.seq[j] = s;
     p.slot[j] = j;
     p.pos[j] = a + j;
-    p.token[j] = prompt[(size_t)s * ld + a + j];
+    p.token[j] = checked_index(prompt[(size_t)s * ld + a + j], V, err, kDevToken);
     p.k[j] = 1;
     p.pred[j] = j;
     p.cond[j] = -1;
@@ -544,7 +546,8 @@ __global__ void plan_prefill_target_kernel(int S, int s, int a, int n,
 __global__ void plan_prefill_draft_kernel(int S, int s, int a, int n,
                                           const int* __restrict__ prompt,
                                           int ld, CallPlan p,
-                                          int* __restrict__ n_aux) {
+                                          int* __restrict__ n_aux, int V,
+                                          int* __restrict__ err) {
   if (threadIdx.x == 0) {
     for (int q = 0; q <= S; ++q) p.seq_off[q] = q <= s ? 0 : n;
     for (int q = 0; q < S; ++q) {
@@ -558,7 +561,7 @@ __global__ void plan_prefill_draft_kernel(int S, int s, int a, int n,
     p.seq[r] = s;
     p.slot[r] = r;
     p.pos[r] = a + 1 + r;
-    p.token[r] = prompt[(size_t)s * ld + a + r];
+    p.token[r] = checked_index(prompt[(size_t)s * ld + a + r], V, err, kDevToken);
     p.k[r] = 1;
     p.pred[r] = r;
     p.cond[r] = (a + r >= 1) ? r : -1;
@@ -804,13 +807,16 @@ void launch_commit_state(const TreeDims& td, const sb_seqs& sq,
   commit_state_kernel<<<td.S, 1024, 0, st>>>(td, sq, acc, ci, taps);
 }
 void launch_plan_prefill_target(int S, int s, int a, int n, const int* prompt,
-                                int ld, const CallPlan& p, hipStream_t st) {
-  plan_prefill_target_kernel<<<1, 256, 0, st>>>(S, s, a, n, prompt, ld, p);
+                                int ld, const CallPlan& p, int V, int* err,
+                                hipStream_t st) {
+  plan_prefill_target_kernel<<<1, 256, 0, st>>>(S, s, a, n, prompt, ld, p, V,
+                                                err);
 }
 void launch_plan_prefill_draft(int S, int s, int a, int n, const int* prompt,
-                               int ld, const CallPlan& p, int* n_aux,
-                               hipStream_t st) {
-  plan_prefill_draft_kernel<<<1, 256, 0, st>>>(S, s, a, n, prompt, ld, p, n_aux);
+                               int ld, const CallPlan& p, int* n_aux, int V,
+                               int* err, hipStream_t st) {
+  plan_prefill_draft_kernel<<<1, 256, 0, st>>>(S, s, a, n, prompt, ld, p,
+                                               n_aux, V, err);
 }
 void launch_prefill_finish(const sb_seqs& sq, int s, int len, int d,
                            const float* taps_pf, int n_last,

@@ -349,6 +349,16 @@ class Runtime:
         T or the caches directly."""
         self._check(self.lib.sb_set_length_bound(self.ctx, int(max_T)))
 
+    def set_debug(self, on: bool):
+        """Start (clearing the status word) or stop the device-side reports
+        of clamped page-table entries and token ids."""
+        self._check(self.lib.sb_set_debug(self.ctx, int(bool(on))))
+
+    def device_check(self):
+        """Raises SBError (SB_EDEVICE) if a kernel clamped an out-of-range
+        page-table entry or token id since the last check."""
+        self._check(self.lib.sb_device_check(self.ctx, self.stream))
+
     # ---- head-only adaptation ----------------------------------------
     def adapt_buffer(self):
         """Device buffer for sb_adapt_push / sb_head_update."""

@@ -145,6 +145,11 @@ def test_calls_before_bind_are_refused(lib):
     assert lib.sb_create(C.byref(c), C.byref(ctx)) == B.SB_OK
     t = B.Tree()
     assert lib.sb_accept(ctx, 1, C.byref(t), None, None, None) == B.SB_ESTATE
+    # the debug status word lives in the workspace
+    assert lib.sb_set_debug(ctx, 1) == B.SB_ESTATE
+    assert lib.sb_device_check(ctx, None) == B.SB_ESTATE
+    assert lib.sb_set_debug(None, 1) == B.SB_EINVAL
+    assert lib.sb_device_check(None, None) == B.SB_EINVAL
     lib.sb_destroy(ctx)
 
 
