@@ -16,6 +16,7 @@
 // stored transposed ([hd][16 slots]) so the V^T operand is two 8/16-byte
 // loads.  Splits are combined with log-sum-exp weights.
 #include <hip/hip_ext.h>
+#include "bounds.h"
 #include "common.h"
 #include "kernels.h"
 

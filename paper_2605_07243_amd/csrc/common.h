@@ -159,16 +159,6 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return t;
 }
 
-// v clamped into 0 .. n - 1; when it was outside and err (the debug status
-// word) is not null, bit (kDevPage / kDevToken) is set in it
-__device__ __forceinline__ int checked_index(int v, int n, int* err, int bit) {
-  if (v < 0 || v >= n) {
-    if (err != nullptr) atomicOr(err, bit);
-    v = min(max(v, 0), n - 1);
-  }
-  return v;
-}
-
 // Logical workgroup id for a launch of `total` workgroups whose neighbours
 // should share an XCD's L2.  The dispatcher deals workgroups out round-robin
 // over the 8 XCDs (id b to XCD b % 8); with total = 8 q + r, XCD x holds

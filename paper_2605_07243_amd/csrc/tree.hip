@@ -4,6 +4,7 @@
 // one-wave-per-sequence kernels; nothing here synchronises with the host.
 #include <float.h>
 
+#include "bounds.h"
 #include "common.h"
 #include "kernels.h"
 #include "specblock.h"
