@@ -168,24 +168,48 @@ __device__ __forceinline__ void sum_parts2(const float* __restrict__ P,
 // t, t + 1024 (d <= 8192), summed over the partials in one pass.
 // add_rows != nullptr adds row add_rows[add_idx[i] - 1] (fp32 [.][d]) to
 // the partial sum.
-template <typename T>
+// Row grids up to this size issue their loads before the live row count
+// arrives (the EARLY forms of residual_kernel and qkv_post_kernel).
+constexpr int kEarlyRows = 128;
+
+template <typename T, bool EARLY>
 __global__ __launch_bounds__(1024) void residual_kernel(
     float* __restrict__ x, const float* __restrict__ P, int ks,
-    size_t part_stride, const int* __restrict__ n, int d, int accumulate,
+    size_t part_stride, const int* n, int d, int accumulate,
     const float* __restrict__ g, float eps, T* __restrict__ out, int ldo,
     float* __restrict__ taps, int tap_mask, const int* __restrict__ out_row,
     const float* __restrict__ add_rows, const int* __restrict__ add_idx) {
   constexpr int MAXV = 2;
   __shared__ float red[16];
   const int i = blockIdx.x;
-  if (i >= *n) return;
+  // EARLY (small grids: few rows, bound by latency): the live row count is
+  // waited for only at the exit test further down.  The partial sums, the
+  // residual and the gains of row i < grid size are in their buffers
+  // whether or not the row is live, so their loads go out together with
+  // the count's (one round trip after the kernel boundary instead of two).
+  // The count is read with a vector load (the empty asm before it rules out
+  // a scalar one, whose wait would also be taken for the kernel arguments
+  // read next), older than the partial loads, so the waits for those cover
+  // it; the second empty asm keeps the loads, and the test, in their
+  // places.  Otherwise (a large grid has many rows past the live count,
+  // which then exit before loading anything) the count is tested first.
+  int nrows = 0;
+  if constexpr (EARLY) {
+    __asm__ volatile("" ::: "memory");
+    nrows = *n;
+  } else {
+    if (i >= *n) return;
+  }
   float* xr = x + (size_t)i * d;
-  const float4* ar = add_rows != nullptr
-      ? reinterpret_cast<const float4*>(add_rows + (size_t)(add_idx[i] - 1) * d)
-      : nullptr;
+  const float4* ar = nullptr;
   float* tr = nullptr;
-  if (taps != nullptr && tap_mask != 0 && out_row[i] >= 0)
-    tr = taps + (size_t)out_row[i] * 3 * d;
+  auto row_extras = [&] {
+    if (add_rows != nullptr)
+      ar = reinterpret_cast<const float4*>(add_rows + (size_t)(add_idx[i] - 1) * d);
+    if (taps != nullptr && tap_mask != 0 && out_row[i] >= 0)
+      tr = taps + (size_t)out_row[i] * 3 * d;
+  };
+  if constexpr (!EARLY) row_extras();
   const int nv = d >> 2;
   float4 v[MAXV];
   float ss = 0.f;
@@ -207,13 +231,28 @@ __global__ __launch_bounds__(1024) void residual_kernel(
                ? sum_parts(P, part_stride, ks, (size_t)i * d + 4 * threadIdx.x)
                : make_float4(0.f, 0.f, 0.f, 0.f);
   }
+  float4 xv[MAXV];
+  if constexpr (EARLY) {
+#pragma unroll
+    for (int q = 0; q < MAXV; ++q) {
+      const int c = threadIdx.x + q * 1024;
+      xv[q] = (accumulate && c < nv) ? reinterpret_cast<const float4*>(xr)[c]
+                                     : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    // (the count passes through the asm so that its test, and the wait for
+    // it, stay here)
+    __asm__ volatile("" : "+v"(nrows)::"memory");
+    if (i >= nrows) return;
+    row_extras();
+  }
 #pragma unroll
   for (int q = 0; q < MAXV; ++q) {
     const int c = threadIdx.x + q * 1024;
     if (c < nv) {
       float4 a = v[q];
       if (ar != nullptr) a = add4(a, ar[c]);
-      if (accumulate) a = add4(a, reinterpret_cast<const float4*>(xr)[c]);
+      if (accumulate)
+        a = add4(a, EARLY ? xv[q] : reinterpret_cast<const float4*>(xr)[c]);
       reinterpret_cast<float4*>(xr)[c] = a;
       if (tr) {
         if (tap_mask & 1) reinterpret_cast<float4*>(tr)[c] = a;
@@ -245,10 +284,11 @@ void launch_residual(float* x, const float* P, int ks, size_t part_stride,
                      const float* g, float eps, T* out, int ldo, float* taps,
                      int tap_mask, const int* out_row, hipStream_t st,
                      const float* add_rows, const int* add_idx) {
-  residual_kernel<T><<<cap, 1024, 0, st>>>(x, P, ks, part_stride, n, d,
-                                           accumulate ? 1 : 0, g, eps, out, ldo,
-                                           taps, tap_mask, out_row, add_rows,
-                                           add_idx);
+  auto k = cap <= kEarlyRows ? residual_kernel<T, true>
+                             : residual_kernel<T, false>;
+  k<<<cap, 1024, 0, st>>>(x, P, ks, part_stride, n, d, accumulate ? 1 : 0, g,
+                          eps, out, ldo, taps, tap_mask, out_row, add_rows,
+                          add_idx);
 }
 
 // RoPE (rotate-half pairs (j, j + hd/2), angle pos * theta^(-2j/hd)) on the
@@ -256,7 +296,7 @@ void launch_residual(float* x, const float* P, int ks, size_t part_stride,
 // the row's slot of its sequence's segment pages.  Grid (rows, item blocks):
 // an item is four rotation pairs of one Q/K head, or four V columns; one
 // item per thread, its partials summed in one pass.
-template <typename T>
+template <typename T, bool EARLY>
 __global__ __launch_bounds__(256) void qkv_post_kernel(
     const float* __restrict__ P, int ks, size_t part_stride, CallPlan p, int H,
     int Hkv, int hd, float theta, T* __restrict__ q, T* __restrict__ seg_k,
@@ -264,7 +304,16 @@ __global__ __launch_bounds__(256) void qkv_post_kernel(
   __shared__ __attribute__((aligned(16))) float cs[128];
   __shared__ __attribute__((aligned(16))) float sn[128];
   const int i = blockIdx.x;
-  if (i >= *p.n) return;
+  // EARLY: the live row count is waited for only after this thread's
+  // partial loads are issued (rows below the grid size are in the partial
+  // slabs whether or not they are live), as in residual_kernel
+  int nrows = 0;
+  if constexpr (EARLY) {
+    __asm__ volatile("" ::: "memory");
+    nrows = *p.n;
+  } else {
+    if (i >= *p.n) return;
+  }
   const int half = hd >> 1;
   const int q4 = half >> 2;
   const int n_rot = (H + Hkv) * q4;
@@ -272,10 +321,6 @@ __global__ __launch_bounds__(256) void qkv_post_kernel(
   const int idx = blockIdx.y * blockDim.x + threadIdx.x;
   const int ncol = (H + 2 * Hkv) * hd;
   const size_t row = (size_t)i * ncol;
-  const int seq = p.seq[i], slot = p.slot[i];
-  const int page = slot >> 4, sl = slot & 15;
-  const size_t page_base = (size_t)seq * seg_pages + page;
-  // issue this thread's partial loads before the angle table is built
   float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
   int head = 0, j = 0;
   if (idx < n_rot) {
@@ -289,6 +334,13 @@ __global__ __launch_bounds__(256) void qkv_post_kernel(
     j = (v % (hd >> 2)) * 4;
     a = sum_parts(P, part_stride, ks, row + (H + Hkv) * hd + head * hd + j);
   }
+  if constexpr (EARLY) {
+    __asm__ volatile("" : "+v"(nrows)::"memory");
+    if (i >= nrows) return;
+  }
+  const int seq = p.seq[i], slot = p.slot[i];
+  const int page = slot >> 4, sl = slot & 15;
+  const size_t page_base = (size_t)seq * seg_pages + page;
   const double pos = (double)p.pos[i];
   for (int t = threadIdx.x; t < half; t += blockDim.x) {
     // angle in double, reduced to [-pi, pi] before the fp32 sincos
@@ -328,7 +380,9 @@ void launch_qkv_post(const float* P, int ks, size_t part_stride,
                      T* q, void* seg_k, void* seg_v, int seg_pages,
                      hipStream_t st) {
   const int items = (H + Hkv) * (hd / 8) + Hkv * (hd / 4);
-  qkv_post_kernel<T><<<dim3(p.cap, (items + 255) / 256), 256, 0, st>>>(
+  auto k = p.cap <= kEarlyRows ? qkv_post_kernel<T, true>
+                               : qkv_post_kernel<T, false>;
+  k<<<dim3(p.cap, (items + 255) / 256), 256, 0, st>>>(
       P, ks, part_stride, p, H, Hkv, hd, theta, q, (T*)seg_k, (T*)seg_v,
       seg_pages);
 }

@@ -105,10 +105,10 @@ __device__ __forceinline__ void vr_stats_merge(float& m, float& s, float& u,
 // n_nt column tiles from there.
 template <int MF, int NF, int PF, bool SWIGLU, int VR>
 __global__ __launch_bounds__(256) void gemm_tile_kernel(
-    const bf16_t* __restrict__ X, int ldx, const bf16_t* __restrict__ W,
-    int K, float* __restrict__ P, int N, size_t part_stride,
-    const int* __restrict__ m_count, int k_chunk, int n_mt, int n_nt,
-    bf16_t* __restrict__ act, int F, float* __restrict__ rec, int n_first) {
+    const bf16_t* X, int ldx, const bf16_t* W, int K, float* __restrict__ P,
+    int N, size_t part_stride, const int* __restrict__ m_count, int k_chunk,
+    int n_mt, int n_nt, bf16_t* __restrict__ act, int F,
+    float* __restrict__ rec, int n_first, int x_rows) {
   static_assert(PF == 2 || PF == 4, "weight ring depth");
   constexpr int BM = 32 * MF;
   constexpr int LD = 64 + 8;
@@ -120,9 +120,9 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(
   const int rest = b / n_mt;
   const int nt = rest % n_nt;
   const int kc = rest / n_nt;
-  const int M = *m_count;
   const int m_base = mt * BM;
-  if (m_base >= M) return;  // whole workgroup
+  // live rows (a scalar load; it is waited for only at the exit test below)
+  const int M = *m_count;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int lr = lane & 31, h = lane >> 5;
   const int nb = n_first + nt * (128 * NF) + wave * (32 * NF);  // first row
@@ -135,16 +135,6 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(
   for (int f = 0; f < NF; ++f) {
     const int rb = min((nb >> 5) + f, N / 32 - 1);
     wp[f] = W + (size_t)(kc0 / 64) * kstride + (size_t)rb * 2048 + lane * 8;
-  }
-  // activation chunks of this thread: c = tid + 256 q is row c / 8,
-  // 16-byte column chunk c % 8 of the stage; rows >= M repeat row M - 1
-  // (their outputs are not stored)
-  const bf16_t* xp[MF];
-#pragma unroll
-  for (int q = 0; q < MF; ++q) {
-    const int c = tid + 256 * q;
-    const int row = min(m_base + c / 8, M - 1);
-    xp[q] = X + (size_t)row * ldx + kc0 + 8 * (c % 8);
   }
   u32x4_t wq[PF][NF][4];
   u32x4_t xq[2][MF];
@@ -220,6 +210,32 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(
     SB_ISSUE_WI(p, s + PF, 3)                                                 \
     __syncthreads();                                                          \
   }
+  // A launch with one activation row tile (a few rows: the projections of
+  // one or a few sequences) streams weights for a short time and pays for
+  // every round trip at its start, so there the first stages' loads, which
+  // do not depend on the live row count, go out together with the count's
+  // load instead of after it: activation rows are read up to the call's
+  // row capacity x_rows (rows past it repeat the last one; rows at or past
+  // the live count may hold anything, and their outputs are not stored),
+  // and a workgroup with no live rows exits with the loads outstanding
+  // (the end of the program waits for them).  The empty asm with a memory
+  // clobber keeps the compiler from sinking the loads below the exit test,
+  // past which alone their results are used (W and X are not __restrict__
+  // for the same reason).  With several row tiles (many rows, long
+  // MFMA-bound launches) the count is waited for first and the rows past
+  // it repeat row M - 1, as issuing early measured slower there.
+  const bool early = n_mt == 1;
+  if (!early && m_base >= M) return;  // whole workgroup
+  const int row_lim = early ? x_rows : M;
+  const bf16_t* xp[MF];
+#pragma unroll
+  for (int q = 0; q < MF; ++q) {
+    const int c = tid + 256 * q;
+    const int row = min(m_base + c / 8, row_lim - 1);
+    xp[q] = X + (size_t)row * ldx + kc0 + 8 * (c % 8);
+  }
+  // (each stage's activations before its weights: the loop's wait counts
+  // assume that order of the outstanding loads)
   SB_ISSUE_X(0, 0)
   SB_ISSUE_W(0, 0)
   SB_ISSUE_X(1, 1)
@@ -228,6 +244,8 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(
     SB_ISSUE_W(2, 2)
     SB_ISSUE_W(3, 3)
   }
+  __asm__ volatile("" ::: "memory");
+  if (m_base >= M) return;  // one row tile and no live rows
   SB_STORE_X(0, 0)
   __syncthreads();
   for (int s0 = 0; s0 < nstage; s0 += PF) {
@@ -652,7 +670,7 @@ void launch_tile(const GemmPlan& g, const bf16_t* X, int ldx, const bf16_t* W,
     hipExtLaunchKernelGGL(gemm_tile_kernel<MF_, NF_, PF_, SWIGLU, VR>, grid,  \
                           dim3(256), 0, st, ea, eb, 0, X, ldx, W, K, P, N,    \
                           part_stride, m_count, k_chunk, n_mt, n_nt, act, F,  \
-                          rec, n_first);                                      \
+                          rec, n_first, m_cap);                               \
     return;                                                                   \
   }
   SB_LAUNCH(1, 1, 2)
