@@ -242,7 +242,10 @@ __global__ __launch_bounds__(1024) void residual_kernel(
     // (the count passes through the asm so that its test, and the wait for
     // it, stay here)
     __asm__ volatile("" : "+v"(nrows)::"memory");
-    if (i >= nrows) return;
+    if (i >= nrows) {   // no load in flight past the end of the program
+      __builtin_amdgcn_s_waitcnt(0);
+      return;
+    }
     row_extras();
   }
 #pragma unroll
@@ -336,7 +339,10 @@ __global__ __launch_bounds__(256) void qkv_post_kernel(
   }
   if constexpr (EARLY) {
     __asm__ volatile("" : "+v"(nrows)::"memory");
-    if (i >= nrows) return;
+    if (i >= nrows) {
+      __builtin_amdgcn_s_waitcnt(0);
+      return;
+    }
   }
   const int seq = p.seq[i], slot = p.slot[i];
   const int page = slot >> 4, sl = slot & 15;

@@ -217,11 +217,11 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(
   // load instead of after it: activation rows are read up to the call's
   // row capacity x_rows (rows past it repeat the last one; rows at or past
   // the live count may hold anything, and their outputs are not stored),
-  // and a workgroup with no live rows exits with the loads outstanding
-  // (the end of the program waits for them).  The empty asm with a memory
-  // clobber keeps the compiler from sinking the loads below the exit test,
-  // past which alone their results are used (W and X are not __restrict__
-  // for the same reason).  With several row tiles (many rows, long
+  // and a workgroup with no live rows waits for them before it exits (no
+  // load in flight past the end of the program).  The empty asm with a
+  // memory clobber keeps the compiler from sinking the loads below the exit
+  // test, past which alone their results are used (W and X are not
+  // __restrict__ for the same reason).  With several row tiles (many rows, long
   // MFMA-bound launches) the count is waited for first and the rows past
   // it repeat row M - 1, as issuing early measured slower there.
   const bool early = n_mt == 1;
@@ -245,7 +245,10 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(
     SB_ISSUE_W(3, 3)
   }
   __asm__ volatile("" ::: "memory");
-  if (m_base >= M) return;  // one row tile and no live rows
+  if (m_base >= M) {  // one row tile and no live rows
+    __builtin_amdgcn_s_waitcnt(0);
+    return;
+  }
   SB_STORE_X(0, 0)
   __syncthreads();
   for (int s0 = 0; s0 < nstage; s0 += PF) {
