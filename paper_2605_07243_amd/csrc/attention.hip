@@ -131,8 +131,15 @@ __global__ __launch_bounds__(NQ * 64) void tree_attn_kernel(
   // committed keys: the prefix, within the page table and the length bound
   // (a bound below a prefix skips the entries past it)
   const int Tp = min(min(p.prefix_len[s], kv.max_pages * 16), key_cap);
-  const int t0 = bz * split_tokens;
-  const int t1 = min(Tp, t0 + split_tokens);
+  // the splits run over this sequence's own prefix: equal runs of whole
+  // 32-key tiles (the host's split_tokens comes from a length bound that
+  // can run well ahead of the prefix, which would leave the last splits
+  // empty and the first ones longer); never longer than split_tokens, which
+  // keeps a split within the page-table stage
+  const int sp_tok =
+      min(split_tokens, ((Tp + (int)gridDim.z - 1) / (int)gridDim.z + 31) & ~31);
+  const int t0 = bz * sp_tok;
+  const int t1 = min(Tp, t0 + sp_tok);
   const bool last_split = bz == gridDim.z - 1;
   const int L = last_split ? min(p.seg_len[s], kv.seg_pages * 16) : 0;
   const int n_pre = t1 > t0 ? (t1 - t0 + 31) / 32 : 0;
@@ -485,7 +492,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
     qg = bx;
     zs = bz;
     nzs = gridDim.z;
-    split_tok = split_tokens;
+    split_tok = -1;   // set from the prefix below
   }
   const int G = H / Hkv;
   const int row0 = p.seq_off[s];
@@ -523,6 +530,10 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
   // committed keys: the prefix, within the page table and the length bound
   // (a bound below a prefix skips the entries past it)
   const int Tp = min(min(p.prefix_len[s], kv.max_pages * 16), key_cap);
+  // fixed splits run over this sequence's own prefix (equal runs of whole
+  // 64-key tiles, never longer than split_tokens), as in tree_attn_kernel
+  if (split_tok < 0)
+    split_tok = min(split_tokens, ((Tp + nzs - 1) / nzs + 63) & ~63);
   const int t0 = zs * split_tok;
   const int t1 = min(Tp, t0 + split_tok);
   const bool last_split = zs == nzs - 1;
