@@ -13,7 +13,8 @@ fp32 model (two sequences, weights generated on the device):
   computes (the roots and every K/V cache entry bit-identical);
 * a root token past the vocabulary is reported at the first expansion;
 * page-table entries past n_pages and negative ones are reported ("page")
-  by verification, and a check after the report comes back clean;
+  by verification (the 16-row kernel, and the 32x32 kernel at the
+  16-sequence bf16 shape), and a check after the report comes back clean;
 * with debug off the same inputs report nothing.
 
 No oracle is involved: the property is the library's own.
@@ -108,5 +109,26 @@ def test_out_of_range_pages_are_reported():
     rt.device_check()               # debug off: nothing is reported
     rt.tpt.copy_(saved)
     rt.set_debug(True)
+    rt.verify()
+    rt.device_check()
+
+
+def test_out_of_range_pages_are_reported_by_the_32x32_kernel():
+    """The same at the 16-sequence bf16 shape (one target layer, weights
+    generated on the device), where verification runs the 32x32 kernel."""
+    w = synth.with_layers(synth.WORKLOADS["llama3-8b-batch16-paged"], 1)
+    rt = Runtime(w, None, seed=15)
+    rt.set_debug(True)
+    rt.prefill(synth.prompts(w))
+    for m in range(1, w.M + 1):
+        rt.expand(m)
+    rt.device_check()
+    saved = rt.tpt.clone()
+    rt.tpt[3, 0] = rt.tpt.numel() + 1
+    print("[debug] 32x32 verify over an out-of-range page-table entry",
+          flush=True)
+    rt.verify()
+    _expect_report(rt, "page-table entry")
+    rt.tpt.copy_(saved)
     rt.verify()
     rt.device_check()
