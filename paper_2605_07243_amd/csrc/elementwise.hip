@@ -281,14 +281,21 @@ __global__ __launch_bounds__(1024) void residual_kernel(
   }
 }
 
+namespace {
+thread_local bool g_rows_likely_empty = false;
+}  // namespace
+
+void set_rows_likely_empty(bool v) { g_rows_likely_empty = v; }
+bool rows_likely_empty() { return g_rows_likely_empty; }
+
 template <typename T>
 void launch_residual(float* x, const float* P, int ks, size_t part_stride,
                      const int* n, int cap, int d, bool accumulate,
                      const float* g, float eps, T* out, int ldo, float* taps,
                      int tap_mask, const int* out_row, hipStream_t st,
                      const float* add_rows, const int* add_idx) {
-  auto k = cap <= kEarlyRows ? residual_kernel<T, true>
-                             : residual_kernel<T, false>;
+  auto k = cap <= kEarlyRows && !g_rows_likely_empty ? residual_kernel<T, true>
+                                                     : residual_kernel<T, false>;
   k<<<cap, 1024, 0, st>>>(x, P, ks, part_stride, n, d, accumulate ? 1 : 0, g,
                           eps, out, ldo, taps, tap_mask, out_row, add_rows,
                           add_idx);
@@ -386,8 +393,9 @@ void launch_qkv_post(const float* P, int ks, size_t part_stride,
                      T* q, void* seg_k, void* seg_v, int seg_pages,
                      hipStream_t st) {
   const int items = (H + Hkv) * (hd / 8) + Hkv * (hd / 4);
-  auto k = p.cap <= kEarlyRows ? qkv_post_kernel<T, true>
-                               : qkv_post_kernel<T, false>;
+  auto k = p.cap <= kEarlyRows && !g_rows_likely_empty
+               ? qkv_post_kernel<T, true>
+               : qkv_post_kernel<T, false>;
   k<<<dim3(p.cap, (items + 255) / 256), 256, 0, st>>>(
       P, ks, part_stride, p, H, Hkv, hd, theta, q, (T*)seg_k, (T*)seg_v,
       seg_pages);

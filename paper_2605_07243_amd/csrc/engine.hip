@@ -985,12 +985,15 @@ int commit_impl(sb_ctx* c, sb_seqs* sq, const sb_tree* t,
   launch_commit_copy<T>(td, *t, *acc, c->ci, true, dp, D.S, D.LD, D.Hkv, D.hd,
                         st);
   // catch-up rows where the tree has no row continuing the accepted path
+  // (usually none: its launches test the live count before loading)
+  set_rows_likely_empty(true);
   cond_rows<T>(c, v->taps, c->taps_idx, c->n_aux, D.S, st);
   const Prefix pf{dkv, c->dseg_k, c->dseg_v, D.dpages};
   CallPlan fb = c->fb;
   fb.n_seqs = sq->n_seqs;
   fb.cap = sq->n_seqs;
   drafter_forward<T>(c, fb, c->cond_buf, pf, 1, false, st);
+  set_rows_likely_empty(false);
   launch_seg_to_cache<T>(fb, dp, D.S, D.LD, D.Hkv, D.hd, st);
   launch_commit_state(td, *sq, *acc, c->ci, v->taps, st);
   if (c->T_bound > 0) c->T_bound += D.M * D.K + 1;

@@ -221,10 +221,11 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(
   // load in flight past the end of the program).  The empty asm with a
   // memory clobber keeps the compiler from sinking the loads below the exit
   // test, past which alone their results are used (W and X are not
-  // __restrict__ for the same reason).  With several row tiles (many rows, long
-  // MFMA-bound launches) the count is waited for first and the rows past
-  // it repeat row M - 1, as issuing early measured slower there.
-  const bool early = n_mt == 1;
+  // __restrict__ for the same reason).  With several row tiles (many rows,
+  // long MFMA-bound launches) the count is waited for first and the rows
+  // past it repeat row M - 1, as issuing early measured slower there; so
+  // too with x_rows = 0 (launches whose rows are usually none).
+  const bool early = n_mt == 1 && x_rows > 0;
   if (!early && m_base >= M) return;  // whole workgroup
   const int row_lim = early ? x_rows : M;
   const bf16_t* xp[MF];
@@ -673,7 +674,7 @@ void launch_tile(const GemmPlan& g, const bf16_t* X, int ldx, const bf16_t* W,
     hipExtLaunchKernelGGL(gemm_tile_kernel<MF_, NF_, PF_, SWIGLU, VR>, grid,  \
                           dim3(256), 0, st, ea, eb, 0, X, ldx, W, K, P, N,    \
                           part_stride, m_count, k_chunk, n_mt, n_nt, act, F,  \
-                          rec, n_first, m_cap);                               \
+                          rec, n_first, rows_likely_empty() ? 0 : m_cap);     \
     return;                                                                   \
   }
   SB_LAUNCH(1, 1, 2)

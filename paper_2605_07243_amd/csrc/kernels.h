@@ -192,6 +192,13 @@ void launch_verify_finalize(const float* part, int n_chunks, const int* n,
                             hipStream_t st);
 
 // Tree kernels.
+// Launches of a forward whose rows are usually all past the live count
+// (the catch-up rows of a commit): while set (per host thread), the
+// few-row GEMM, residual and RoPE launches test the count before loading
+// anything, so that an empty launch exits at once.
+void set_rows_likely_empty(bool v);
+bool rows_likely_empty();
+
 // Debug status bits (sb_device_check): a caller-supplied page-table entry
 // or token id was outside its range and was clamped into it.
 constexpr int kDevPage = 1, kDevToken = 2;
