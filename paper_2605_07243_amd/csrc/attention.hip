@@ -790,7 +790,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn32_kernel(
 // partial loads are issued before the (m, l) loads and the weights, so a
 // row of up to 4 BT columns costs one memory round trip.
 template <int NS>
-constexpr int merge_threads() { return NS <= 8 ? 1024 : 512; }
+constexpr int merge_threads() { return NS <= 16 ? 1024 : 512; }
 
 template <int NS>
 __global__ __launch_bounds__(merge_threads<NS>()) void attn_merge_kernel_t(
