@@ -409,10 +409,10 @@ int sb_set_length_bound(sb_ctx* ctx, int32_t max_T);
  * of sb_seqs.root.  Every such read is clamped into range (page to
  * 0 .. n_pages - 1, token to 0 .. vocab - 1), so a bad value never reads or
  * writes outside the pools or the embedding table; it silently computes on
- * the clamped index instead.  sb_set_debug(ctx, 1) clears the context's
- * device status word and makes the kernels of later calls set a bit in it
- * for every clamp (one atomic per clamped read; nothing when inputs are in
- * range); sb_set_debug(ctx, 0) stops reporting.  sb_device_check returns
+ * the clamped index instead.  sb_set_debug(ctx, 1) waits for the device,
+ * clears the context's status word and makes the kernels of later calls
+ * set a bit in it for every clamp (one atomic per clamped read; nothing
+ * when inputs are in range); sb_set_debug(ctx, 0) stops reporting.  sb_device_check returns
  * SB_OK at once if sb_set_debug has not been called since sb_bind (the
  * word is not cleared at bind, which touches no device memory); otherwise
  * it waits for `stream`, reads the word and, if it is not zero, clears it

@@ -1409,7 +1409,10 @@ int sb_set_length_bound(sb_ctx* c, int32_t max_T) {
 int sb_set_debug(sb_ctx* c, int32_t on) {
   if (!c) return SB_EINVAL;
   if (!c->bound) return fail(c, SB_ESTATE, "context not bound (call sb_bind)");
-  if (hipMemset(c->dev_status, 0, sizeof(int)) != hipSuccess)
+  // kernels of earlier calls (on any stream) finish before the word is
+  // cleared, so that none of them sets a bit after it
+  if (hipDeviceSynchronize() != hipSuccess ||
+      hipMemset(c->dev_status, 0, sizeof(int)) != hipSuccess)
     return fail(c, SB_EHIP, "clearing the debug status word failed");
   c->status_live = true;
   c->debug = on != 0;
